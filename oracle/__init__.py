@@ -1,0 +1,235 @@
+"""Plain fp64 CPU oracle for the QTEA compressed ternary GEMV.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg are the only callers.  The GPU library never imports,
+links or runs anything here, and this package never imports the GPU
+library.  The arithmetic lives in ``qtea_oracle.c`` (plain C loops, fp64);
+this module only marshals numpy arrays through ctypes.
+
+Pins (tests/test_oracle.py): exhaustive code round trip, sign-symmetry and
+zero-pattern closed forms, hand-worked example (tests/golden), brute force
+in exact rational arithmetic on tiny inputs, textbook special cases, the
+paper's bits-per-weight figures.  Every function is pinned; none is marked
+"parity unpinned".
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "qtea_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+OK, ERR_ARG, ERR_TRIT, ERR_CODE, ERR_RESID, ERR_NOMEM = 0, -1, -2, -3, -4, -5
+
+
+class OracleError(RuntimeError):
+    def __init__(self, rc, what):
+        super().__init__(f"oracle {what} failed with status {rc}")
+        self.rc = rc
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain C, OpenMP over rows)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-std=c11", "-fno-fast-math",
+             "-ffp-contract=off", "-o", tmp, _SRC, "-lm"]
+        )
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        i64, i32, vp, dbl = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_double
+        lib.or_half_to_double.restype = dbl
+        lib.or_half_to_double.argtypes = [ctypes.c_uint16]
+        lib.or_num_packs.restype = i64
+        lib.or_num_packs.argtypes = [i64]
+        lib.or_encode5.restype = i32
+        lib.or_encode5.argtypes = [vp]
+        lib.or_decode_code.restype = i32
+        lib.or_decode_code.argtypes = [i32, vp]
+        lib.or_pack.restype = i32
+        lib.or_pack.argtypes = [vp, i64, i64, vp]
+        lib.or_unpack.restype = i32
+        lib.or_unpack.argtypes = [vp, i64, i64, vp]
+        lib.or_check_salient.restype = i32
+        lib.or_check_salient.argtypes = [vp, i64, i64]
+        lib.or_resid_rows.restype = i32
+        lib.or_resid_rows.argtypes = [vp, i64, i64, vp]
+        lib.or_dense_rows.restype = i32
+        lib.or_dense_rows.argtypes = [i64, i64, vp, vp, i64, vp, vp, vp, i64, vp, vp, vp]
+        lib.or_gemv_rows.restype = i32
+        lib.or_gemv_rows.argtypes = [i64, i64, vp, vp, i64, vp, vp, vp, i64, vp, vp, vp, i64, vp, i32]
+        lib.or_gemv_lut_rows.restype = i32
+        lib.or_gemv_lut_rows.argtypes = [i64, i64, vp, vp, i64, vp, vp, vp, i64, vp, vp, vp, i64, vp]
+        lib.or_bpw_full.restype = dbl
+        lib.or_bpw_full.argtypes = [i64, i64, i64]
+        lib.or_bpw_paper.restype = dbl
+        lib.or_bpw_paper.argtypes = [dbl, dbl]
+        lib.or_algorithmic_bytes.restype = i64
+        lib.or_algorithmic_bytes.argtypes = [i64, i64, i64]
+        _lib = lib
+    return _lib
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _bits16(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.float16:
+        return a.view(np.uint16)
+    return _c(a, np.uint16)
+
+
+def threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def half_to_double(h: int) -> float:
+    return float(_L().or_half_to_double(int(h) & 0xFFFF))
+
+
+def num_packs(K: int) -> int:
+    return int(_L().or_num_packs(K))
+
+
+def encode5(t) -> int:
+    t = _c(t, np.int8)
+    assert t.size == 5
+    return int(_L().or_encode5(t.ctypes.data))
+
+
+def decode_code(c: int):
+    t = np.zeros(5, dtype=np.int8)
+    rc = _L().or_decode_code(int(c), t.ctypes.data)
+    if rc:
+        raise OracleError(rc, "decode_code")
+    return t
+
+
+def pack(trits) -> np.ndarray:
+    t = _c(trits, np.int8)
+    n, K = t.shape
+    out = np.empty((n, num_packs(K)), dtype=np.uint8)
+    rc = _L().or_pack(t.ctypes.data, n, K, out.ctypes.data)
+    if rc:
+        raise OracleError(rc, "pack")
+    return out
+
+
+def unpack(codes, K: int) -> np.ndarray:
+    c = _c(codes, np.uint8)
+    n = c.shape[0]
+    if c.shape[1] != num_packs(K):
+        raise ValueError("code row length must be ceil(K/5)")
+    out = np.empty((n, K), dtype=np.int8)
+    rc = _L().or_unpack(c.ctypes.data, n, K, out.ctypes.data)
+    if rc:
+        raise OracleError(rc, "unpack")
+    return out
+
+
+def check_salient(S, K: int) -> int:
+    S = _c(S, np.int32)
+    return int(_L().or_check_salient(S.ctypes.data, S.size, K))
+
+
+def resid_rows(idx, N: int) -> np.ndarray:
+    idx = _c(idx, np.uint8)
+    nS = idx.shape[0]
+    out = np.empty((nS, N // 4), dtype=np.int32)
+    rc = _L().or_resid_rows(idx.ctypes.data, nS, N, out.ctypes.data)
+    if rc:
+        raise OracleError(rc, "resid_rows")
+    return out
+
+
+def _layer_args(N, K, alpha, v, S, R, idx):
+    alpha, v = _bits16(alpha), _bits16(v)
+    S = _c(S, np.int32)
+    nS = S.size
+    R = _bits16(R).reshape(nS, N // 4) if nS else np.zeros((0, N // 4), np.uint16)
+    idx = _c(idx, np.uint8).reshape(nS, N // 4) if nS else np.zeros((0, N // 4), np.uint8)
+    assert alpha.size == N and v.size == K
+    keep = (alpha, v, S, R, idx)
+    return keep, [alpha.ctypes.data, v.ctypes.data, S.ctypes.data, nS, R.ctypes.data, idx.ctypes.data]
+
+
+def _rows_args(N, K, codes_rows, rows):
+    rows = np.arange(N, dtype=np.int64) if rows is None else _c(rows, np.int64)
+    P = _c(codes_rows, np.uint8)
+    if P.shape != (rows.size, num_packs(K)):
+        raise ValueError(f"codes_rows must be [{rows.size}][{num_packs(K)}], got {P.shape}")
+    return P, rows
+
+
+def dense_rows(N, K, codes_rows, alpha, v, S, R, idx, rows=None) -> np.ndarray:
+    """fp64 dequantized rows (alpha_r v_j T_rj plus the stored residuals)."""
+    P, rows = _rows_args(N, K, codes_rows, rows)
+    keep, la = _layer_args(N, K, alpha, v, S, R, idx)
+    W = np.empty((rows.size, K), dtype=np.float64)
+    rc = _L().or_dense_rows(N, K, P.ctypes.data, rows.ctypes.data, rows.size, *la, W.ctypes.data)
+    if rc:
+        raise OracleError(rc, "dense_rows")
+    return W
+
+
+def gemv(N, K, codes_rows, alpha, v, S, R, idx, x, rows=None, nthreads=None) -> np.ndarray:
+    """fp64 y[b][i] for output rows `rows` (default: all rows)."""
+    P, rows = _rows_args(N, K, codes_rows, rows)
+    keep, la = _layer_args(N, K, alpha, v, S, R, idx)
+    x = _bits16(x).reshape(-1, K)
+    B = x.shape[0]
+    y = np.empty((B, rows.size), dtype=np.float64)
+    rc = _L().or_gemv_rows(N, K, P.ctypes.data, rows.ctypes.data, rows.size, *la, x.ctypes.data,
+                           B, y.ctypes.data, int(nthreads or threads()))
+    if rc:
+        raise OracleError(rc, "gemv")
+    return y
+
+
+def gemv_lut(N, K, codes_rows, alpha, v, S, R, idx, x, rows=None) -> np.ndarray:
+    """fp64 y through per-pack 243-entry tables (same result as gemv)."""
+    P, rows = _rows_args(N, K, codes_rows, rows)
+    keep, la = _layer_args(N, K, alpha, v, S, R, idx)
+    x = _bits16(x).reshape(-1, K)
+    B = x.shape[0]
+    y = np.empty((B, rows.size), dtype=np.float64)
+    rc = _L().or_gemv_lut_rows(N, K, P.ctypes.data, rows.ctypes.data, rows.size, *la,
+                               x.ctypes.data, B, y.ctypes.data)
+    if rc:
+        raise OracleError(rc, "gemv_lut")
+    return y
+
+
+def bpw_full(N, K, nS) -> float:
+    return float(_L().or_bpw_full(N, K, nS))
+
+
+def bpw_paper(f, value_bits) -> float:
+    return float(_L().or_bpw_paper(float(f), float(value_bits)))
+
+
+def algorithmic_bytes(N, K, nS) -> int:
+    return int(_L().or_algorithmic_bytes(N, K, nS))
