@@ -1,0 +1,166 @@
+/*
+ * qtea.h - C ABI of the MI355X (gfx950) compressed ternary GEMV library.
+ *
+ * The operation (paper: "Efficient Ternary Computation", Eq. 10 with one
+ * quantization group spanning all K input columns and zero bias, plus the
+ * salient residual of Eq. 11):
+ *
+ *   y[b][r] = alpha_r * sum_{j<K} T[r][j] * v_j * x[b][j]
+ *           + sum_{s<nS} [r == 4g + idx[s][g], g = r/4] * R[s][g] * x[b][S_s]
+ *
+ * T[r][j] in {-1, 0, +1} are ternary codes (stored five per byte in base 3,
+ * "3^5 < 2^8"), alpha_r a per-output-row fp16 scale, v_j a per-input-column
+ * fp16 rescale (folded into the activations, as the paper fuses v_j x_j into
+ * the table precompute), S the sorted salient input columns and, in each
+ * salient column, one fp16 residual R[s][g] per group g of four consecutive
+ * output rows at in-group position idx[s][g] in 0..3 (the paper's 1:4
+ * semi-structured residual with a 2-bit local index).  The residual is
+ * scaled by neither alpha nor v.  Weight orientation is nn.Linear's:
+ * W is N (out) x K (in), y = W x.
+ *
+ * Conventions for every entry point:
+ *   - All pointers named "device" are HIP device pointers owned by the
+ *     caller.  The library never allocates or frees memory and keeps no
+ *     global state; every entry point is reentrant.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Device work is
+ *     enqueued on it and is stream-ordered with the caller's other work.
+ *     Only qtea_pack synchronizes the stream (to return its validation
+ *     result); the GEMV entry points never synchronize.
+ *   - Return value: QTEA_OK (0) or a negative QTEA_ERR_* code; no exception
+ *     crosses the ABI.  On an argument error nothing is enqueued.
+ *   - fp16 values are passed as their IEEE binary16 bit patterns (uint16_t).
+ *   - y / Y are fully overwritten (not accumulated into).  Outputs must not
+ *     alias any input.
+ */
+#ifndef QTEA_H_
+#define QTEA_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QTEA_ABI_VERSION 1
+#define QTEA_MAX_BATCH 16
+
+enum qtea_status {
+  QTEA_OK = 0,
+  QTEA_ERR_INVALID_ARG = -1, /* null pointer, bad size, bad descriptor      */
+  QTEA_ERR_BAD_TRIT = -2,    /* a trit outside {-1, 0, +1}                   */
+  QTEA_ERR_BAD_RESIDUAL = -3,/* idx > 3, or S not strictly increasing in [0,K) */
+  QTEA_ERR_BATCH = -4,       /* batch outside [1, QTEA_MAX_BATCH]            */
+  QTEA_ERR_WORKSPACE = -5,   /* workspace or packed buffer too small         */
+  QTEA_ERR_HIP = -6,         /* a HIP runtime call or kernel launch failed   */
+};
+
+/*
+ * Host-side description of one packed matrix.  Filled by qtea_pack, owned
+ * by the caller, read by the other entry points.  The packed device buffer
+ * it describes is opaque: its tiling is private to the library and may
+ * change between library versions (`layout` records which one).
+ */
+typedef struct qtea_desc {
+  uint32_t magic;       /* QTEA_DESC_MAGIC when valid                        */
+  uint32_t layout;      /* device layout version                             */
+  int64_t N, K;         /* output rows, input columns                        */
+  int64_t n_salient;    /* |S|                                               */
+  int64_t n_packs;      /* ceil(K / 5) one-byte packs per row                */
+  int64_t n_groups;     /* ceil(n_packs / 16) sixteen-pack groups            */
+  int64_t n_pad;        /* N rounded up to a multiple of 64                  */
+  int64_t bytes_total;  /* size of the packed buffer in bytes                */
+  int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx;
+} qtea_desc;
+
+#define QTEA_DESC_MAGIC 0x51544541u /* "QTEA" */
+
+/* Text for a status code (static storage; never NULL). */
+const char* qtea_status_string(int status);
+
+/* Library ABI version (QTEA_ABI_VERSION of the built library). */
+int qtea_abi_version(void);
+
+/*
+ * Size of the packed device buffer for an N x K matrix with n_salient
+ * salient columns.  Requires N >= 4, N % 4 == 0 (four-row residual groups),
+ * K >= 1, 0 <= n_salient <= K.  Writes *out_bytes.
+ */
+int qtea_packed_bytes(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes);
+
+/*
+ * Pack dense inputs into the device layout (paper: five trits per byte in
+ * base 3; per-row scale; per-column rescale; salient residual with one value
+ * and a 2-bit position per four entries).  Offline: synchronizes `stream`.
+ *
+ *   trits       device int8  [N][K], row-major, values in {-1, 0, +1}
+ *   row_scale   device fp16  [N]       alpha
+ *   col_rescale device fp16  [K]       v
+ *   salient     device int32 [n_salient], strictly increasing, in [0, K)
+ *   resid_val   device fp16  [n_salient][N/4]   R[s][g]
+ *   resid_idx   device uint8 [n_salient][N/4]   position of R[s][g] in rows 4g..4g+3
+ *   packed      device buffer of packed_bytes >= qtea_packed_bytes(...)
+ *   out_desc    host; filled on success
+ *
+ * Byte code of columns 5p..5p+4 of a row: sum_i (T[r][5p+i] + 1) * 3^i, with
+ * the zero trit in place of columns >= K.  The salient/residual pointers may
+ * be NULL when n_salient == 0.
+ * Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_WORKSPACE (packed buffer too small),
+ * QTEA_ERR_BAD_TRIT, QTEA_ERR_BAD_RESIDUAL (checked on the device; *out_desc
+ * is left invalid), QTEA_ERR_HIP.
+ */
+int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
+              const uint16_t* col_rescale, const int32_t* salient, int64_t n_salient,
+              const uint16_t* resid_val, const uint8_t* resid_idx, void* packed,
+              int64_t packed_bytes, qtea_desc* out_desc, void* stream);
+
+/*
+ * Workspace bytes that qtea_gemv (batch = 1) / qtea_gemm_lowbatch need for
+ * this matrix at this batch size.  The workspace holds per-K-slice partial
+ * sums and per-row-block arrival counters.  It must be zero-filled before
+ * its first use (qtea_workspace_init or any zero fill); every call that
+ * runs to completion leaves the counters at zero again, so one workspace
+ * serves any sequence of stream-ordered calls.  Calls that may overlap in
+ * time must not share a workspace.
+ */
+int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes);
+
+/* Enqueue a zero fill of `bytes` bytes of `workspace` (a kernel, not a
+ * memset node, so it is safe inside captured graphs). */
+int qtea_workspace_init(void* workspace, int64_t bytes, void* stream);
+
+/*
+ * y = W x for one activation vector (batch 1).
+ *   packed      device buffer filled by qtea_pack for *desc
+ *   x           device fp16 [K]
+ *   y           device fp32 [N]
+ *   workspace   device, >= qtea_workspace_bytes(desc, 1), see above
+ * fp32 accumulation; results are run-to-run deterministic (fixed reduction
+ * order).  Identical to qtea_gemm_lowbatch with batch 1.
+ */
+int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y,
+              void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Y = X W^T for 1 <= batch <= QTEA_MAX_BATCH activation rows (low-batch
+ * decode: one token per row).
+ *   X  device fp16 [batch][K] row-major;  Y  device fp32 [batch][N] row-major.
+ * Errors as qtea_gemv plus QTEA_ERR_BATCH.
+ */
+int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
+                       float* Y, void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Test support: read the packed buffer back into plain form, bit for bit.
+ *   canon_codes device uint8 [N][n_packs]  canonical byte codes (or NULL)
+ *   trits       device int8  [N][K]        decoded trits          (or NULL)
+ *   resid_row   device int32 [n_salient][N/4] output row 4g + idx (or NULL)
+ * Does not synchronize.
+ */
+int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_codes,
+                      int8_t* trits, int32_t* resid_row, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QTEA_H_ */

@@ -1,0 +1,233 @@
+"""MI355X (gfx950) compressed ternary GEMV: Python binding of libqtea.so.
+
+The binding marshals arguments only: every step of the GEMV runs in the HIP
+kernels of ``csrc/qtea.hip`` behind the C ABI of ``include/qtea.h``.  Torch
+is used to allocate device memory and to name the current HIP stream.
+There is no CPU fallback: if the library is not built, loading it raises.
+
+Entry points carry the C names: qtea_packed_bytes, qtea_pack,
+qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
+qtea_debug_unpack, qtea_status_string, qtea_abi_version.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libqtea.so")
+
+QTEA_OK = 0
+QTEA_ERR_INVALID_ARG = -1
+QTEA_ERR_BAD_TRIT = -2
+QTEA_ERR_BAD_RESIDUAL = -3
+QTEA_ERR_BATCH = -4
+QTEA_ERR_WORKSPACE = -5
+QTEA_ERR_HIP = -6
+QTEA_MAX_BATCH = 16
+QTEA_DESC_MAGIC = 0x51544541
+
+# Every function the header declares (checked by tests/test_abi.py).
+EXPORTS = (
+    "qtea_status_string", "qtea_abi_version", "qtea_packed_bytes", "qtea_pack",
+    "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
+    "qtea_debug_unpack",
+)
+
+
+class QteaDesc(ctypes.Structure):
+    """Mirror of struct qtea_desc (include/qtea.h)."""
+    _fields_ = [
+        ("magic", ctypes.c_uint32), ("layout", ctypes.c_uint32),
+        ("N", ctypes.c_int64), ("K", ctypes.c_int64), ("n_salient", ctypes.c_int64),
+        ("n_packs", ctypes.c_int64), ("n_groups", ctypes.c_int64), ("n_pad", ctypes.c_int64),
+        ("bytes_total", ctypes.c_int64),
+        ("off_trits", ctypes.c_int64), ("off_alpha", ctypes.c_int64), ("off_v", ctypes.c_int64),
+        ("off_salient", ctypes.c_int64), ("off_spos", ctypes.c_int64), ("off_rval", ctypes.c_int64),
+        ("off_ridx", ctypes.c_int64),
+    ]
+
+
+class QteaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {qtea_status_string(status)} ({status})")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built (run __graft_entry__.build()); "
+                          "there is no fallback path")
+    lib = ctypes.CDLL(path)
+    i64, i32, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+    pdesc = ctypes.POINTER(QteaDesc)
+    lib.qtea_status_string.restype = ctypes.c_char_p
+    lib.qtea_status_string.argtypes = [i32]
+    lib.qtea_abi_version.restype = i32
+    lib.qtea_abi_version.argtypes = []
+    lib.qtea_packed_bytes.restype = i32
+    lib.qtea_packed_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(i64)]
+    lib.qtea_pack.restype = i32
+    lib.qtea_pack.argtypes = [vp, i64, i64, vp, vp, vp, i64, vp, vp, vp, i64, pdesc, vp]
+    lib.qtea_workspace_bytes.restype = i32
+    lib.qtea_workspace_bytes.argtypes = [pdesc, i32, ctypes.POINTER(i64)]
+    lib.qtea_workspace_init.restype = i32
+    lib.qtea_workspace_init.argtypes = [vp, i64, vp]
+    lib.qtea_gemv.restype = i32
+    lib.qtea_gemv.argtypes = [pdesc, vp, vp, vp, vp, i64, vp]
+    lib.qtea_gemm_lowbatch.restype = i32
+    lib.qtea_gemm_lowbatch.argtypes = [pdesc, vp, vp, i32, vp, vp, i64, vp]
+    lib.qtea_debug_unpack.restype = i32
+    lib.qtea_debug_unpack.argtypes = [pdesc, vp, vp, vp, vp, vp]
+    _lib = lib
+    return lib
+
+
+def _stream(stream=None):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check(status: int, what: str):
+    if status != QTEA_OK:
+        raise QteaError(status, what)
+
+
+def _need_cuda(*tensors):
+    for t in tensors:
+        if t is not None and not t.is_cuda:
+            raise ValueError("qtea entry points take device tensors")
+        if t is not None and not t.is_contiguous():
+            raise ValueError("qtea entry points take contiguous tensors")
+
+
+# ---------------------------------------------------------------------------
+# Entry points (same names as the C ABI).
+# ---------------------------------------------------------------------------
+def qtea_status_string(status: int) -> str:
+    return load().qtea_status_string(int(status)).decode()
+
+
+def qtea_abi_version() -> int:
+    return int(load().qtea_abi_version())
+
+
+def qtea_packed_bytes(N: int, K: int, n_salient: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().qtea_packed_bytes(N, K, n_salient, ctypes.byref(out)), "qtea_packed_bytes")
+    return out.value
+
+
+def qtea_pack(trits, row_scale, col_rescale, salient, resid_val, resid_idx, packed,
+              stream=None) -> QteaDesc:
+    """Pack device tensors (int8 [N][K], fp16 [N], fp16 [K], int32 [nS],
+    fp16 [nS][N/4], uint8 [nS][N/4]) into `packed` (uint8, >= qtea_packed_bytes)."""
+    import torch
+
+    _need_cuda(trits, row_scale, col_rescale, salient, resid_val, resid_idx, packed)
+    assert trits.dtype == torch.int8 and row_scale.dtype == torch.float16
+    assert col_rescale.dtype == torch.float16 and salient.dtype == torch.int32
+    assert resid_val.dtype == torch.float16 and resid_idx.dtype == torch.uint8
+    N, K = trits.shape
+    nS = salient.numel()
+    d = QteaDesc()
+    st = load().qtea_pack(_ptr(trits), N, K, _ptr(row_scale), _ptr(col_rescale),
+                          _ptr(salient) if nS else None, nS,
+                          _ptr(resid_val) if nS else None, _ptr(resid_idx) if nS else None,
+                          _ptr(packed), packed.numel() * packed.element_size(), ctypes.byref(d),
+                          _stream(stream))
+    _check(st, "qtea_pack")
+    return d
+
+
+def qtea_workspace_bytes(desc: QteaDesc, batch: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().qtea_workspace_bytes(ctypes.byref(desc), int(batch), ctypes.byref(out)),
+           "qtea_workspace_bytes")
+    return out.value
+
+
+def qtea_workspace_init(workspace, stream=None):
+    _need_cuda(workspace)
+    _check(load().qtea_workspace_init(_ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(stream)), "qtea_workspace_init")
+
+
+def qtea_gemv(desc: QteaDesc, packed, x, y, workspace, stream=None):
+    _need_cuda(packed, x, y, workspace)
+    _check(load().qtea_gemv(ctypes.byref(desc), _ptr(packed), _ptr(x), _ptr(y), _ptr(workspace),
+                            workspace.numel() * workspace.element_size(), _stream(stream)),
+           "qtea_gemv")
+
+
+def qtea_gemm_lowbatch(desc: QteaDesc, packed, X, batch: int, Y, workspace, stream=None):
+    _need_cuda(packed, X, Y, workspace)
+    _check(load().qtea_gemm_lowbatch(ctypes.byref(desc), _ptr(packed), _ptr(X), int(batch), _ptr(Y),
+                                     _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                     _stream(stream)), "qtea_gemm_lowbatch")
+
+
+def qtea_debug_unpack(desc: QteaDesc, packed, canon_codes=None, trits=None, resid_row=None,
+                      stream=None):
+    _need_cuda(packed, canon_codes, trits, resid_row)
+    _check(load().qtea_debug_unpack(ctypes.byref(desc), _ptr(packed), _ptr(canon_codes), _ptr(trits),
+                                    _ptr(resid_row), _stream(stream)), "qtea_debug_unpack")
+
+
+# ---------------------------------------------------------------------------
+# Convenience: one packed matrix with its own device buffer.
+# ---------------------------------------------------------------------------
+@dataclass
+class PackedMatrix:
+    desc: QteaDesc
+    packed: object  # torch uint8 device tensor
+
+    @property
+    def N(self):
+        return self.desc.N
+
+    @property
+    def K(self):
+        return self.desc.K
+
+
+def pack_matrix(trits, alpha, v, S, R, idx, stream=None) -> PackedMatrix:
+    """Allocate the packed buffer and pack (all arguments device tensors)."""
+    import torch
+
+    N, K = trits.shape
+    nbytes = qtea_packed_bytes(N, K, S.numel())
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=trits.device)
+    d = qtea_pack(trits, alpha, v, S, R, idx, packed, stream=stream)
+    return PackedMatrix(d, packed)
+
+
+def new_workspace(desc: QteaDesc, batch: int, device="cuda"):
+    """A zero-filled workspace for this matrix and batch size."""
+    import torch
+
+    n = qtea_workspace_bytes(desc, batch)
+    return torch.zeros(max(n, 4), dtype=torch.uint8, device=device)
+
+
+def algorithmic_bytes(N: int, K: int, n_salient: int) -> int:
+    """Weight bytes one GEMV must read in the paper's format: packed trits
+    (ceil(K/5) bytes per row), fp16 residual values plus 2-bit positions for
+    one entry per four rows of each salient column, fp16 alpha and v, and
+    the int32 salient list."""
+    entries = (N // 4) * n_salient
+    return N * ((K + 4) // 5) + 2 * entries + (2 * entries + 7) // 8 + 2 * N + 2 * K + 4 * n_salient

@@ -1,0 +1,835 @@
+// Compressed ternary GEMV for gfx950: packing, the lookup-table GEMV and
+// the C ABI declared in include/qtea.h.
+//
+// Device layout (layout version 1), all regions 256-byte aligned:
+//   header   256 B: magic, layout, sizes; a validation flag word at +128.
+//   trits    [n_pad/64 tiles][n_groups][64 rows][16 bytes]
+//            One 16-byte unit holds the sixteen packs of one 16-pack group
+//            for one row; a wavefront (64 lanes = 64 rows of a tile) reads
+//            1 KiB contiguous per 128-bit load.  Byte i of the unit of row r
+//            holds pack 16*g + ((i + r) mod 16): rows are rotated so that at
+//            step i the 16 lanes of a quarter-wave address 16 different
+//            packs' table columns (distinct LDS banks).
+//   alpha    fp16 [n_pad]              (zero in the row padding)
+//   v        fp16 [n_groups * 80]      (zero in the column padding)
+//   salient  int32 [n_salient]
+//   spos     int32 [n_groups + 1]      first s with S_s >= 80 * g
+//   rval     fp16 [n_salient][n_pad/4] residual of four-row group g
+//   ridx     u32  [n_salient][n_pad/64] 2-bit positions, 16 groups per word
+//
+// GEMV (one launch): workgroup = (row block, K slice).  For each chunk of
+// 16-pack groups of its slice it computes a_j = v_j x_j, builds the 243-entry
+// table of every pack of the chunk in LDS, then each lane (one output row)
+// streams its row's packed bytes and adds one table entry per byte.  The
+// salient residual of the slice's columns is added in the same pass.  The
+// slice partials go to the workspace; the last workgroup of a row block to
+// arrive sums them in slice order (deterministic) and writes y.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "qtea.h"
+
+namespace {
+
+constexpr int kGroupPacks = 16;
+constexpr int kGroupCols = 80;   // 16 packs x 5 columns
+constexpr int kTileRows = 64;    // one row per lane of a wavefront
+constexpr int kCodes = 243;      // 3^5
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr uint32_t kZeroCode4 = 0x79797979u;  // four copies of code 121 (all-zero trits)
+constexpr int kLayout = 1;
+constexpr int64_t kAlign = 256;
+constexpr int64_t kHeaderBytes = 256;
+constexpr int kFlagOffset = 128;
+
+constexpr uint32_t kFlagBadTrit = 1u;
+constexpr uint32_t kFlagBadResid = 2u;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+__device__ __forceinline__ float h2f(uint16_t h) {
+  _Float16 v;
+  __builtin_memcpy(&v, &h, 2);
+  return (float)v;
+}
+
+// ---------------------------------------------------------------------------
+// Layout arithmetic shared by the host entry points.
+// ---------------------------------------------------------------------------
+struct Layout {
+  int64_t n_packs, n_groups, n_pad, n_tiles;
+  int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx, total;
+};
+
+bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L) {
+  if (N < 4 || N % 4 != 0 || K < 1 || nS < 0 || nS > K) return false;
+  if (N > (int64_t(1) << 31) - 64 || K > (int64_t(1) << 31) - 80) return false;
+  L->n_packs = cdiv(K, 5);
+  L->n_groups = cdiv(L->n_packs, kGroupPacks);
+  L->n_pad = align_up(N, kTileRows);
+  L->n_tiles = L->n_pad / kTileRows;
+  int64_t o = kHeaderBytes;
+  L->off_trits = o;
+  o = align_up(o + L->n_pad * L->n_groups * kGroupPacks, kAlign);
+  L->off_alpha = o;
+  o = align_up(o + 2 * L->n_pad, kAlign);
+  L->off_v = o;
+  o = align_up(o + 2 * L->n_groups * kGroupCols, kAlign);
+  L->off_salient = o;
+  o = align_up(o + 4 * nS, kAlign);
+  L->off_spos = o;
+  o = align_up(o + 4 * (L->n_groups + 1), kAlign);
+  L->off_rval = o;
+  o = align_up(o + 2 * nS * (L->n_pad / 4), kAlign);
+  L->off_ridx = o;
+  o = align_up(o + 4 * nS * (L->n_pad / 64), kAlign);
+  L->total = o;
+  return true;
+}
+
+bool desc_ok(const qtea_desc* d) {
+  if (!d || d->magic != QTEA_DESC_MAGIC || d->layout != kLayout) return false;
+  Layout L;
+  if (!make_layout(d->N, d->K, d->n_salient, &L)) return false;
+  return L.total == d->bytes_total && L.off_trits == d->off_trits && L.off_alpha == d->off_alpha &&
+         L.off_v == d->off_v && L.off_salient == d->off_salient && L.off_spos == d->off_spos &&
+         L.off_rval == d->off_rval && L.off_ridx == d->off_ridx && L.n_pad == d->n_pad &&
+         L.n_groups == d->n_groups && L.n_packs == d->n_packs;
+}
+
+// ---------------------------------------------------------------------------
+// Packing kernels (offline).
+// ---------------------------------------------------------------------------
+__global__ void validate_kernel(const int8_t* __restrict__ trits, int64_t nt,
+                                const uint8_t* __restrict__ ridx, int64_t ni,
+                                const int32_t* __restrict__ S, int64_t nS, int64_t K,
+                                uint32_t* __restrict__ flags) {
+  uint32_t f = 0;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < nt; i += stride) {
+    const int8_t t = trits[i];
+    if (t < -1 || t > 1) f |= kFlagBadTrit;
+  }
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < ni; i += stride)
+    if (ridx[i] > 3) f |= kFlagBadResid;
+  for (int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; s < nS; s += stride) {
+    const int32_t c = S[s];
+    if (c < 0 || c >= K || (s > 0 && c <= S[s - 1])) f |= kFlagBadResid;
+  }
+  if (f) atomicOr(flags, f);
+}
+
+// One thread per 16-byte unit (tile, group, row-in-tile).
+__global__ void pack_trits_kernel(const int8_t* __restrict__ trits, int64_t N, int64_t K,
+                                  int64_t n_groups, int64_t n_units, uint8_t* __restrict__ out) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < n_units; u += stride) {
+    const int64_t l = u % kTileRows;
+    const int64_t g = (u / kTileRows) % n_groups;
+    const int64_t tile = u / (kTileRows * n_groups);
+    const int64_t r = tile * kTileRows + l;
+    uint32_t w[4] = {kZeroCode4, kZeroCode4, kZeroCode4, kZeroCode4};
+    if (r < N) {
+      const int8_t* row = trits + r * K;
+      for (int i = 0; i < kGroupPacks; ++i) {
+        const int64_t p = g * kGroupPacks + ((i + l) & (kGroupPacks - 1));
+        uint32_t code = 0, pw = 1;
+        for (int e = 0; e < 5; ++e) {
+          const int64_t j = 5 * p + e;
+          int t = j < K ? row[j] : 0;
+          t = t < -1 ? -1 : (t > 1 ? 1 : t);  // invalid input is reported by validate_kernel
+          code += uint32_t(t + 1) * pw;
+          pw *= 3;
+        }
+        const int sh = 8 * (i & 3);
+        w[i >> 2] = (w[i >> 2] & ~(0xffu << sh)) | (code << sh);
+      }
+    }
+    const u32x4 v = {w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<u32x4*>(out + u * 16) = v;
+  }
+}
+
+__global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint16_t* __restrict__ v,
+                                 const int32_t* __restrict__ S, const uint16_t* __restrict__ rval,
+                                 const uint8_t* __restrict__ ridx, int64_t N, int64_t K, int64_t nS,
+                                 int64_t n_pad, int64_t n_groups, uint16_t* __restrict__ o_alpha,
+                                 uint16_t* __restrict__ o_v, int32_t* __restrict__ o_S,
+                                 int32_t* __restrict__ o_spos, uint16_t* __restrict__ o_rval,
+                                 uint32_t* __restrict__ o_ridx) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  const int64_t t0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (int64_t i = t0; i < n_pad; i += stride) o_alpha[i] = i < N ? alpha[i] : 0;
+  for (int64_t i = t0; i < n_groups * kGroupCols; i += stride) o_v[i] = i < K ? v[i] : 0;
+  for (int64_t i = t0; i < nS; i += stride) o_S[i] = S[i];
+  for (int64_t g = t0; g <= n_groups; g += stride) {
+    // lower bound of 80 g in the sorted salient list
+    int64_t lo = 0, hi = nS;
+    const int64_t key = g * kGroupCols;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) / 2;
+      if (S[mid] < key)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    o_spos[g] = int32_t(lo);
+  }
+  const int64_t G = N / 4, Gp = n_pad / 4, Wp = n_pad / 64;
+  for (int64_t i = t0; i < nS * Gp; i += stride) {
+    const int64_t s = i / Gp, g = i % Gp;
+    o_rval[i] = g < G ? rval[s * G + g] : 0;
+  }
+  for (int64_t i = t0; i < nS * Wp; i += stride) {
+    const int64_t s = i / Wp, w = i % Wp;
+    uint32_t word = 0;
+    for (int k = 0; k < 16; ++k) {
+      const int64_t g = 16 * w + k;
+      if (g < G) word |= uint32_t(ridx[s * G + g] & 3) << (2 * k);
+    }
+    o_ridx[i] = word;
+  }
+}
+
+__global__ void write_header_kernel(uint8_t* packed, int64_t N, int64_t K, int64_t nS) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    uint32_t* h = reinterpret_cast<uint32_t*>(packed);
+    h[0] = QTEA_DESC_MAGIC;
+    h[1] = kLayout;
+    int64_t* h64 = reinterpret_cast<int64_t*>(packed + 8);
+    h64[0] = N;
+    h64[1] = K;
+    h64[2] = nS;
+    reinterpret_cast<uint32_t*>(packed + kFlagOffset)[0] = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Debug unpack (bit-exact read-back of the layout).
+// ---------------------------------------------------------------------------
+__global__ void unpack_codes_kernel(const uint8_t* __restrict__ tr, int64_t N, int64_t K,
+                                    int64_t n_packs, int64_t n_groups, uint8_t* __restrict__ canon,
+                                    int8_t* __restrict__ trits) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < N * n_packs; e += stride) {
+    const int64_t r = e / n_packs, p = e % n_packs;
+    const int64_t tile = r / kTileRows, l = r % kTileRows;
+    const int64_t g = p / kGroupPacks, q = p % kGroupPacks;
+    const int64_t i = (q - l) & (kGroupPacks - 1);
+    const uint8_t c = tr[((tile * n_groups + g) * kTileRows + l) * 16 + i];
+    if (canon) canon[e] = c;
+    if (trits) {
+      uint32_t rest = c;
+      for (int d = 0; d < 5; ++d) {
+        const int64_t j = 5 * p + d;
+        if (j < K) trits[r * K + j] = int8_t(int(rest % 3) - 1);
+        rest /= 3;
+      }
+    }
+  }
+}
+
+__global__ void unpack_resid_kernel(const uint32_t* __restrict__ ridx, int64_t N, int64_t nS,
+                                    int64_t n_pad, int32_t* __restrict__ rows) {
+  const int64_t G = N / 4, Wp = n_pad / 64;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < nS * G; e += stride) {
+    const int64_t s = e / G, g = e % G;
+    const uint32_t w = ridx[s * Wp + g / 16];
+    rows[e] = int32_t(4 * g + ((w >> (2 * (g % 16))) & 3));
+  }
+}
+
+__global__ void fill_zero_kernel(uint32_t* __restrict__ p, int64_t n_words, uint8_t* __restrict__ tail,
+                                 int64_t n_tail) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  const int64_t t0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (int64_t i = t0; i < n_words; i += stride) p[i] = 0;
+  for (int64_t i = t0; i < n_tail; i += stride) tail[i] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// The lookup-table GEMV.
+// ---------------------------------------------------------------------------
+struct GemvArgs {
+  const uint8_t* trits;
+  const uint16_t* alpha;
+  const uint16_t* v;
+  const int32_t* S;
+  const int32_t* spos;
+  const uint16_t* rval;
+  const uint32_t* ridx;
+  const uint16_t* x;
+  float* y;
+  float* part;
+  uint32_t* counters;
+  int64_t N, K, n_pad;
+  int n_groups, n_tiles;
+  int nrb, nslices, ks_groups;
+};
+
+// Batch vectors per table pass (BT) and 16-pack groups per table chunk (KC).
+// Table word of (code, group k, slot, bt) = ((code * KC + k) * 16 + slot) * BT + bt:
+// one code row is KC * 16 * BT floats = 256 bytes whenever KC * BT == 4, so
+// an address is code * 256 + low byte, formed by one v_perm_b32.
+template <int B>
+struct Cfg {
+  static constexpr int BT = B < 4 ? B : 4;
+  static constexpr int NPASS = (B + BT - 1) / BT;
+  static constexpr int KC = BT == 1 ? 4 : (BT == 2 ? 2 : 1);
+  static constexpr int COLS = KC * kGroupCols;  // activation columns per chunk
+  static constexpr bool PERM = KC * BT == 4;    // 256-byte code rows
+  static constexpr int ROW = KC * kGroupPacks * BT;  // floats per code row
+  static constexpr int LUT_FLOATS = kCodes * ROW;
+  // Table-build task = (pack, DEPTH leading digits); it writes the 3^(5-DEPTH)
+  // codes sharing those digits from a compile-time digit tree.
+  static constexpr int DEPTH = BT <= 2 ? 1 : 2;
+  static constexpr int NPRE = DEPTH == 1 ? 3 : 9;
+  static constexpr int SUB = kCodes / NPRE;
+  static constexpr int X_PER_THREAD = (B * COLS + kThreads - 1) / kThreads;
+  static constexpr int V_PER_THREAD = (COLS + kThreads - 1) / kThreads;
+};
+
+constexpr int kResBatch = 8;  // salient columns whose loads are issued together
+
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Leaves of the digit tree below `t`: digit DIG (and the ones below it)
+// enumerated at compile time; the value of code offset OFF + d * 3^DIG is
+// t + (d - 1) * a[DIG].  Leaves are stored at compile-time offsets from dst.
+template <int DIG, int OFF, int BT, int STRIDE>
+__device__ __forceinline__ void tree(float* dst, const float (&t)[BT], const float (&a)[5][BT]) {
+  constexpr int P3 = DIG == 0 ? 1 : DIG == 1 ? 3 : DIG == 2 ? 9 : DIG == 3 ? 27 : 81;
+#pragma unroll
+  for (int d = 0; d < 3; ++d) {
+    float u[BT];
+#pragma unroll
+    for (int bt = 0; bt < BT; ++bt) u[bt] = d == 0 ? t[bt] - a[DIG][bt] : (d == 2 ? t[bt] + a[DIG][bt] : t[bt]);
+    if constexpr (DIG == 0) {
+#pragma unroll
+      for (int bt = 0; bt < BT; ++bt) dst[(OFF + d) * STRIDE + bt] = u[bt];
+    } else {
+      if (d == 0) tree<DIG - 1, OFF, BT, STRIDE>(dst, u, a);
+      if (d == 1) tree<DIG - 1, OFF + P3, BT, STRIDE>(dst, u, a);
+      if (d == 2) tree<DIG - 1, OFF + 2 * P3, BT, STRIDE>(dst, u, a);
+    }
+  }
+}
+
+template <int B, int TPW>
+__global__ __launch_bounds__(kThreads) void lut_gemv_kernel(const GemvArgs p) {
+  using C = Cfg<B>;
+  constexpr int BT = C::BT, KC = C::KC, COLS = C::COLS;
+  __shared__ float lut[C::LUT_FLOATS];
+  __shared__ float x_lds[B * COLS];  // this chunk's activations, fp32
+  __shared__ float v_lds[COLS];      // this chunk's column rescales, fp32
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int quarter = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rb = blockIdx.x / p.nslices;
+  const int ks = blockIdx.x % p.nslices;
+  const int g0 = ks * p.ks_groups;
+  const int g1 = min(p.n_groups, g0 + p.ks_groups);
+  const int64_t Gp = p.n_pad / 4, Wp = p.n_pad / 64;
+
+  int tile[TPW];
+  bool valid[TPW];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) {
+    tile[j] = rb * (kWaves * TPW) + j * kWaves + wave;
+    valid[j] = tile[j] < p.n_tiles;
+  }
+  float acc[TPW][B], racc[TPW][B];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j)
+#pragma unroll
+    for (int b = 0; b < B; ++b) acc[j][b] = racc[j][b] = 0.0f;
+
+  // Byte i of a lane's unit holds slot (i + lane) mod 16: table offsets of
+  // the 16 slots, one per byte, for the v_perm address formation.
+  uint32_t rotw[4];
+#pragma unroll
+  for (int q4 = 0; q4 < 4; ++q4) {
+    uint32_t v4 = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v4 |= uint32_t(((q4 * 4 + e + lane) & 15) * BT * 4) << (8 * e);
+    rotw[q4] = v4;
+  }
+
+  for (int c0 = g0; c0 < g1; c0 += KC) {
+    const int nk = min(KC, g1 - c0);
+    const int64_t col0 = int64_t(c0) * kGroupCols;
+    // (1) activations and rescales of the chunk (issued first: needed first)
+    float xr[C::X_PER_THREAD], vr[C::V_PER_THREAD];
+#pragma unroll
+    for (int u = 0; u < C::X_PER_THREAD; ++u) {
+      const int e = tid + u * kThreads;
+      const int b = e / COLS, col = e % COLS;
+      xr[u] = (e < B * COLS && col < nk * kGroupCols && col0 + col < p.K) ? h2f(p.x[b * p.K + col0 + col]) : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < C::V_PER_THREAD; ++u) {
+      const int col = tid + u * kThreads;
+      vr[u] = (col < nk * kGroupCols) ? h2f(p.v[col0 + col]) : 0.0f;  // v is zero-padded to whole groups
+    }
+    // (2) packed bytes of this chunk for this lane's rows.  Quarter q of the
+    // wave takes the chunk's groups in the order q, q+1, ... so that at any
+    // step the four quarters address four different groups' table columns.
+    u32x4 w[TPW][KC];
+    int grp[KC];
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      int gk = k + quarter;
+      gk = gk >= nk ? gk - nk : gk;
+      gk = gk >= nk ? gk - nk : gk;
+      gk = gk >= nk ? gk - nk : gk;
+      grp[k] = gk;
+#pragma unroll
+      for (int j = 0; j < TPW; ++j) {
+        if (valid[j] && k < nk) {
+          const u32x4* src = reinterpret_cast<const u32x4*>(
+              p.trits + ((int64_t(tile[j]) * p.n_groups + c0 + gk) * kTileRows + lane) * 16);
+          w[j][k] = __builtin_nontemporal_load(src);
+        } else {
+          w[j][k] = u32x4(kZeroCode4);
+        }
+      }
+    }
+    // (3) salient columns of the chunk (uniform scalar loads)
+    const int sb = p.spos[c0], se = p.spos[c0 + nk];
+
+    __syncthreads();  // previous chunk's readers of lut / x_lds are done
+#pragma unroll
+    for (int u = 0; u < C::X_PER_THREAD; ++u) {
+      const int e = tid + u * kThreads;
+      if (e < B * COLS) x_lds[e] = xr[u];
+    }
+#pragma unroll
+    for (int u = 0; u < C::V_PER_THREAD; ++u) {
+      const int col = tid + u * kThreads;
+      if (col < COLS) v_lds[col] = vr[u];
+    }
+    // residual metadata of the first salient batch: lands during the build
+    int r_col[kResBatch];
+    uint32_t r_word[TPW][kResBatch];
+    uint16_t r_val[TPW][kResBatch];
+    auto load_res = [&](int s0) {
+#pragma unroll
+      for (int u = 0; u < kResBatch; ++u) {
+        const int s = s0 + u;
+        const bool ok = s < se;
+        r_col[u] = ok ? p.S[s] - int(col0) : 0;
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+          const int64_t r = int64_t(tile[j]) * kTileRows + lane;
+          r_word[j][u] = ok && valid[j] ? p.ridx[s * Wp + tile[j]] : 0u;
+          r_val[j][u] = ok && valid[j] ? p.rval[s * Gp + (r >> 2)] : uint16_t(0);
+        }
+      }
+    };
+    if (sb < se) load_res(sb);
+    __syncthreads();
+
+#pragma unroll
+    for (int pass = 0; pass < C::NPASS; ++pass) {
+      if (pass > 0) __syncthreads();  // lookups of the previous pass are done
+      // (4) table build: entry (group k, slot, code) = sum_i (d_i(code) - 1) * v_j x_j,
+      // j = 5 * pack + i.  Consecutive threads take consecutive slots.
+      for (int task = tid; task < nk * kGroupPacks * C::NPRE; task += kThreads) {
+        const int pk = task % (nk * kGroupPacks);
+        const int pf = task / (nk * kGroupPacks);
+        const int k = pk >> 4, slot = pk & 15;
+        const int cb = pk * 5;
+        float a[5][BT];
+#pragma unroll
+        for (int i = 0; i < 5; ++i)
+#pragma unroll
+          for (int bt = 0; bt < BT; ++bt) {
+            const int b = pass * BT + bt;
+            a[i][bt] = b < B ? v_lds[cb + i] * x_lds[b * COLS + cb + i] : 0.0f;
+          }
+        float t[BT];
+        float* dst = lut + ((pf * C::SUB * KC + k) * kGroupPacks + slot) * BT;
+        if constexpr (C::DEPTH == 1) {
+#pragma unroll
+          for (int bt = 0; bt < BT; ++bt) t[bt] = pf == 0 ? -a[4][bt] : (pf == 2 ? a[4][bt] : 0.0f);
+          tree<3, 0, BT, C::ROW>(dst, t, a);
+        } else {
+          const int d4 = pf / 3, d3 = pf - 3 * d4;
+#pragma unroll
+          for (int bt = 0; bt < BT; ++bt) {
+            const float t4 = d4 == 0 ? -a[4][bt] : (d4 == 2 ? a[4][bt] : 0.0f);
+            t[bt] = d3 == 0 ? t4 - a[3][bt] : (d3 == 2 ? t4 + a[3][bt] : t4);
+          }
+          tree<2, 0, BT, C::ROW>(dst, t, a);
+        }
+      }
+      __syncthreads();
+      // (5) lookup-accumulate: one table entry (BT floats) per packed byte.
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        if (k >= nk) break;
+        const uint32_t gbyte = uint32_t(grp[k] * kGroupPacks * BT * 4) * 0x01010101u;
+        const uint32_t lowb[4] = {rotw[0] | gbyte, rotw[1] | gbyte, rotw[2] | gbyte, rotw[3] | gbyte};
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+          if (!valid[j]) continue;
+          const uint32_t ww[4] = {w[j][k].x, w[j][k].y, w[j][k].z, w[j][k].w};
+#pragma unroll
+          for (int i = 0; i < kGroupPacks; ++i) {
+            uint32_t addr;
+            if constexpr (C::PERM) {
+              // [byte0 = low byte, byte1 = code, bytes 2-3 = 0] = code * 256 + low
+              const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (i & 3)) << 8) | uint32_t(i & 3);
+              addr = __builtin_amdgcn_perm(ww[i >> 2], lowb[i >> 2], sel);
+            } else {
+              const uint32_t code = (ww[i >> 2] >> (8 * (i & 3))) & 0xffu;
+              addr = code * uint32_t(C::ROW * 4) +
+                     uint32_t((grp[k] * kGroupPacks + ((i + lane) & 15)) * BT * 4);
+            }
+            const float* e = reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + addr);
+#pragma unroll
+            for (int bt = 0; bt < BT; ++bt)
+              if (pass * BT + bt < B) acc[j][pass * BT + bt] += e[bt];
+          }
+        }
+      }
+    }
+
+    // (6) salient residual of the chunk's columns (scaled by neither alpha nor v)
+    for (int s0 = sb; s0 < se; s0 += kResBatch) {
+      if (s0 != sb) load_res(s0);
+#pragma unroll
+      for (int j = 0; j < TPW; ++j) {
+        const int64_t r = int64_t(tile[j]) * kTileRows + lane;
+        const uint32_t shift = 2 * ((r >> 2) & 15);
+#pragma unroll
+        for (int u = 0; u < kResBatch; ++u) {
+          const bool hit = s0 + u < se && ((r_word[j][u] >> shift) & 3u) == uint32_t(r & 3);
+          if (hit) {
+            const float rv = h2f(r_val[j][u]);
+#pragma unroll
+            for (int b = 0; b < B; ++b) racc[j][b] += rv * x_lds[b * COLS + r_col[u]];
+          }
+        }
+      }
+    }
+  }
+
+  // Slice partial: alpha_r * (table sum) + residual.
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) {
+    if (!valid[j]) continue;
+    const int64_t r = int64_t(tile[j]) * kTileRows + lane;
+    const float al = h2f(p.alpha[r]);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const float v = al * acc[j][b] + racc[j][b];
+      if (p.nslices == 1) {
+        if (r < p.N) p.y[b * p.N + r] = v;
+      } else {
+        store_coherent(p.part + (int64_t(ks) * B + b) * p.n_pad + r, v);
+      }
+    }
+  }
+  if (p.nslices == 1) return;
+
+  // The last workgroup of this row block to arrive sums the slices in
+  // order.  Partials are written and read with agent-scope (L2-coherent)
+  // accesses; the wait below makes this workgroup's partials complete
+  // before its arrival is counted.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t prev = __hip_atomic_fetch_add(p.counters + rb, 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    s_last = prev == uint32_t(p.nslices - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  if (tid == 0)
+    __hip_atomic_store(p.counters + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) {
+    if (!valid[j]) continue;
+    const int64_t r = int64_t(tile[j]) * kTileRows + lane;
+    if (r >= p.N) continue;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const float* src = p.part + int64_t(b) * p.n_pad + r;
+      const int64_t qstride = int64_t(B) * p.n_pad;
+      float sum = 0.0f;
+      for (int q0 = 0; q0 < p.nslices; q0 += 8) {
+        float t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t[u] = q0 + u < p.nslices ? load_coherent(src + (q0 + u) * qstride) : 0.0f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (q0 + u < p.nslices) sum += t[u];
+      }
+      p.y[b * p.N + r] = sum;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launch planning.
+// ---------------------------------------------------------------------------
+struct Plan {
+  int tpw, nrb, nslices, ks_groups;
+};
+
+int kc_for_batch(int B) {
+  const int bt = B < 4 ? B : 4;
+  return bt == 1 ? 4 : (bt == 2 ? 2 : 1);
+}
+
+Plan make_plan(const qtea_desc& d, int B) {
+  Plan pl;
+  const int64_t n_tiles = d.n_pad / kTileRows;
+  const int kc = kc_for_batch(B);
+  if (B == 1) {
+    // One table chunk per workgroup: one build, no chunk loop.
+    pl.ks_groups = kc;
+    pl.nslices = int(cdiv(d.n_groups, kc));
+    pl.tpw = cdiv(n_tiles, 2 * kWaves) * pl.nslices >= 512 ? 2 : 1;
+    pl.nrb = int(cdiv(n_tiles, int64_t(kWaves) * pl.tpw));
+    return pl;
+  }
+  pl.tpw = n_tiles >= 256 ? 2 : 1;
+  pl.nrb = int(cdiv(n_tiles, int64_t(kWaves) * pl.tpw));
+  const int64_t target_wgs = 640;
+  int64_t nsl = cdiv(target_wgs, pl.nrb);
+  // Partial sums cost 8 bytes per row and batch vector per slice (write and
+  // read back); keep them to about a quarter of the row's packed bytes.
+  const int64_t cap = d.n_packs / (32 * int64_t(B));
+  if (nsl > cap) nsl = cap;
+  if (nsl < 1) nsl = 1;
+  int64_t ks = cdiv(d.n_groups, nsl);
+  ks = cdiv(ks, kc) * kc;
+  pl.ks_groups = int(ks);
+  pl.nslices = int(cdiv(d.n_groups, ks));
+  return pl;
+}
+
+int64_t workspace_need(const qtea_desc& d, int B) {
+  const Plan pl = make_plan(d, B);
+  const int64_t counters = align_up(4 * cdiv(d.n_pad / kTileRows, kWaves), kAlign);
+  const int64_t parts = pl.nslices > 1 ? 4 * int64_t(pl.nslices) * B * d.n_pad : 0;
+  return counters + parts;
+}
+
+template <int B, int TPW>
+hipError_t launch_t(const GemvArgs& a, int grid, hipStream_t st) {
+  hipLaunchKernelGGL((lut_gemv_kernel<B, TPW>), dim3(grid), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int B>
+hipError_t launch_b(const GemvArgs& a, int tpw, int grid, hipStream_t st) {
+  return tpw == 2 ? launch_t<B, 2>(a, grid, st) : launch_t<B, 1>(a, grid, st);
+}
+
+hipError_t launch_gemv(const GemvArgs& a, int B, int tpw, int grid, hipStream_t st) {
+  switch (B) {
+    case 1: return launch_b<1>(a, tpw, grid, st);
+    case 2: return launch_b<2>(a, tpw, grid, st);
+    case 3: return launch_b<3>(a, tpw, grid, st);
+    case 4: return launch_b<4>(a, tpw, grid, st);
+    case 5: return launch_b<5>(a, tpw, grid, st);
+    case 6: return launch_b<6>(a, tpw, grid, st);
+    case 7: return launch_b<7>(a, tpw, grid, st);
+    case 8: return launch_b<8>(a, tpw, grid, st);
+    case 9: return launch_b<9>(a, tpw, grid, st);
+    case 10: return launch_b<10>(a, tpw, grid, st);
+    case 11: return launch_b<11>(a, tpw, grid, st);
+    case 12: return launch_b<12>(a, tpw, grid, st);
+    case 13: return launch_b<13>(a, tpw, grid, st);
+    case 14: return launch_b<14>(a, tpw, grid, st);
+    case 15: return launch_b<15>(a, tpw, grid, st);
+    case 16: return launch_b<16>(a, tpw, grid, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int grid_for(int64_t n, int64_t per_thread_block = 256) {
+  int64_t g = cdiv(n, per_thread_block);
+  if (g < 1) g = 1;
+  if (g > 65536) g = 65536;
+  return int(g);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI.
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* qtea_status_string(int status) {
+  switch (status) {
+    case QTEA_OK: return "ok";
+    case QTEA_ERR_INVALID_ARG: return "invalid argument";
+    case QTEA_ERR_BAD_TRIT: return "trit outside {-1, 0, +1}";
+    case QTEA_ERR_BAD_RESIDUAL: return "bad residual position or salient column list";
+    case QTEA_ERR_BATCH: return "batch outside [1, 16]";
+    case QTEA_ERR_WORKSPACE: return "workspace or packed buffer too small";
+    case QTEA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int qtea_abi_version(void) { return QTEA_ABI_VERSION; }
+
+int qtea_packed_bytes(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes) {
+  Layout L;
+  if (!out_bytes || !make_layout(N, K, n_salient, &L)) return QTEA_ERR_INVALID_ARG;
+  *out_bytes = L.total;
+  return QTEA_OK;
+}
+
+int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
+              const uint16_t* col_rescale, const int32_t* salient, int64_t n_salient,
+              const uint16_t* resid_val, const uint8_t* resid_idx, void* packed,
+              int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
+  Layout L;
+  if (!out_desc) return QTEA_ERR_INVALID_ARG;
+  out_desc->magic = 0;
+  if (!make_layout(N, K, n_salient, &L)) return QTEA_ERR_INVALID_ARG;
+  if (!trits || !row_scale || !col_rescale || !packed) return QTEA_ERR_INVALID_ARG;
+  if (n_salient > 0 && (!salient || !resid_val || !resid_idx)) return QTEA_ERR_INVALID_ARG;
+  if (packed_bytes < L.total) return QTEA_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* pk = static_cast<uint8_t*>(packed);
+  uint32_t* flags = reinterpret_cast<uint32_t*>(pk + kFlagOffset);
+
+  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, st, pk, N, K, n_salient);
+  const int64_t ni = n_salient * (N / 4);
+  hipLaunchKernelGGL(validate_kernel, dim3(grid_for(N * K, 256 * 16)), dim3(256), 0, st, trits, N * K,
+                     resid_idx, ni, salient, n_salient, K, flags);
+  const int64_t n_units = L.n_tiles * L.n_groups * kTileRows;
+  hipLaunchKernelGGL(pack_trits_kernel, dim3(grid_for(n_units)), dim3(256), 0, st, trits, N, K,
+                     L.n_groups, n_units, pk + L.off_trits);
+  const int64_t meta_n = L.n_pad + L.n_groups * kGroupCols + n_salient * (L.n_pad / 4);
+  hipLaunchKernelGGL(pack_meta_kernel, dim3(grid_for(meta_n)), dim3(256), 0, st, row_scale,
+                     col_rescale, salient, resid_val, resid_idx, N, K, n_salient, L.n_pad, L.n_groups,
+                     reinterpret_cast<uint16_t*>(pk + L.off_alpha),
+                     reinterpret_cast<uint16_t*>(pk + L.off_v), reinterpret_cast<int32_t*>(pk + L.off_salient),
+                     reinterpret_cast<int32_t*>(pk + L.off_spos), reinterpret_cast<uint16_t*>(pk + L.off_rval),
+                     reinterpret_cast<uint32_t*>(pk + L.off_ridx));
+  if (hipGetLastError() != hipSuccess) return QTEA_ERR_HIP;
+  uint32_t hflags = 0;
+  if (hipMemcpyAsync(&hflags, flags, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return QTEA_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return QTEA_ERR_HIP;
+  if (hflags & kFlagBadTrit) return QTEA_ERR_BAD_TRIT;
+  if (hflags & kFlagBadResid) return QTEA_ERR_BAD_RESIDUAL;
+
+  qtea_desc d;
+  d.magic = QTEA_DESC_MAGIC;
+  d.layout = kLayout;
+  d.N = N;
+  d.K = K;
+  d.n_salient = n_salient;
+  d.n_packs = L.n_packs;
+  d.n_groups = L.n_groups;
+  d.n_pad = L.n_pad;
+  d.bytes_total = L.total;
+  d.off_trits = L.off_trits;
+  d.off_alpha = L.off_alpha;
+  d.off_v = L.off_v;
+  d.off_salient = L.off_salient;
+  d.off_spos = L.off_spos;
+  d.off_rval = L.off_rval;
+  d.off_ridx = L.off_ridx;
+  *out_desc = d;
+  return QTEA_OK;
+}
+
+int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes) {
+  if (!out_bytes || !desc_ok(desc)) return QTEA_ERR_INVALID_ARG;
+  if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
+  *out_bytes = workspace_need(*desc, batch);
+  return QTEA_OK;
+}
+
+int qtea_workspace_init(void* workspace, int64_t bytes, void* stream) {
+  if (!workspace || bytes < 0 || (reinterpret_cast<uintptr_t>(workspace) & 3)) return QTEA_ERR_INVALID_ARG;
+  if (bytes == 0) return QTEA_OK;
+  const int64_t words = bytes / 4;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(words)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), static_cast<uint32_t*>(workspace), words,
+                     static_cast<uint8_t*>(workspace) + 4 * words, bytes - 4 * words);
+  return hipGetLastError() == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+}
+
+int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
+                       float* Y, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc) || !packed || !X || !Y) return QTEA_ERR_INVALID_ARG;
+  if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
+  const qtea_desc& d = *desc;
+  const Plan pl = make_plan(d, batch);
+  const int64_t need = workspace_need(d, batch);
+  if (!workspace || workspace_bytes < need) return QTEA_ERR_WORKSPACE;
+  const uint8_t* pk = static_cast<const uint8_t*>(packed);
+  GemvArgs a;
+  a.trits = pk + d.off_trits;
+  a.alpha = reinterpret_cast<const uint16_t*>(pk + d.off_alpha);
+  a.v = reinterpret_cast<const uint16_t*>(pk + d.off_v);
+  a.S = reinterpret_cast<const int32_t*>(pk + d.off_salient);
+  a.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
+  a.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
+  a.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
+  a.x = X;
+  a.y = Y;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  a.counters = reinterpret_cast<uint32_t*>(ws);
+  a.part = reinterpret_cast<float*>(ws + align_up(4 * cdiv(d.n_pad / kTileRows, kWaves), kAlign));
+  a.N = d.N;
+  a.K = d.K;
+  a.n_pad = d.n_pad;
+  a.n_groups = int(d.n_groups);
+  a.n_tiles = int(d.n_pad / kTileRows);
+  a.nrb = pl.nrb;
+  a.nslices = pl.nslices;
+  a.ks_groups = pl.ks_groups;
+  const int grid = pl.nrb * pl.nslices;
+  if (launch_gemv(a, batch, pl.tpw, grid, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return QTEA_ERR_HIP;
+  return QTEA_OK;
+}
+
+int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y, void* workspace,
+              int64_t workspace_bytes, void* stream) {
+  return qtea_gemm_lowbatch(desc, packed, x, 1, y, workspace, workspace_bytes, stream);
+}
+
+int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_codes, int8_t* trits,
+                      int32_t* resid_row, void* stream) {
+  if (!desc_ok(desc) || !packed) return QTEA_ERR_INVALID_ARG;
+  const qtea_desc& d = *desc;
+  const uint8_t* pk = static_cast<const uint8_t*>(packed);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (canon_codes || trits)
+    hipLaunchKernelGGL(unpack_codes_kernel, dim3(grid_for(d.N * d.n_packs)), dim3(256), 0, st,
+                       pk + d.off_trits, d.N, d.K, d.n_packs, d.n_groups, canon_codes, trits);
+  if (resid_row && d.n_salient > 0)
+    hipLaunchKernelGGL(unpack_resid_kernel, dim3(grid_for(d.n_salient * (d.N / 4))), dim3(256), 0, st,
+                       reinterpret_cast<const uint32_t*>(pk + d.off_ridx), d.N, d.n_salient, d.n_pad,
+                       resid_row);
+  return hipGetLastError() == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+}
+
+}  // extern "C"

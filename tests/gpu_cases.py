@@ -1,0 +1,130 @@
+"""Shared helpers of the GPU parity tests: seeded cases, the HIP path run
+through the C ABI, and the tolerance check against the fp64 oracle.
+
+Tolerance (floating point outputs): per batch vector the relative L2 error
+is at most 1e-3, and per output row r the absolute error is at most
+2e-3 * ||x_b||_1 * max_j |W_eff[r][j]| (W_eff includes the residual).
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+import numpy as np
+
+import oracle
+import synth
+
+REL_L2 = 1e-3
+ROW_ABS = 2e-3
+
+
+def dyadic_case(seed, N, K, B, nS):
+    """Inputs whose every partial sum is exact in fp32: then the GPU result
+    equals the fp64 oracle bit for bit, whatever the summation order."""
+    rng = np.random.default_rng(seed)
+    S = np.sort(rng.choice(K, size=nS, replace=False)).astype(np.int32) if nS else np.zeros(0, np.int32)
+    return {
+        "N": N, "K": K,
+        "trits": rng.integers(-1, 2, size=(N, K)).astype(np.int8),
+        "alpha": (2.0 ** -rng.integers(0, 6, size=N)).astype(np.float16),
+        "v": rng.choice([0.5, 1.0, 1.5, 2.0], size=K).astype(np.float16),
+        "S": S,
+        "R": (rng.integers(-64, 65, size=(nS, N // 4)) / 64.0).astype(np.float16),
+        "idx": rng.integers(0, 4, size=(nS, N // 4)).astype(np.uint8),
+        "x": (rng.integers(-8, 9, size=(B, K)) / 4.0).astype(np.float16),
+    }
+
+
+def synth_case(seed, N, K, B, p0=Fraction(2, 5), frac=Fraction(2, 100), layer=0, mat=0, nS=None):
+    L = synth.layer_inputs(seed, layer, mat, N, K, p0=p0, frac=frac)
+    if nS is not None:  # override the salient count (edge cases)
+        rng = np.random.default_rng(seed + 1)
+        L["S"] = np.sort(rng.choice(K, size=nS, replace=False)).astype(np.int32)
+        L["R"] = (rng.standard_normal((nS, N // 4)) * 0.01).astype(np.float16)
+        L["idx"] = rng.integers(0, 4, size=(nS, N // 4)).astype(np.uint8)
+    L["x"] = synth.activations(seed, layer, mat, B, K)
+    return L
+
+
+def to_dev(a, dev="cuda"):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def gpu_pack(case, dev="cuda"):
+    import paper_2609_00224_amd as q
+
+    return q.pack_matrix(to_dev(case["trits"], dev), to_dev(case["alpha"], dev), to_dev(case["v"], dev),
+                         to_dev(case["S"], dev), to_dev(case["R"], dev), to_dev(case["idx"], dev))
+
+
+def gpu_unpack(pm, dev="cuda"):
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    d = pm.desc
+    codes = torch.empty((d.N, d.n_packs), dtype=torch.uint8, device=dev)
+    trits = torch.empty((d.N, d.K), dtype=torch.int8, device=dev)
+    rows = torch.empty((max(d.n_salient, 1), d.N // 4), dtype=torch.int32, device=dev)
+    q.qtea_debug_unpack(d, pm.packed, canon_codes=codes, trits=trits,
+                        resid_row=rows if d.n_salient else None)
+    torch.cuda.synchronize()
+    return codes.cpu().numpy(), trits.cpu().numpy(), rows.cpu().numpy()[: d.n_salient]
+
+
+def gpu_gemm(pm, x, dev="cuda", ws=None, use_gemv=False):
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    B = x.shape[0]
+    X = to_dev(x, dev)
+    Y = torch.full((B, pm.desc.N), float("nan"), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = q.new_workspace(pm.desc, B, dev)
+    if use_gemv:
+        assert B == 1
+        q.qtea_gemv(pm.desc, pm.packed, X, Y, ws)
+    else:
+        q.qtea_gemm_lowbatch(pm.desc, pm.packed, X, B, Y, ws)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy()
+
+
+def oracle_rows(case, rows=None, codes=None, need_wmax=True, block=512):
+    """fp64 oracle outputs and max |W_eff| of the given rows (default all).
+    The dense rows for max |W_eff| are formed a block of rows at a time."""
+    N, K = case["N"], case["K"]
+    if rows is None:
+        rows = np.arange(N, dtype=np.int64)
+    if codes is None:
+        codes = oracle.pack(case["trits"][rows])
+    args = (N, K, codes, case["alpha"], case["v"], case["S"], case["R"], case["idx"])
+    y = oracle.gemv(*args, case["x"], rows=rows)
+    if not need_wmax:
+        return y, None
+    wmax = np.empty(rows.size)
+    for i in range(0, rows.size, block):
+        sl = slice(i, i + block)
+        W = oracle.dense_rows(N, K, codes[sl], *args[3:], rows=rows[sl])
+        wmax[sl] = np.abs(W).max(axis=1)
+    return y, wmax
+
+
+def assert_close(y_gpu, y_ref, x, wmax, what=""):
+    """The tolerance stated in the module docstring."""
+    y_gpu = np.asarray(y_gpu, dtype=np.float64)
+    assert np.all(np.isfinite(y_gpu)), f"{what}: non-finite outputs"
+    xl1 = np.abs(x.astype(np.float64)).sum(axis=1)
+    for b in range(y_ref.shape[0]):
+        d = np.abs(y_gpu[b] - y_ref[b])
+        nrm = np.linalg.norm(y_ref[b])
+        if nrm > 0:
+            rel = np.linalg.norm(d) / nrm
+            assert rel <= REL_L2, f"{what}: batch {b} relative L2 error {rel:.3e}"
+        bound = ROW_ABS * xl1[b] * wmax
+        bad = np.nonzero(d > bound)[0]
+        assert bad.size == 0, (f"{what}: batch {b} row bound exceeded at {bad[:5]} "
+                               f"err {d[bad[:5]]} bound {bound[bad[:5]]}")

@@ -1,0 +1,77 @@
+"""The C-ABI library loads and exports every function include/qtea.h
+declares; host-side argument checks answer without touching a device."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_2609_00224_amd as q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qtea.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(qtea_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(q.LIB_PATH):
+        pytest.fail("libqtea.so is not built: run __graft_entry__.build()")
+    return q.load()
+
+
+def test_header_lists_the_binding_exports():
+    assert sorted(q.EXPORTS) == _declared_functions()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+        ctypes.cast(getattr(lib, name), ctypes.c_void_p)
+
+
+def test_abi_version_and_status_strings(lib):
+    assert q.qtea_abi_version() == 1
+    assert q.qtea_status_string(0) == "ok"
+    for s in range(-6, 0):
+        assert q.qtea_status_string(s) != "unknown status"
+    assert q.qtea_status_string(-99) == "unknown status"
+
+
+def test_packed_bytes_and_argument_checks(lib):
+    n = q.qtea_packed_bytes(4096, 4096, 82)
+    # packed trits are the largest region: 4096 rows x 52 groups x 16 bytes
+    assert n >= 4096 * 52 * 16 and n % 256 == 0
+    for bad in [(0, 4096, 0), (6, 10, 0), (4, 0, 0), (4, 10, 11), (4, 10, -1)]:
+        with pytest.raises(q.QteaError) as e:
+            q.qtea_packed_bytes(*bad)
+        assert e.value.status == q.QTEA_ERR_INVALID_ARG
+
+
+def test_invalid_descriptor_rejected_on_host(lib):
+    d = q.QteaDesc()
+    with pytest.raises(q.QteaError) as e:
+        q.qtea_workspace_bytes(d, 1)
+    assert e.value.status == q.QTEA_ERR_INVALID_ARG
+    out = ctypes.c_int64(0)
+    assert lib.qtea_gemv(ctypes.byref(d), None, None, None, None, 0, None) == q.QTEA_ERR_INVALID_ARG
+    assert lib.qtea_gemm_lowbatch(ctypes.byref(d), None, None, 1, None, None, 0, None) == q.QTEA_ERR_INVALID_ARG
+    assert lib.qtea_debug_unpack(ctypes.byref(d), None, None, None, None, None) == q.QTEA_ERR_INVALID_ARG
+    assert lib.qtea_workspace_bytes(None, 1, ctypes.byref(out)) == q.QTEA_ERR_INVALID_ARG
+    dd = q.QteaDesc()
+    assert lib.qtea_pack(None, 4, 4, None, None, None, 0, None, None, None, 0, ctypes.byref(dd),
+                         None) == q.QTEA_ERR_INVALID_ARG
+    assert dd.magic == 0
+
+
+def test_algorithmic_bytes_matches_oracle():
+    for N, K, nS in [(4096, 4096, 82), (8192, 28672, 573), (4, 1, 0), (12, 37, 5)]:
+        assert q.algorithmic_bytes(N, K, nS) == oracle.algorithmic_bytes(N, K, nS)
