@@ -14,8 +14,9 @@
 //   v        fp16 [n_groups * 80]      (zero in the column padding)
 //   salient  int32 [n_salient]
 //   spos     int32 [n_groups + 1]      first s with S_s >= 80 * g
-//   rval     fp16 [n_salient][n_pad/4] residual of four-row group g
-//   ridx     u32  [n_salient][n_pad/64] 2-bit positions, 16 groups per word
+//   rval     fp16 [n_pad/4][n_salient]  residual of four-row group g (row-group major:
+//            the rows of a workgroup read one contiguous run)
+//   ridx     u32  [n_pad/64][n_salient] 2-bit positions of 16 consecutive groups
 //
 // GEMV (one launch): workgroup = (row block, K slice).  For each chunk of
 // 16-pack groups of its slice it computes a_j = v_j x_j, builds the 243-entry
@@ -48,6 +49,9 @@ constexpr uint32_t kFlagBadTrit = 1u;
 constexpr uint32_t kFlagBadResid = 2u;
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) float lds_float;
 
 inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -182,11 +186,11 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
   }
   const int64_t G = N / 4, Gp = n_pad / 4, Wp = n_pad / 64;
   for (int64_t i = t0; i < nS * Gp; i += stride) {
-    const int64_t s = i / Gp, g = i % Gp;
+    const int64_t g = i / nS, s = i % nS;
     o_rval[i] = g < G ? rval[s * G + g] : 0;
   }
   for (int64_t i = t0; i < nS * Wp; i += stride) {
-    const int64_t s = i / Wp, w = i % Wp;
+    const int64_t w = i / nS, s = i % nS;
     uint32_t word = 0;
     for (int k = 0; k < 16; ++k) {
       const int64_t g = 16 * w + k;
@@ -236,11 +240,11 @@ __global__ void unpack_codes_kernel(const uint8_t* __restrict__ tr, int64_t N, i
 
 __global__ void unpack_resid_kernel(const uint32_t* __restrict__ ridx, int64_t N, int64_t nS,
                                     int64_t n_pad, int32_t* __restrict__ rows) {
-  const int64_t G = N / 4, Wp = n_pad / 64;
+  const int64_t G = N / 4;
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
   for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < nS * G; e += stride) {
     const int64_t s = e / G, g = e % G;
-    const uint32_t w = ridx[s * Wp + g / 16];
+    const uint32_t w = ridx[(g / 16) * nS + s];
     rows[e] = int32_t(4 * g + ((w >> (2 * (g % 16))) & 3));
   }
 }
@@ -269,7 +273,7 @@ struct GemvArgs {
   float* part;
   uint32_t* counters;
   int64_t N, K, n_pad;
-  int n_groups, n_tiles;
+  int n_groups, n_tiles, nS;
   int nrb, nslices, ks_groups;
 };
 
@@ -343,7 +347,6 @@ __global__ __launch_bounds__(kThreads) void lut_gemv_kernel(const GemvArgs p) {
   const int ks = blockIdx.x % p.nslices;
   const int g0 = ks * p.ks_groups;
   const int g1 = min(p.n_groups, g0 + p.ks_groups);
-  const int64_t Gp = p.n_pad / 4, Wp = p.n_pad / 64;
 
   int tile[TPW];
   bool valid[TPW];
@@ -435,8 +438,8 @@ __global__ __launch_bounds__(kThreads) void lut_gemv_kernel(const GemvArgs p) {
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
           const int64_t r = int64_t(tile[j]) * kTileRows + lane;
-          r_word[j][u] = ok && valid[j] ? p.ridx[s * Wp + tile[j]] : 0u;
-          r_val[j][u] = ok && valid[j] ? p.rval[s * Gp + (r >> 2)] : uint16_t(0);
+          r_word[j][u] = ok && valid[j] ? p.ridx[int64_t(tile[j]) * p.nS + s] : 0u;
+          r_val[j][u] = ok && valid[j] ? p.rval[(r >> 2) * p.nS + s] : uint16_t(0);
         }
       }
     };
@@ -613,7 +616,7 @@ struct B1Args {
   float* part;
   uint32_t* counters;
   int64_t N, K, n_pad;
-  int n_groups, n_tiles;
+  int n_groups, n_tiles, nS;
   int nslices, rbt;
 };
 
@@ -639,7 +642,6 @@ __global__ __launch_bounds__(WAVES * 64) void lut_gemv_b1_kernel(const B1Args p)
   const int tile_hi = min(p.n_tiles, tile_lo + p.rbt);
   // tiles of this wave: tile_lo + wave + WAVES i
   const int ntw = tile_hi - tile_lo > wave ? (tile_hi - tile_lo - wave + WAVES - 1) / WAVES : 0;
-  const int64_t Gp = p.n_pad / 4, Wp = p.n_pad / 64;
 
   // (1) activations, rescales, salient range
   for (int c = tid; c < COLS; c += NT) {
@@ -685,10 +687,10 @@ __global__ __launch_bounds__(WAVES * 64) void lut_gemv_b1_kernel(const B1Args p)
       }
     }
     alb[slot] = ok ? p.alpha[r] : uint16_t(0);
-    rwl[slot] = ok && lane < nsal ? p.ridx[(sb + lane) * Wp + tile] : 0u;
+    rwl[slot] = ok && lane < nsal ? p.ridx[int64_t(tile) * p.nS + sb + lane] : 0u;
 #pragma unroll
     for (int u = 0; u < kResBatch; ++u)
-      rvb[slot][u] = ok && u < nsal ? p.rval[(sb + u) * Gp + (r >> 2)] : uint16_t(0);
+      rvb[slot][u] = ok && u < nsal ? p.rval[(r >> 2) * p.nS + sb + u] : uint16_t(0);
   };
   fetch(0, 0);  // one tile in flight during the table build, the rest after it
   // salient columns relative to the slice's first column (lane u < nsal)
@@ -760,8 +762,8 @@ __global__ __launch_bounds__(WAVES * 64) void lut_gemv_b1_kernel(const B1Args p)
       }
       fetch(u, i + PD);  // refill slot u
       for (int s = sb + kResBatch; s < se; ++s) {  // salient columns beyond one batch
-        const uint32_t word = p.ridx[s * Wp + tile];
-        if (((word >> shift) & 3u) == uint32_t(r & 3)) racc += h2f(p.rval[s * Gp + (r >> 2)]) * x_lds[p.S[s] - int(col0)];
+        const uint32_t word = p.ridx[int64_t(tile) * p.nS + s];
+        if (((word >> shift) & 3u) == uint32_t(r & 3)) racc += h2f(p.rval[(r >> 2) * p.nS + s]) * x_lds[p.S[s] - int(col0)];
       }
       const float v = al * acc + racc;
       if constexpr (ACCUM) {
@@ -813,6 +815,271 @@ __global__ __launch_bounds__(WAVES * 64) void lut_gemv_b1_kernel(const B1Args p)
       const int64_t r = r0 + int64_t(h) * NT;
       if (r < row_hi) p.y[r] = sum[h];
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Factored-table kernel (whole K per workgroup).
+//
+// The 243-entry table of a pack factors into two small ones: with the code
+// split c = lo + 9 hi (lo = d0 + 3 d1, hi = d2 + 3 d3 + 9 d4),
+//   L[c] = T_lo[lo] + T_hi[hi],  T_lo[lo] = sum_{i<2} (d_i - 1) a_i,
+//                                 T_hi[hi] = sum_{i=2..4} (d_i - 1) a_i.
+// 36 instead of 243 entries per pack (144 bytes at batch 1) lets one CU hold
+// the tables of K up to 5120 columns at once, so a workgroup owns whole rows:
+// no K split, no cross-workgroup reduction, no workspace.  K beyond one
+// table chunk is walked in chunks, the table rebuilt per chunk.
+//
+// Lane mapping: a wave covers 16 rows (one per lane of a quarter-wave) and
+// four consecutive groups (one per quarter); the KS waves of a 16-row block
+// take interleaved groups.  Byte i of a row's unit is pack slot (i + row) mod
+// 16, so the 16 lanes of a quarter address 16 different packs and the four
+// quarters four different groups: with tables laid out [index][pack] and a
+// pack stride that is a multiple of 64 words, every lookup instruction hits
+// 64 distinct banks.
+// ---------------------------------------------------------------------------
+struct FkArgs {
+  const uint8_t* trits;
+  const uint16_t* alpha;
+  const uint16_t* v;
+  const int32_t* S;
+  const int32_t* spos;
+  const uint16_t* rval;
+  const uint32_t* ridx;
+  const uint16_t* x;
+  float* y;
+  int64_t N, K, n_pad;
+  int n_groups, nS;
+  int R;   // rows per workgroup (multiple of 16)
+  int KS;  // waves per 16-row block (K parts)
+  int CG;  // 16-pack groups per table chunk (multiple of 4)
+  int NP;  // table pack stride (multiple of 64, >= 16 CG)
+};
+
+constexpr int kFkU = 4;          // 16-byte units per lane per load batch
+constexpr int kFkMaxThreads = 1024;
+
+// Packs per table chunk (the table's pack stride) at batch B: 36 x NP x B
+// floats stay within 150 KB, and NP * B is a multiple of 64 words.
+template <int B>
+constexpr int fk_np() {
+  return B == 1 ? 1024 : B == 2 ? 512 : B == 3 ? 320 : 256;
+}
+
+template <int B>
+__global__ __launch_bounds__(kFkMaxThreads) void fk_gemv_kernel(const FkArgs p) {
+  extern __shared__ float smem[];
+  constexpr int NP = fk_np<B>();
+  float* tab = smem;                         // [36][NP][B]: T_lo rows 0..8, T_hi rows 9..35
+  float* red = smem + 36 * NP * B;           // [R][KS][2B] per-wave partial sums
+  const int nthreads = blockDim.x;
+  const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, l16 = lane & 15;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rbk = wave / p.KS, kp = wave - rbk * p.KS;
+  const int lpr = 4 * p.KS;                  // lanes per row
+  const int li = q + 4 * kp;                 // this lane's index among its row's lanes
+  const int64_t row = int64_t(blockIdx.x) * p.R + rbk * 16 + l16;
+  const bool row_ok = rbk * 16 < p.R && row < p.n_pad;
+  const int64_t tile = row >> 6;
+  const uint32_t rowbit = uint32_t(row & 3), shift = 2 * uint32_t((row >> 2) & 15);
+
+  // LDS byte address of this lane's first group, slot (i + row) mod 16, table row 0
+  const lds_char* tab_l = (const lds_char*)smem;
+  const uint32_t tab_base = uint32_t(size_t(tab_l));
+  uint32_t soff[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    soff[i] = tab_base + uint32_t((li * kGroupPacks + ((i + int(row)) & 15)) * B * 4);
+
+  float acc[B], racc[B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) acc[b] = racc[b] = 0.0f;
+
+  constexpr uint32_t rstride = uint32_t(NP * B * 4);  // bytes per table index row
+  constexpr uint32_t hi_off = 9u * rstride;            // T_hi follows the 9 rows of T_lo
+  for (int cg0 = 0; cg0 < p.n_groups; cg0 += p.CG) {
+    const int ncg = min(p.CG, p.n_groups - cg0);
+    const int npk = ncg * kGroupPacks;
+    const int64_t col0 = int64_t(cg0) * kGroupCols;
+    // units (16-byte pieces of the row) of this lane: group li + lpr m of the chunk
+    const int nu = row_ok && li < ncg ? (ncg - li + lpr - 1) / lpr : 0;
+    auto unit_ptr = [&](int m) {
+      return reinterpret_cast<const u32x4*>(
+          p.trits + ((tile * p.n_groups + cg0 + li + lpr * m) * kTileRows + (row & 63)) * 16);
+    };
+    u32x4 wa[kFkU], wb[kFkU];
+    auto load_units = [&](u32x4 (&w)[kFkU], int m0) {
+#pragma unroll
+      for (int u = 0; u < kFkU; ++u)
+        w[u] = m0 + u < nu ? __builtin_nontemporal_load(unit_ptr(m0 + u)) : u32x4(kZeroCode4);
+    };
+    // salient columns of the chunk: this lane takes sb + li + lpr n
+    const int sb = p.spos[cg0], se = p.spos[cg0 + ncg];
+    // Activations of this thread's first table-build packs are requested
+    // before any packed byte, so they do not queue behind the weight stream.
+    constexpr int kFkT = 2;
+    float xa[kFkT][5][B], va[kFkT][5];
+    auto load_act = [&](int pl0) {
+#pragma unroll
+      for (int j = 0; j < kFkT; ++j) {
+        const int pl = pl0 + j * nthreads;
+        const int64_t c5 = col0 + 5 * pl;
+#pragma unroll
+        for (int i = 0; i < 5; ++i) {
+          const bool use = pl < npk;
+          va[j][i] = use ? h2f(p.v[c5 + i]) : 0.0f;  // v zero-padded to whole groups
+#pragma unroll
+          for (int b = 0; b < B; ++b) xa[j][i][b] = use && c5 + i < p.K ? h2f(p.x[b * p.K + c5 + i]) : 0.0f;
+        }
+      }
+    };
+    load_act(tid);
+    load_units(wa, 0);  // first units stream in during the table build
+
+    __syncthreads();  // previous chunk's readers of the tables are done
+    // Table build: each thread takes whole packs (all 36 entries: T_lo from
+    // digits 0-1, T_hi from digits 2-4), kFkT packs at a time with all their
+    // activation loads issued first.
+    for (int pl0 = tid; pl0 < npk; pl0 += kFkT * nthreads) {
+      if (pl0 != tid) load_act(pl0);
+#pragma unroll
+      for (int j = 0; j < kFkT; ++j) {
+        const int pl = pl0 + j * nthreads;
+        if (pl >= npk) break;
+        float a[5][B];
+#pragma unroll
+        for (int i = 0; i < 5; ++i)
+#pragma unroll
+          for (int b = 0; b < B; ++b) a[i][b] = va[j][i] * xa[j][i][b];
+        float* dst = tab + int64_t(pl) * B;
+        // T_lo[3 d1 + d0]
+#pragma unroll
+        for (int d1 = 0; d1 < 3; ++d1)
+#pragma unroll
+          for (int d0 = 0; d0 < 3; ++d0)
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+              float e = d1 == 0 ? -a[1][b] : (d1 == 2 ? a[1][b] : 0.0f);
+              e = d0 == 0 ? e - a[0][b] : (d0 == 2 ? e + a[0][b] : e);
+              dst[int64_t(d1 * 3 + d0) * NP * B + b] = e;
+            }
+        // T_hi[9 d4 + 3 d3 + d2], rows 9..35
+#pragma unroll
+        for (int d4 = 0; d4 < 3; ++d4)
+#pragma unroll
+          for (int d3 = 0; d3 < 3; ++d3)
+#pragma unroll
+            for (int d2 = 0; d2 < 3; ++d2)
+#pragma unroll
+              for (int b = 0; b < B; ++b) {
+                float e = d4 == 0 ? -a[4][b] : (d4 == 2 ? a[4][b] : 0.0f);
+                e = d3 == 0 ? e - a[3][b] : (d3 == 2 ? e + a[3][b] : e);
+                e = d2 == 0 ? e - a[2][b] : (d2 == 2 ? e + a[2][b] : e);
+                dst[int64_t(9 + d4 * 9 + d3 * 3 + d2) * NP * B + b] = e;
+              }
+      }
+    }
+    // residual loads of this lane's salient columns (first batch), in flight during the build
+    constexpr int RB = 8;
+    int rs_col[RB];
+    uint32_t rs_word[RB];
+    uint16_t rs_val[RB];
+    auto load_res = [&](int n0) {
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        const int s = sb + li + lpr * (n0 + u);
+        const bool ok = row_ok && s < se;
+        rs_col[u] = ok ? p.S[s] : -1;
+        rs_word[u] = ok ? p.ridx[tile * p.nS + s] : 0u;
+        rs_val[u] = ok ? p.rval[(row >> 2) * p.nS + s] : uint16_t(0);
+      }
+    };
+    load_res(0);
+    __syncthreads();
+    // activations at the first batch of salient columns: land during the lookups
+    float xv[RB][B];
+    auto load_xv = [&]() {
+#pragma unroll
+      for (int u = 0; u < RB; ++u)
+#pragma unroll
+        for (int b = 0; b < B; ++b) xv[u][b] = rs_col[u] >= 0 ? h2f(p.x[b * p.K + rs_col[u]]) : 0.0f;
+    };
+    load_xv();
+
+    // Lookup-accumulate: two table entries per packed byte.
+    auto consume = [&](const u32x4 (&w)[kFkU], int m0) {
+#pragma unroll
+      for (int u = 0; u < kFkU; ++u) {
+        if (m0 + u >= nu) break;
+        // groups of this lane are li + lpr m: the part beyond the first is wave-uniform
+        const uint32_t um = uint32_t(lpr * (m0 + u) * kGroupPacks * B * 4);
+        const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t c = (ww[i >> 2] >> (8 * (i & 3))) & 0xffu;
+          const uint32_t hi = __umul24(c, 57u) >> 9;  // c / 9 for c < 243
+          const uint32_t lo = c - 9u * hi;
+          const uint32_t so = soff[i] + um;
+          const lds_float* elo = (const lds_float*)(size_t)(lo * rstride + so);
+          const lds_float* ehi = (const lds_float*)(size_t)(hi * rstride + so + hi_off);
+#pragma unroll
+          for (int b = 0; b < B; ++b) acc[b] += elo[b] + ehi[b];
+        }
+      }
+    };
+    for (int m0 = 0; m0 < nu; m0 += 2 * kFkU) {
+      load_units(wb, m0 + kFkU);
+      consume(wa, m0);
+      load_units(wa, m0 + 2 * kFkU);
+      consume(wb, m0 + kFkU);
+    }
+
+    // Salient residual of the chunk: scaled by neither alpha nor v.
+    const int nres = row_ok && sb + li < se ? (se - sb - li + lpr - 1) / lpr : 0;
+    for (int n0 = 0; n0 < nres; n0 += RB) {
+      if (n0 > 0) {
+        load_res(n0);
+        load_xv();
+      }
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+        if (rs_col[u] >= 0 && ((rs_word[u] >> shift) & 3u) == rowbit) {
+          const float rv = h2f(rs_val[u]);
+#pragma unroll
+          for (int b = 0; b < B; ++b) racc[b] += rv * xv[u][b];
+        }
+      }
+    }
+  }
+
+  // Reduce the row's 4 KS partial sums in a fixed order: the four quarters
+  // of the wave first, then the KS waves of the row block through LDS.
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    acc[b] += __shfl_xor(acc[b], 16);
+    acc[b] += __shfl_xor(acc[b], 32);
+    racc[b] += __shfl_xor(racc[b], 16);
+    racc[b] += __shfl_xor(racc[b], 32);
+  }
+  if (q == 0 && rbk * 16 < p.R) {
+    float* r = red + ((rbk * 16 + l16) * p.KS + kp) * 2 * B;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      r[b] = acc[b];
+      r[B + b] = racc[b];
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < p.R * B; e += nthreads) {
+    const int rr = e / B, b = e - rr * B;
+    const int64_t orow = int64_t(blockIdx.x) * p.R + rr;
+    if (orow >= p.N) continue;
+    float sa = 0.0f, sr = 0.0f;
+    for (int k = 0; k < p.KS; ++k) {
+      sa += red[(rr * p.KS + k) * 2 * B + b];
+      sr += red[(rr * p.KS + k) * 2 * B + B + b];
+    }
+    p.y[b * p.N + orow] = h2f(p.alpha[orow]) * sa + sr;
   }
 }
 
@@ -913,6 +1180,64 @@ int grid_for(int64_t n, int64_t per_thread_block = 256) {
   if (g > 65536) g = 65536;
   return int(g);
 }
+
+// Plan of the factored-table kernel.
+struct FkPlan {
+  int R, KS, CG, NP, threads, grid;
+  size_t lds;
+};
+
+constexpr size_t kLdsBytes = 160 * 1024;
+
+FkPlan fk_plan(const qtea_desc& d, int B) {
+  FkPlan f;
+  // Rows per workgroup: one workgroup per CU covers the matrix (multiples of 16 rows).
+  f.R = int(cdiv(cdiv(d.N, 16), 256) * 16);
+  if (f.R > 256) f.R = 256;
+  f.grid = int(cdiv(d.N, f.R));
+  const int blocks = f.R / 16;
+  const int G = int(d.n_groups);
+  // K parts per 16-row block: up to 16 waves per workgroup.
+  int ks = 16 / blocks;
+  if (ks < 1) ks = 1;
+  // Table chunk: the kernel's fixed pack stride bounds the groups per chunk;
+  // chunks are balanced.
+  const int np = B == 1 ? fk_np<1>() : B == 2 ? fk_np<2>() : B == 3 ? fk_np<3>() : fk_np<4>();
+  const int cgmax = np / kGroupPacks;
+  const int nch = int(cdiv(G, cgmax));
+  f.CG = int(cdiv(G, nch));
+  f.NP = np;
+  const int maxks = int(cdiv(f.CG, 4));  // at least one group per lane
+  f.KS = ks < maxks ? ks : maxks;
+  f.threads = blocks * f.KS * 64;
+  f.lds = size_t(36) * f.NP * B * 4 + size_t(f.R) * f.KS * 2 * B * 4;
+  return f;
+}
+
+template <int B>
+hipError_t launch_fk(const FkArgs& a, const FkPlan& f, hipStream_t st) {
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&fk_gemv_kernel<B>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, int(kLdsBytes));
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL(fk_gemv_kernel<B>, dim3(f.grid), dim3(f.threads), f.lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fk_b(const FkArgs& a, const FkPlan& f, int B, hipStream_t st) {
+  switch (B) {
+    case 1: return launch_fk<1>(a, f, st);
+    case 2: return launch_fk<2>(a, f, st);
+    case 3: return launch_fk<3>(a, f, st);
+    case 4: return launch_fk<4>(a, f, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+bool use_fk(int B) { return B <= 4; }
 
 }  // namespace
 
@@ -1044,9 +1369,33 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
   a.n_pad = d.n_pad;
   a.n_groups = int(d.n_groups);
   a.n_tiles = int(d.n_pad / kTileRows);
+  a.nS = int(d.n_salient);
   a.nrb = pl.nrb;
   a.nslices = pl.nslices;
   a.ks_groups = pl.ks_groups;
+  if (use_fk(batch)) {
+    const FkPlan f = fk_plan(d, batch);
+    FkArgs k;
+    k.trits = a.trits;
+    k.alpha = a.alpha;
+    k.v = a.v;
+    k.S = a.S;
+    k.spos = a.spos;
+    k.rval = a.rval;
+    k.ridx = a.ridx;
+    k.x = a.x;
+    k.y = a.y;
+    k.N = a.N;
+    k.K = a.K;
+    k.n_pad = a.n_pad;
+    k.n_groups = a.n_groups;
+    k.nS = a.nS;
+    k.R = f.R;
+    k.KS = f.KS;
+    k.CG = f.CG;
+    k.NP = f.NP;
+    return launch_fk_b(k, f, batch, static_cast<hipStream_t>(stream)) == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+  }
   const int grid = pl.nrb * pl.nslices;
   if (batch == 1) {
     B1Args b;
@@ -1066,6 +1415,7 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
     b.n_pad = a.n_pad;
     b.n_groups = a.n_groups;
     b.n_tiles = a.n_tiles;
+    b.nS = a.nS;
     b.nslices = pl.nslices;
     b.rbt = pl.rbt;
     hipLaunchKernelGGL((lut_gemv_b1_kernel<2, 4, false>), dim3(grid), dim3(256), 0,
