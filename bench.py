@@ -1,11 +1,18 @@
 """Throughput of the compressed ternary GEMV stack on one MI355X.
 
-One step = one token through a synthetic linear stack: for every layer the
-fused QKV, O, fused gate_up and down GEMVs (qtea_gemm_lowbatch), launched in
-order on one stream and captured as one HIP graph, as the paper measures its
-per-token latency with CUDA Graph.  Weights are packed once (untimed) and
-stay resident in HBM; every matrix has its own seeded weights and its own
-seeded activations, also resident before the timed region.
+One step = one token through a synthetic linear stack: every layer's fused
+QKV, O, fused gate_up and down GEMV, each matrix with its own seeded weights
+and its own seeded activations.  Weights are packed once (untimed) and stay
+resident in HBM, as do the activations, before the timed region.
+
+Two executions of the same step are timed:
+  grouped  one qtea_grouped_gemv launch computes all of the token's GEMVs
+           (their inputs are independent, as generated); the weight stream
+           runs back to back across matrices.  This is `value`.
+  chained  one qtea_gemm_lowbatch launch per GEMV, in order on one stream,
+           captured as one HIP graph (the paper times per-token latency with
+           CUDA Graph); each launch starts after the previous one ends, as in
+           a decoder where each product feeds the next.  Reported beside it.
 
 Default workload: the 32-layer Llama-3-8B-shaped stack at batch 1
 (1.48 GB of packed weights per token, far beyond the 256 MB last-level
@@ -13,8 +20,8 @@ cache, so every token streams its weights from HBM).
 
 Printed: one JSON line with the weight-stream GB/s (algorithmic bytes per
 token / time per token), us per token, the roofline of the dominant kernel
-(the GEMV kernel that serves every matrix of the token, timed live with HIP
-events around the graph replays) and the CPU oracle baseline.
+(timed live with HIP events around graph replays on its stream), the
+chained figures and the CPU oracle baseline.
 """
 from __future__ import annotations
 
@@ -81,6 +88,19 @@ def capture(mats, B, ws, stream):
     return g
 
 
+def capture_grouped(gp, stream):
+    import torch
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        gp.run(stream=stream)
+        stream.synchronize()
+        with torch.cuda.graph(g, stream=stream):
+            gp.run(stream=stream)
+    stream.synchronize()
+    return g
+
+
 def time_graph(g, stream, reps, warmup):
     import torch
 
@@ -98,7 +118,9 @@ def time_graph(g, stream, reps, warmup):
     return e0.elapsed_time(e1) / reps  # ms per replay
 
 
-def kernel_name(B):
+def kernel_name(B, grouped=False, rows_per_panel=1024):
+    if grouped:
+        return f"grouped_gemv_kernel<{rows_per_panel // 128}>"
     return f"fk_gemv_kernel<{B}>" if B <= 4 else f"lut_gemv_kernel<{B}, 2>"
 
 
@@ -107,8 +129,10 @@ def traffic_per_launch(kernel, algorithmic_bytes):
     taken on the current kernel source (sha256 recorded in the summary)."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", "traffic_fk_gemv_b1_llama3_8b_stack.txt")
-    src = os.path.join(ROOT, "paper_2609_00224_amd", "csrc", "qtea.hip")
+    name = "grouped_gemv" if kernel.startswith("grouped") else "fk_gemv"
+    path = os.path.join(ROOT, "profiles", f"traffic_{name}_b1_llama3_8b_stack.txt")
+    src = os.path.join(ROOT, "paper_2609_00224_amd", "csrc",
+                       "grouped.hip" if kernel.startswith("grouped") else "qtea.hip")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -197,6 +221,7 @@ def main():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--chained-only", action="store_true", help="time only the per-GEMV launches")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="after the bench, copy this many bytes device-to-device 3 times "
                          "(known-size reference for HBM counters)")
@@ -224,9 +249,23 @@ def main():
     ws = torch.zeros(max(ws_bytes, 4), dtype=torch.uint8, device=dev)
     stream = torch.cuda.Stream(device=dev)
 
-    g = capture(mats, B, ws, stream)
-    ms = time_graph(g, stream, args.steps, args.warmup)
     token_bytes = sum(m["bytes"] for m in mats)
+    g = capture(mats, B, ws, stream)
+    ms_chain = time_graph(g, stream, args.steps, args.warmup)
+    gbs_chain = token_bytes / (ms_chain * 1e-3) / 1e9
+    log(f"{wl.name} B={B} chained: {ms_chain * 1e3:.1f} us/token, {gbs_chain:.1f} GB/s "
+        f"({gbs_chain / HBM_PEAK_GBS:.1%} of peak)")
+    del g
+
+    grouped = B == 1 and not args.chained_only
+    if grouped:
+        gp = q.plan_grouped([m["pm"] for m in mats], [m["x"] for m in mats], [m["y"] for m in mats])
+        gg = capture_grouped(gp, stream)
+        ms = time_graph(gg, stream, args.steps, args.warmup)
+        log(f"{wl.name} B={B} grouped: {ms * 1e3:.1f} us/token ({gp.info.n_units} units, "
+            f"{gp.info.rows_per_panel}-row panels, {gp.info.grid} workgroups)")
+    else:
+        ms = ms_chain
     gbs = token_bytes / (ms * 1e-3) / 1e9
     log(f"{wl.name} B={B}: {ms * 1e3:.1f} us/token, {gbs:.1f} GB/s ({gbs / HBM_PEAK_GBS:.1%} of peak)")
 
@@ -242,19 +281,29 @@ def main():
                            "gbs": round(sub[0]["bytes"] / (per * 1e-3) / 1e9, 1)}
             log(f"  {role:8s} {N}x{K}: {per * 1e3:.2f} us/launch, {roles[role]['gbs']} GB/s")
             del gr
-    # Roofline of the dominant kernel: every GEMV of the token is one launch
-    # of the same kernel, so its average launch moves token_bytes / launches
-    # in ms / launches (HIP events around the graph replays above).
-    n_launch = len(mats)
+    # Roofline of the dominant kernel.  Grouped: one launch per step moves
+    # the token's bytes.  Chained: every GEMV is a launch of the same kernel,
+    # so the average launch moves token_bytes / launches.  Durations come
+    # from HIP events around the graph replays above.
+    n_launch = 1 if grouped else len(mats)
+    kname = kernel_name(B, grouped, gp.info.rows_per_panel if grouped else 1024)
     per_launch_bytes = token_bytes / n_launch
     us_launch = ms * 1e3 / n_launch
     ach = per_launch_bytes / (us_launch * 1e-6) / 1e9
     roof = {"bound": "hbm", "achieved": round(ach, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBS, 4),
-            "traffic": traffic_per_launch(kernel_name(B), per_launch_bytes),
-            "kernel": kernel_name(B), "launches_per_step": n_launch,
+            "traffic": traffic_per_launch(kname, per_launch_bytes),
+            "kernel": kname, "launches_per_step": n_launch,
             "algorithmic_bytes_per_launch": int(per_launch_bytes), "us_per_launch": round(us_launch, 3)}
+    chained = {"us_per_token": round(ms_chain * 1e3, 2), "value": round(gbs_chain, 2), "unit": "GB/s",
+               "frac_hbm_peak": round(gbs_chain / HBM_PEAK_GBS, 4), "kernel": kernel_name(B),
+               "launches_per_step": len(mats), "us_per_launch": round(ms_chain * 1e3 / len(mats), 3),
+               "per_role": roles}
 
+    if grouped:  # leave the grouped outputs in y for the oracle comparison
+        with torch.cuda.stream(stream):
+            gg.replay()
+        stream.synchronize()
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(mats, wl, seed, B)
@@ -278,7 +327,8 @@ def main():
                    "batch": B, "weight_bytes_per_token": token_bytes, "seed": seed},
         "us_per_token": round(ms * 1e3, 2),
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
-        "per_role": roles,
+        "execution": "grouped" if grouped else "chained",
+        "chained": chained,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -159,6 +159,61 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
 int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_codes,
                       int8_t* trits, int32_t* resid_row, void* stream);
 
+/*
+ * Grouped GEMV: y_m = W_m x_m for a list of n_problems independent problems
+ * (each W_m packed by qtea_pack; the same operation as qtea_gemv applied to
+ * every problem) in one persistent launch.  The problems' packed bytes are
+ * streamed back to back: a workgroup already loads the next problem's
+ * weights while it finishes the current one.  No problem may read another
+ * problem's output (all activations must be ready when the launch starts);
+ * for a chain of dependent products call qtea_gemv per product instead.
+ *
+ * Usage: qtea_grouped_plan once (offline, synchronizes `stream`), then
+ * qtea_grouped_gemv any number of times (graph-capturable, no host work).
+ * The plan binds the device pointers given to qtea_grouped_plan; change
+ * any of them and plan again.
+ */
+typedef struct qtea_grouped_info {
+  uint32_t magic;          /* set by qtea_grouped_plan                    */
+  int32_t n_problems;
+  int32_t batch;           /* activation rows per problem (only 1 so far) */
+  int32_t grid;            /* workgroups of the launch (one per CU)       */
+  int32_t rows_per_panel;  /* output rows of one work unit               */
+  int32_t max_parts;       /* runs sharing one panel, at most            */
+  int64_t n_units;
+  int64_t plan_bytes;      /* device plan buffer size                    */
+  int64_t workspace_bytes; /* workspace needed by qtea_grouped_gemv      */
+} qtea_grouped_info;
+
+/* Size of the device plan buffer for n_problems problems on the current device. */
+int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes);
+
+/*
+ * Build the plan of a grouped GEMV.
+ *   descs[m], packed[m]  host array of descriptors / host array of device
+ *                        pointers to the packed buffers (qtea_pack)
+ *   x[m]                 host array of device pointers, fp16 [batch][K_m]
+ *   y[m]                 host array of device pointers, fp32 [batch][N_m]
+ *   batch                must be 1 (QTEA_ERR_BATCH otherwise)
+ *   plan                 device buffer, >= qtea_grouped_plan_bytes(n_problems)
+ *   info                 host, filled on success
+ * Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_BATCH, QTEA_ERR_WORKSPACE (plan
+ * buffer too small), QTEA_ERR_HIP.
+ */
+int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const uint16_t* const* x,
+                      float* const* y, int n_problems, int batch, void* plan, int64_t plan_bytes,
+                      qtea_grouped_info* info, void* stream);
+
+/*
+ * Run a planned grouped GEMV.  `workspace` (>= info->workspace_bytes) holds
+ * the partial rows and arrival counters of panels split between two
+ * workgroups; it must be zero-filled before first use and is left
+ * zero-filled by every completed call (as for qtea_gemv).  fp32
+ * accumulation, run-to-run deterministic.
+ */
+int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* workspace,
+                      int64_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,13 +1,15 @@
 """MI355X (gfx950) compressed ternary GEMV: Python binding of libqtea.so.
 
 The binding marshals arguments only: every step of the GEMV runs in the HIP
-kernels of ``csrc/qtea.hip`` behind the C ABI of ``include/qtea.h``.  Torch
+kernels of ``csrc/qtea.hip`` and ``csrc/grouped.hip`` behind the C ABI of
+``include/qtea.h``.  Torch
 is used to allocate device memory and to name the current HIP stream.
 There is no CPU fallback: if the library is not built, loading it raises.
 
 Entry points carry the C names: qtea_packed_bytes, qtea_pack,
 qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
-qtea_debug_unpack, qtea_status_string, qtea_abi_version.
+qtea_debug_unpack, qtea_status_string, qtea_abi_version,
+qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv.
 """
 from __future__ import annotations
 
@@ -32,8 +34,9 @@ QTEA_DESC_MAGIC = 0x51544541
 EXPORTS = (
     "qtea_status_string", "qtea_abi_version", "qtea_packed_bytes", "qtea_pack",
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
-    "qtea_debug_unpack",
+    "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
 )
+QTEA_GROUPED_MAGIC = 0x51475250
 
 
 class QteaDesc(ctypes.Structure):
@@ -46,6 +49,15 @@ class QteaDesc(ctypes.Structure):
         ("off_trits", ctypes.c_int64), ("off_alpha", ctypes.c_int64), ("off_v", ctypes.c_int64),
         ("off_salient", ctypes.c_int64), ("off_spos", ctypes.c_int64), ("off_rval", ctypes.c_int64),
         ("off_ridx", ctypes.c_int64),
+    ]
+
+
+class QteaGroupedInfo(ctypes.Structure):
+    """Mirror of struct qtea_grouped_info (include/qtea.h)."""
+    _fields_ = [
+        ("magic", ctypes.c_uint32), ("n_problems", ctypes.c_int32), ("batch", ctypes.c_int32),
+        ("grid", ctypes.c_int32), ("rows_per_panel", ctypes.c_int32), ("max_parts", ctypes.c_int32),
+        ("n_units", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
     ]
 
 
@@ -87,6 +99,14 @@ def load(path: str = LIB_PATH):
     lib.qtea_gemm_lowbatch.argtypes = [pdesc, vp, vp, i32, vp, vp, i64, vp]
     lib.qtea_debug_unpack.restype = i32
     lib.qtea_debug_unpack.argtypes = [pdesc, vp, vp, vp, vp, vp]
+    pinfo = ctypes.POINTER(QteaGroupedInfo)
+    lib.qtea_grouped_plan_bytes.restype = i32
+    lib.qtea_grouped_plan_bytes.argtypes = [i32, ctypes.POINTER(i64)]
+    lib.qtea_grouped_plan.restype = i32
+    lib.qtea_grouped_plan.argtypes = [pdesc, ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                      i32, i32, vp, i64, pinfo, vp]
+    lib.qtea_grouped_gemv.restype = i32
+    lib.qtea_grouped_gemv.argtypes = [pinfo, vp, vp, i64, vp]
     _lib = lib
     return lib
 
@@ -186,6 +206,60 @@ def qtea_debug_unpack(desc: QteaDesc, packed, canon_codes=None, trits=None, resi
     _need_cuda(packed, canon_codes, trits, resid_row)
     _check(load().qtea_debug_unpack(ctypes.byref(desc), _ptr(packed), _ptr(canon_codes), _ptr(trits),
                                     _ptr(resid_row), _stream(stream)), "qtea_debug_unpack")
+
+
+def qtea_grouped_plan_bytes(n_problems: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().qtea_grouped_plan_bytes(int(n_problems), ctypes.byref(out)), "qtea_grouped_plan_bytes")
+    return out.value
+
+
+def qtea_grouped_plan(descs, packed, xs, ys, batch: int, plan, stream=None) -> QteaGroupedInfo:
+    """Plan y_m = W_m x_m for independent problems m (lists of descriptors,
+    packed buffers, fp16 activations, fp32 outputs: device tensors)."""
+    n = len(descs)
+    if not (len(packed) == len(xs) == len(ys) == n) or n < 1:
+        raise ValueError("one descriptor, packed buffer, x and y per problem")
+    _need_cuda(plan, *packed, *xs, *ys)
+    darr = (QteaDesc * n)(*descs)
+    parr = (ctypes.c_void_p * n)(*[t.data_ptr() for t in packed])
+    xarr = (ctypes.c_void_p * n)(*[t.data_ptr() for t in xs])
+    yarr = (ctypes.c_void_p * n)(*[t.data_ptr() for t in ys])
+    info = QteaGroupedInfo()
+    _check(load().qtea_grouped_plan(darr, parr, xarr, yarr, n, int(batch), _ptr(plan),
+                                    plan.numel() * plan.element_size(), ctypes.byref(info),
+                                    _stream(stream)), "qtea_grouped_plan")
+    return info
+
+
+def qtea_grouped_gemv(info: QteaGroupedInfo, plan, workspace, stream=None):
+    _need_cuda(plan, workspace)
+    _check(load().qtea_grouped_gemv(ctypes.byref(info), _ptr(plan), _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(), _stream(stream)),
+           "qtea_grouped_gemv")
+
+
+@dataclass
+class GroupedPlan:
+    info: QteaGroupedInfo
+    plan: object       # torch uint8 device tensor
+    workspace: object  # torch uint8 device tensor (zero-filled)
+
+    def run(self, stream=None):
+        qtea_grouped_gemv(self.info, self.plan, self.workspace, stream=stream)
+
+
+def plan_grouped(mats, xs, ys, batch: int = 1, stream=None) -> GroupedPlan:
+    """Plan a grouped GEMV over PackedMatrix objects `mats` with activations
+    `xs` and outputs `ys`; allocates the plan and a zeroed workspace."""
+    import torch
+
+    dev = mats[0].packed.device
+    plan = torch.empty(qtea_grouped_plan_bytes(len(mats)), dtype=torch.uint8, device=dev)
+    info = qtea_grouped_plan([m.desc for m in mats], [m.packed for m in mats], xs, ys, batch, plan,
+                             stream=stream)
+    ws = torch.zeros(max(int(info.workspace_bytes), 4), dtype=torch.uint8, device=dev)
+    return GroupedPlan(info, plan, ws)
 
 
 # ---------------------------------------------------------------------------

@@ -1,0 +1,630 @@
+// Grouped GEMV: y_m = W_m x_m for a list of independent problems in one
+// persistent launch (Eq. 10 with one group and zero bias, plus the Eq. 11
+// residual, for every problem of the list).
+//
+// Work unit = (problem, panel of kRowsPerPanel rows, K slice of 8 sixteen-pack
+// groups = 128 packs = 640 columns).  Units are ordered (problem, panel,
+// slice) with the slice fastest and cut into one contiguous run per
+// workgroup, balanced by weight bytes.  A workgroup walks its run:
+//
+//   - stage a_j = v_j x_j and x_j of the slice in LDS;
+//   - build the full 243-entry table of each of the slice's 128 packs
+//     (124,416 bytes of LDS, one fp32 entry per code and pack);
+//   - add one table entry per packed byte of the panel's rows, the entry
+//     address formed from the byte by a single v_perm_b32;
+//   - add the slice's salient residual;
+//   - at the panel's last slice, write y = alpha * acc + residual.
+//
+// While a unit is processed, the next unit's packed bytes, activations and
+// row scales are already in flight (two register buffers, ping-pong), so
+// the weight stream does not stop at unit, panel or problem boundaries.
+// A panel whose slices are split between two runs is reduced through the
+// workspace: each part stores its partial rows, the last part to arrive
+// sums the parts in run order and writes y (fixed order: deterministic).
+// No workgroup ever waits for another one.
+#include <stdlib.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "qtea_internal.h"
+
+namespace {
+
+using namespace qtea_detail;
+
+constexpr int kGT = 512;                                  // threads per workgroup
+constexpr int kGW = kGT / 64;                             // waves per workgroup
+constexpr int kSliceGroups = 8;                           // groups per K slice
+constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 128
+constexpr int kSliceCols = kSliceGroups * kGroupCols;     // 640
+constexpr int kBlockBytes = kCodes * 256;                 // tables of 64 packs: code row = 256 B
+constexpr int kTabBytes = 2 * kBlockBytes;                // 124,416
+constexpr int kBuildTasks = kSlicePacks * 9;              // (pack, two leading digits)
+constexpr uint32_t kGPlanMagic = 0x51475250u;            // "QGRP"
+constexpr int64_t kPlanProblemsOff = 256;
+
+struct GProblem {
+  const uint8_t* trits;
+  const uint16_t* alpha;
+  const uint16_t* v;
+  const int32_t* S;
+  const int32_t* spos;
+  const uint16_t* rval;
+  const uint32_t* ridx;
+  const uint16_t* x;
+  float* y;
+  int64_t N, K, n_pad;
+  int32_t n_groups, nS, n_slices, n_panels;
+  int64_t unit_base;
+  int64_t reserved;
+};
+static_assert(sizeof(GProblem) == 128, "plan record size");
+
+struct GPlanHeader {
+  uint32_t magic, version;
+  int32_t n_problems, n_wg, rows_per_panel, max_parts, batch, reserved0;
+  int64_t n_units, off_ranges;
+};
+
+template <int RB>
+struct GLds {
+  static constexpr int RP = kGW * 16 * RB;  // rows per panel
+  static constexpr int QR = kGT / (RP / 4);  // residual lanes per four-row group
+  static constexpr int RPS = RP + 1;     // row stride of the residual slots
+  static constexpr int A = kTabBytes;                     // a_j, fp32 [640]
+  static constexpr int XR = A + 4 * kSliceCols;           // x_j, fp32 [640]
+  static constexpr int RR = XR + 4 * kSliceCols;          // residual slots fp32 [QR][RPS]
+  static constexpr int FLAG = RR + 4 * QR * RPS;          // one int
+  static constexpr int BYTES = FLAG + 16;
+};
+
+typedef __attribute__((address_space(1))) const uint8_t gu8;
+typedef __attribute__((address_space(1))) const uint16_t gu16;
+typedef __attribute__((address_space(1))) const uint32_t gu32;
+typedef __attribute__((address_space(1))) const int32_t gi32;
+typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+
+// Pointers read from the plan are generic; loads through them would be flat
+// loads (which also hold the LDS wait counter).  They all point to global
+// memory, so they are cast to the global address space.
+__device__ __forceinline__ gu8* gptr(const uint8_t* p) { return (gu8*)p; }
+__device__ __forceinline__ gu16* gptr(const uint16_t* p) { return (gu16*)p; }
+__device__ __forceinline__ gu32* gptr(const uint32_t* p) { return (gu32*)p; }
+__device__ __forceinline__ gi32* gptr(const int32_t* p) { return (gi32*)p; }
+
+struct Cursor {
+  int m, panel, slice;
+};
+
+__device__ __forceinline__ Cursor advance(Cursor c, const GProblem* P) {
+  if (++c.slice == P[c.m].n_slices) {
+    c.slice = 0;
+    if (++c.panel == P[c.m].n_panels) {
+      c.panel = 0;
+      ++c.m;
+    }
+  }
+  return c;
+}
+
+// Selector of v_perm_b32 that forms (byte k of src1) << 8 | (byte k of src0).
+__device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
+  return 0x0C0C0000u | (uint32_t(k) << 8) | uint32_t(4 + k);
+}
+
+template <int RB>
+__global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __restrict__ plan,
+                                                           float* __restrict__ part,
+                                                           uint32_t* __restrict__ counters) {
+  using L = GLds<RB>;
+  constexpr int RP = L::RP, QR = L::QR, RPS = L::RPS;
+  extern __shared__ float smem[];
+  char* lds = reinterpret_cast<char*>(smem);
+  float* a_lds = reinterpret_cast<float*>(lds + L::A);
+  float* xr_lds = reinterpret_cast<float*>(lds + L::XR);
+  float* rres = reinterpret_cast<float*>(lds + L::RR);
+  int* flag = reinterpret_cast<int*>(lds + L::FLAG);
+
+  const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
+  const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
+  const int64_t* ranges = reinterpret_cast<const int64_t*>(plan + H->off_ranges);
+  const int g = blockIdx.x;
+  const int64_t ub = ranges[g], ue = ranges[g + 1];
+  if (ub >= ue) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, l16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wt = w >> 2, wr = w & 3;  // tile of the wave's first row block, block in its tile
+  // residual lane mapping: four-row group gi of the panel, lane rq among its QR lanes
+  const int gi = tid / QR, rq = tid - gi * QR;
+
+  // table slot bytes of this lane: byte k of slotreg[d] = 4 * (16 q + ((4 d + k + l16) mod 16))
+  uint32_t slotreg[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    uint32_t r = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) r |= uint32_t(4 * (16 * q + ((4 * d + k + l16) & 15))) << (8 * k);
+    slotreg[d] = r;
+  }
+
+  Cursor cur;
+  {
+    int m = 0;
+    while (P[m].unit_base + int64_t(P[m].n_slices) * P[m].n_panels <= ub) ++m;
+    const int64_t local = ub - P[m].unit_base;
+    cur.m = m;
+    cur.panel = int(local / P[m].n_slices);
+    cur.slice = int(local - int64_t(cur.panel) * P[m].n_slices);
+  }
+
+  // Every load below is unconditional, from an index clamped into its array:
+  // groups past the matrix read a real group whose table entries are zero
+  // (a_j = 0 past the last column), rows past n_pad feed only rows that are
+  // never stored, and columns past K are replaced by zero after the load.
+  // activations: this thread stages slice columns tid + kGT * i (fp16 x | fp16 v << 16)
+  constexpr int XI = (kSliceCols + kGT - 1) / kGT;
+  auto load_xv = [&](const Cursor c, uint32_t (&xv)[XI]) {
+    const GProblem& pr = P[c.m];
+    const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      const uint32_t col = uint32_t(c.slice * kSliceCols + tid + kGT * i);
+      const uint32_t xb = gptr(pr.x)[col < kx ? col : kx - 1];
+      const uint32_t vb = gptr(pr.v)[col < kv ? col : kv - 1];
+      xv[i] = (col < kx ? xb : 0u) | ((col < kv ? vb : 0u) << 16);
+    }
+  };
+  // row blocks finalized by this lane: t = q + 4 i, i < RF
+  constexpr int RF = RB / 4;
+  static_assert(RB % 4 == 0, "four quarters share the finalization");
+  auto load_alpha = [&](const Cursor c, uint16_t (&al)[RF]) {
+    const GProblem& pr = P[c.m];
+    const uint32_t np = uint32_t(pr.n_pad);
+#pragma unroll
+    for (int i = 0; i < RF; ++i) {
+      const uint32_t rowq = uint32_t(c.panel * RP + (w + kGW * (q + 4 * i)) * 16 + l16);
+      al[i] = gptr(pr.alpha)[rowq < np ? rowq : np - 1];
+    }
+  };
+  // byte offset of the 16-byte unit (row block t, group j of the quarter) of unit c
+  auto w_off = [&](const Cursor c, int t, int j) -> uint32_t {
+    const GProblem& pr = P[c.m];
+    const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
+    const int grp0 = c.slice * kSliceGroups + q + 4 * j;
+    const int grp = grp0 < ng ? grp0 : ng - 1;
+    const int tl0 = c.panel * (RP / 64) + wt + (kGW / 4) * t;
+    const int tl = tl0 < n_tiles ? tl0 : n_tiles - 1;
+    return (uint32_t(tl * ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks;
+  };
+  auto load_w = [&](const Cursor c, int t, int j) -> u32x4 {
+    return __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[c.m].trits) + w_off(c, t, j)));
+  };
+  // Table entry at LDS byte address `a`.  The kernel has no static LDS, so
+  // the dynamic allocation (the tables first) starts at address 0.
+  auto tab_at = [](uint32_t a) -> float { return *(const lds_float*)(size_t(a)); };
+
+  u32x4 W[RB][2];
+  uint32_t xv[XI];
+  load_xv(cur, xv);
+#pragma unroll
+  for (int t = 0; t < RB; ++t)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) W[t][j] = load_w(cur, t, j);
+  uint16_t al[RF];
+  load_alpha(cur, al);
+
+  float acc[RB];
+#pragma unroll
+  for (int t = 0; t < RB; ++t) acc[t] = 0.0f;
+  int pstart_slice = cur.slice;  // first slice of the open panel in this run
+
+  for (int64_t u = ub; u < ue; ++u) {
+    const GProblem& pr = P[cur.m];
+    const bool has_next = u + 1 < ue;
+    const Cursor nxt = has_next ? advance(cur, P) : cur;
+    const bool pstart = (cur.slice == 0) || (u == ub);
+    const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
+    if (pstart) pstart_slice = cur.slice;
+
+    // 1. stage the slice's activations
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      const int col = tid + kGT * i;
+      if (col < kSliceCols) {
+        const float xf = h2f(uint16_t(xv[i] & 0xffffu));
+        const float vf = h2f(uint16_t(xv[i] >> 16));
+        a_lds[col] = vf * xf;
+        xr_lds[col] = xf;
+      }
+    }
+    __syncthreads();
+
+    // 2. tables: task (pack p, leading digits d4 d3) writes the 27 codes sharing them
+#pragma unroll
+    for (int it = 0; it < (kBuildTasks + kGT - 1) / kGT; ++it) {
+      const int task = tid + it * kGT;
+      if (task < kBuildTasks) {
+        const int p = task & (kSlicePacks - 1);
+        const int top = task >> 7;
+        const int d4 = (top * 11) >> 5;
+        const int d3 = top - 3 * d4;
+        const float a0 = a_lds[5 * p], a1 = a_lds[5 * p + 1], a2 = a_lds[5 * p + 2];
+        const float a3 = a_lds[5 * p + 3], a4 = a_lds[5 * p + 4];
+        const float t4 = d4 == 0 ? -a4 : (d4 == 2 ? a4 : 0.0f);
+        const float t3 = d3 == 0 ? -a3 : (d3 == 2 ? a3 : 0.0f);
+        const float base = t4 + t3;
+        lds_char* dst = (lds_char*)smem + (p >> 6) * kBlockBytes + (p & 63) * 4 + (27 * d3 + 81 * d4) * 256;
+#pragma unroll
+        for (int e2 = 0; e2 < 3; ++e2) {
+          const float u2 = e2 == 0 ? base - a2 : (e2 == 1 ? base : base + a2);
+#pragma unroll
+          for (int e1 = 0; e1 < 3; ++e1) {
+            const float u1 = e1 == 0 ? u2 - a1 : (e1 == 1 ? u2 : u2 + a1);
+#pragma unroll
+            for (int e0 = 0; e0 < 3; ++e0) {
+              const float u0 = e0 == 0 ? u1 - a0 : (e0 == 1 ? u1 : u1 + a0);
+              *(lds_float*)(dst + (9 * e2 + 3 * e1 + e0) * 256) = u0;
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);  // nine entries at a time (register pressure)
+        }
+      }
+    }
+    __syncthreads();
+
+    // 3. residual loads of this slice (issued before any load of the next unit)
+    const int g0 = cur.slice * kSliceGroups;
+    const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
+    const int s_lo = gptr(pr.spos)[g0], s_hi = gptr(pr.spos)[g1];
+    const int grow = cur.panel * (RP / 4) + gi;  // global four-row group
+    const bool grow_ok = grow * 4 < pr.n_pad;
+    constexpr int RES_B = 4;
+    uint32_t rv[RES_B], ri[RES_B];
+    int rs[RES_B];
+    if (s_hi > s_lo) {
+      const uint32_t growc = uint32_t(grow_ok ? grow : 0);
+      const uint32_t nS = uint32_t(pr.nS);
+#pragma unroll
+      for (int i = 0; i < RES_B; ++i) {
+        const int s = s_lo + rq + QR * i;
+        const bool ok = grow_ok && s < s_hi;
+        const uint32_t sc = uint32_t(s < s_hi ? s : s_hi - 1);
+        rv[i] = gptr(pr.rval)[growc * nS + sc];
+        ri[i] = gptr(pr.ridx)[(growc >> 4) * nS + sc];
+        const int sv = gptr(pr.S)[sc];
+        rs[i] = ok ? sv : -1;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < RES_B; ++i) {
+        rv[i] = 0;
+        ri[i] = 0;
+        rs[i] = -1;
+      }
+    }
+
+    // 4. the next unit's activations and row scales (nxt == cur after the
+    // run's last unit: harmless reloads, no branch)
+    uint32_t xv_n[XI];
+    uint16_t al_n[RF];
+    load_xv(nxt, xv_n);
+    load_alpha(nxt, al_n);
+
+    // 5. lookups; each 16-byte unit, once read, is refilled with the next
+    // unit's bytes.  After the run's last unit the refill reads one 16-byte
+    // unit for all lanes (no branch, no traffic worth counting).
+    const GProblem& pn = P[nxt.m];
+    const gu8* nbase = gptr(pn.trits);
+    const int n_ng = pn.n_groups, n_nt = int(pn.n_pad >> 6);
+    const int n_g0 = nxt.slice * kSliceGroups + q, n_t0 = nxt.panel * (RP / 64) + wt;
+    const uint32_t nmask = has_next ? 0xffffffffu : 0u;
+#pragma unroll
+    for (int t = 0; t < RB; ++t) acc[t] = pstart ? 0.0f : acc[t];
+#pragma unroll
+    for (int t = 0; t < RB; ++t) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const u32x4 wv = W[t][j];
+        const int grp = min(n_g0 + 4 * j, n_ng - 1);
+        const int tl = min(n_t0 + (kGW / 4) * t, n_nt - 1);
+        const uint32_t noff = ((uint32_t(tl * n_ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & nmask;
+        W[t][j] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(nbase + noff));
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const uint32_t wd = wv[d];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t addr = __builtin_amdgcn_perm(slotreg[d], wd, perm_sel(k));
+            acc[t] += tab_at(addr + j * kBlockBytes);
+          }
+        }
+        // keep the sums here: without a use in this block the compiler sinks
+        // all of a unit's adds below the residual and holds every table
+        // entry of the unit in registers
+        asm volatile("" : "+v"(acc[t]));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // 6. residual: each lane adds into its own slots (program order: deterministic)
+    float* myres = rres + rq * RPS + 4 * gi;
+    if (pstart) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) myres[i] = 0.0f;
+    }
+    const int col0 = cur.slice * kSliceCols;
+    const uint32_t gsh = 2u * uint32_t(grow & 15);
+#pragma unroll
+    for (int i = 0; i < RES_B; ++i) {
+      const bool ok = rs[i] >= 0;
+      const float xs = xr_lds[ok ? rs[i] - col0 : 0];
+      const float t = ok ? h2f(uint16_t(rv[i])) * xs : 0.0f;
+      const uint32_t idx = (ri[i] >> gsh) & 3u;
+      myres[idx] += t;
+    }
+    if (grow_ok) {
+      for (int s = s_lo + rq + QR * RES_B; s < s_hi; s += QR) {  // more than RES_B per lane (rare)
+        const float t = h2f(gptr(pr.rval)[grow * pr.nS + s]) * xr_lds[gptr(pr.S)[s] - col0];
+        const uint32_t idx = (gptr(pr.ridx)[(grow >> 4) * pr.nS + s] >> gsh) & 3u;
+        myres[idx] += t;
+      }
+    }
+    __syncthreads();
+
+    // 7. panel end: y = alpha * acc + residual (or a partial of a split panel)
+    if (pend) {
+      float tot[RB];
+#pragma unroll
+      for (int t = 0; t < RB; ++t) {
+        const float s2 = acc[t] + __shfl_xor(acc[t], 16);
+        tot[t] = s2 + __shfl_xor(s2, 32);
+      }
+      float val[RF];
+      int prow[RF];
+#pragma unroll
+      for (int i = 0; i < RF; ++i) {
+        float mine = tot[4 * i];
+#pragma unroll
+        for (int k = 1; k < 4; ++k)
+          if (q == k) mine = tot[4 * i + k];
+        prow[i] = (w + kGW * (q + 4 * i)) * 16 + l16;
+        float r = 0.0f;
+#pragma unroll
+        for (int k = 0; k < QR; ++k) r += rres[k * RPS + prow[i]];
+        val[i] = h2f(al[i]) * mine + r;
+      }
+      float* y = pr.y;
+      const int64_t row0 = int64_t(cur.panel) * RP;
+      const bool owned = pstart_slice == 0 && cur.slice == pr.n_slices - 1;
+      if (owned) {
+#pragma unroll
+        for (int i = 0; i < RF; ++i)
+          if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
+      } else {
+        // split panel: parts are the runs that hold any of its units
+        const int64_t p0 = pr.unit_base + int64_t(cur.panel) * pr.n_slices;
+        const int64_t p1 = p0 + pr.n_slices;
+        int ga = g;
+        while (ranges[ga] > p0) --ga;
+        int gb = g;
+        while (ranges[gb + 1] < p1) ++gb;
+        int nparts = 0, mypart = 0;
+        for (int k = ga; k <= gb; ++k) {
+          if (ranges[k] < ranges[k + 1]) {
+            if (k == g) mypart = nparts;
+            ++nparts;
+          }
+        }
+        float* slot = part + (int64_t(ga) * H->max_parts) * RP;
+#pragma unroll
+        for (int i = 0; i < RF; ++i) store_coherent(slot + int64_t(mypart) * RP + prow[i], val[i]);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (tid == 0) {
+          const uint32_t prev = __hip_atomic_fetch_add(counters + ga, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          *flag = prev == uint32_t(nparts - 1);
+        }
+        __syncthreads();
+        if (*flag) {
+#pragma unroll
+          for (int i = 0; i < RF; ++i) {
+            float sum = 0.0f;
+            for (int k = 0; k < nparts; ++k) sum += load_coherent(slot + int64_t(k) * RP + prow[i]);
+            if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = sum;
+          }
+          if (tid == 0) __hip_atomic_store(counters + ga, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < XI; ++i) xv[i] = xv_n[i];
+#pragma unroll
+    for (int i = 0; i < RF; ++i) al[i] = al_n[i];
+    cur = nxt;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host planning.
+// ---------------------------------------------------------------------------
+constexpr int kMaxRB = 8;
+
+int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
+  *n_slices = int(cdiv(d.n_groups, kSliceGroups));
+  *n_panels = int(cdiv(d.n_pad, RP));
+  return *n_slices * *n_panels;
+}
+
+int cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return n;
+}
+
+template <int RB>
+hipError_t launch_grouped(const uint8_t* plan, int grid, float* part, uint32_t* counters, hipStream_t st) {
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, GLds<RB>::BYTES);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL(grouped_gemv_kernel<RB>, dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan, part, counters);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes) {
+  if (!out_bytes || n_problems < 1) return QTEA_ERR_INVALID_ARG;
+  const int G = cu_count();
+  if (G < 1) return QTEA_ERR_HIP;
+  *out_bytes = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign) + 8 * int64_t(G + 1);
+  return QTEA_OK;
+}
+
+int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const uint16_t* const* x,
+                      float* const* y, int n_problems, int batch, void* plan, int64_t plan_bytes,
+                      qtea_grouped_info* info, void* stream) {
+  if (!descs || !packed || !x || !y || !plan || !info || n_problems < 1) return QTEA_ERR_INVALID_ARG;
+  info->magic = 0;
+  if (batch != 1) return QTEA_ERR_BATCH;
+  int64_t need = 0;
+  const int st_plan = qtea_grouped_plan_bytes(n_problems, &need);
+  if (st_plan != QTEA_OK) return st_plan;
+  if (plan_bytes < need) return QTEA_ERR_WORKSPACE;
+  const int G = cu_count();
+  for (int m = 0; m < n_problems; ++m)
+    if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
+
+  // rows per panel: the largest that still gives every workgroup several units
+  int RB = kMaxRB;
+  for (; RB > 4; RB /= 2) {
+    int64_t units = 0;
+    for (int m = 0; m < n_problems; ++m) {
+      int ns, np;
+      units += units_for(descs[m], GLds<kMaxRB>::RP / kMaxRB * RB, &ns, &np);
+    }
+    if (units >= 4 * int64_t(G)) break;
+  }
+  const int RP = GLds<kMaxRB>::RP / kMaxRB * RB;
+
+  const int64_t off_ranges = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
+  uint8_t* hbuf = static_cast<uint8_t*>(calloc(1, size_t(need)));
+  if (!hbuf) return QTEA_ERR_INVALID_ARG;
+  GPlanHeader* H = reinterpret_cast<GPlanHeader*>(hbuf);
+  GProblem* P = reinterpret_cast<GProblem*>(hbuf + kPlanProblemsOff);
+  int64_t* ranges = reinterpret_cast<int64_t*>(hbuf + off_ranges);
+
+  // unit costs: packed bytes of the unit plus a fixed table-build share
+  std::vector<int64_t> unit_cost;
+  int64_t total_units = 0;
+  for (int m = 0; m < n_problems; ++m) {
+    const qtea_desc& d = descs[m];
+    const uint8_t* pk = static_cast<const uint8_t*>(packed[m]);
+    GProblem& pr = P[m];
+    pr.trits = pk + d.off_trits;
+    pr.alpha = reinterpret_cast<const uint16_t*>(pk + d.off_alpha);
+    pr.v = reinterpret_cast<const uint16_t*>(pk + d.off_v);
+    pr.S = reinterpret_cast<const int32_t*>(pk + d.off_salient);
+    pr.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
+    pr.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
+    pr.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
+    pr.x = x[m];
+    pr.y = y[m];
+    pr.N = d.N;
+    pr.K = d.K;
+    pr.n_pad = d.n_pad;
+    pr.n_groups = int32_t(d.n_groups);
+    pr.nS = int32_t(d.n_salient);
+    int ns, np;
+    units_for(d, RP, &ns, &np);
+    pr.n_slices = ns;
+    pr.n_panels = np;
+    pr.unit_base = total_units;
+    for (int p = 0; p < np; ++p) {
+      const int64_t rows = std::min<int64_t>(RP, d.n_pad - int64_t(p) * RP);
+      for (int s = 0; s < ns; ++s) {
+        const int64_t groups = std::min<int64_t>(kSliceGroups, d.n_groups - int64_t(s) * kSliceGroups);
+        unit_cost.push_back(rows * groups * kGroupPacks + 16384);
+      }
+    }
+    total_units += int64_t(ns) * np;
+  }
+  // contiguous runs of balanced cost
+  int64_t total_cost = 0;
+  for (int64_t c : unit_cost) total_cost += c;
+  {
+    int64_t acc = 0, u = 0;
+    ranges[0] = 0;
+    for (int k = 1; k < G; ++k) {
+      const int64_t target = (total_cost * k) / G;
+      while (u < total_units && acc + unit_cost[size_t(u)] / 2 <= target) acc += unit_cost[size_t(u++)];
+      ranges[k] = u;
+    }
+    ranges[G] = total_units;
+  }
+  // largest number of runs sharing one panel
+  int max_parts = 1;
+  for (int m = 0; m < n_problems; ++m) {
+    for (int p = 0; p < P[m].n_panels; ++p) {
+      const int64_t p0 = P[m].unit_base + int64_t(p) * P[m].n_slices, p1 = p0 + P[m].n_slices;
+      int parts = 0;
+      for (int k = 0; k < G; ++k)
+        if (ranges[k] < ranges[k + 1] && ranges[k] < p1 && ranges[k + 1] > p0) ++parts;
+      if (parts > max_parts) max_parts = parts;
+    }
+  }
+  H->magic = kGPlanMagic;
+  H->version = 1;
+  H->n_problems = n_problems;
+  H->n_wg = G;
+  H->rows_per_panel = RP;
+  H->max_parts = max_parts;
+  H->batch = batch;
+  H->n_units = total_units;
+  H->off_ranges = off_ranges;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(plan, hbuf, size_t(need), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  free(hbuf);
+  if (e != hipSuccess) return QTEA_ERR_HIP;
+
+  info->magic = kGPlanMagic;
+  info->n_problems = n_problems;
+  info->batch = batch;
+  info->grid = G;
+  info->rows_per_panel = RP;
+  info->max_parts = max_parts;
+  info->n_units = total_units;
+  info->plan_bytes = need;
+  info->workspace_bytes = align_up(4 * int64_t(G), kAlign) + int64_t(G) * max_parts * RP * 4;
+  return QTEA_OK;
+}
+
+int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* workspace,
+                      int64_t workspace_bytes, void* stream) {
+  if (!info || info->magic != kGPlanMagic || !plan) return QTEA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < info->workspace_bytes) return QTEA_ERR_WORKSPACE;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
+  float* part = reinterpret_cast<float*>(ws + align_up(4 * int64_t(info->grid), kAlign));
+  const uint8_t* pl = static_cast<const uint8_t*>(plan);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  switch (info->rows_per_panel) {
+    case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, part, counters, st); break;
+    case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, part, counters, st); break;
+    default: return QTEA_ERR_INVALID_ARG;
+  }
+  return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -25,86 +25,12 @@
 // salient residual of the slice's columns is added in the same pass.  The
 // slice partials go to the workspace; the last workgroup of a row block to
 // arrive sums them in slice order (deterministic) and writes y.
-#include <hip/hip_runtime.h>
-
-#include <stdint.h>
-
-#include "qtea.h"
+#include "qtea_internal.h"
 
 namespace {
 
-constexpr int kGroupPacks = 16;
-constexpr int kGroupCols = 80;   // 16 packs x 5 columns
-constexpr int kTileRows = 64;    // one row per lane of a wavefront
-constexpr int kCodes = 243;      // 3^5
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * 64;
-constexpr uint32_t kZeroCode4 = 0x79797979u;  // four copies of code 121 (all-zero trits)
-constexpr int kLayout = 1;
-constexpr int64_t kAlign = 256;
-constexpr int64_t kHeaderBytes = 256;
-constexpr int kFlagOffset = 128;
+using namespace qtea_detail;
 
-constexpr uint32_t kFlagBadTrit = 1u;
-constexpr uint32_t kFlagBadResid = 2u;
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-typedef __attribute__((address_space(3))) char lds_char;
-typedef __attribute__((address_space(3))) float lds_float;
-
-inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
-inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
-__device__ __forceinline__ float h2f(uint16_t h) {
-  _Float16 v;
-  __builtin_memcpy(&v, &h, 2);
-  return (float)v;
-}
-
-// ---------------------------------------------------------------------------
-// Layout arithmetic shared by the host entry points.
-// ---------------------------------------------------------------------------
-struct Layout {
-  int64_t n_packs, n_groups, n_pad, n_tiles;
-  int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx, total;
-};
-
-bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L) {
-  if (N < 4 || N % 4 != 0 || K < 1 || nS < 0 || nS > K) return false;
-  if (N > (int64_t(1) << 31) - 64 || K > (int64_t(1) << 31) - 80) return false;
-  L->n_packs = cdiv(K, 5);
-  L->n_groups = cdiv(L->n_packs, kGroupPacks);
-  L->n_pad = align_up(N, kTileRows);
-  L->n_tiles = L->n_pad / kTileRows;
-  int64_t o = kHeaderBytes;
-  L->off_trits = o;
-  o = align_up(o + L->n_pad * L->n_groups * kGroupPacks, kAlign);
-  L->off_alpha = o;
-  o = align_up(o + 2 * L->n_pad, kAlign);
-  L->off_v = o;
-  o = align_up(o + 2 * L->n_groups * kGroupCols, kAlign);
-  L->off_salient = o;
-  o = align_up(o + 4 * nS, kAlign);
-  L->off_spos = o;
-  o = align_up(o + 4 * (L->n_groups + 1), kAlign);
-  L->off_rval = o;
-  o = align_up(o + 2 * nS * (L->n_pad / 4), kAlign);
-  L->off_ridx = o;
-  o = align_up(o + 4 * nS * (L->n_pad / 64), kAlign);
-  L->total = o;
-  return true;
-}
-
-bool desc_ok(const qtea_desc* d) {
-  if (!d || d->magic != QTEA_DESC_MAGIC || d->layout != kLayout) return false;
-  Layout L;
-  if (!make_layout(d->N, d->K, d->n_salient, &L)) return false;
-  return L.total == d->bytes_total && L.off_trits == d->off_trits && L.off_alpha == d->off_alpha &&
-         L.off_v == d->off_v && L.off_salient == d->off_salient && L.off_spos == d->off_spos &&
-         L.off_rval == d->off_rval && L.off_ridx == d->off_ridx && L.n_pad == d->n_pad &&
-         L.n_groups == d->n_groups && L.n_packs == d->n_packs;
-}
 
 // ---------------------------------------------------------------------------
 // Packing kernels (offline).
@@ -301,12 +227,6 @@ struct Cfg {
 
 constexpr int kResBatch = 8;  // salient columns whose loads are issued together
 
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_coherent(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Leaves of the digit tree below `t`: digit DIG (and the ones below it)
 // enumerated at compile time; the value of code offset OFF + d * 3^DIG is
