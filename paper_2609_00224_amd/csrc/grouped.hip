@@ -33,7 +33,7 @@ namespace {
 
 using namespace qtea_detail;
 
-constexpr int kGT = 512;                                  // threads per workgroup
+constexpr int kGT = 1024;                                 // threads per workgroup
 constexpr int kGW = kGT / 64;                             // waves per workgroup
 constexpr int kSliceGroups = 8;                           // groups per K slice
 constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 128
@@ -60,6 +60,7 @@ struct GProblem {
   int64_t reserved;
 };
 static_assert(sizeof(GProblem) == 128, "plan record size");
+static_assert(kSliceCols % 64 == 0 && kBuildTasks % 64 == 0, "passes of whole waves");
 
 struct GPlanHeader {
   uint32_t magic, version;
@@ -84,6 +85,7 @@ typedef __attribute__((address_space(1))) const uint16_t gu16;
 typedef __attribute__((address_space(1))) const uint32_t gu32;
 typedef __attribute__((address_space(1))) const int32_t gi32;
 typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+typedef __attribute__((address_space(1))) float gf32;
 
 // Pointers read from the plan are generic; loads through them would be flat
 // loads (which also hold the LDS wait counter).  They all point to global
@@ -92,6 +94,10 @@ __device__ __forceinline__ gu8* gptr(const uint8_t* p) { return (gu8*)p; }
 __device__ __forceinline__ gu16* gptr(const uint16_t* p) { return (gu16*)p; }
 __device__ __forceinline__ gu32* gptr(const uint32_t* p) { return (gu32*)p; }
 __device__ __forceinline__ gi32* gptr(const int32_t* p) { return (gi32*)p; }
+// Read-only and read with a uniform index: the constant address space lets
+// the compiler use scalar loads, which do not wait behind the vector loads.
+typedef __attribute__((address_space(4))) const int32_t ci32;
+__device__ __forceinline__ ci32* cptr(const int32_t* p) { return (ci32*)p; }
 
 struct Cursor {
   int m, panel, slice;
@@ -159,65 +165,91 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     cur.slice = int(local - int64_t(cur.panel) * P[m].n_slices);
   }
 
-  // Every load below is unconditional, from an index clamped into its array:
-  // groups past the matrix read a real group whose table entries are zero
-  // (a_j = 0 past the last column), rows past n_pad feed only rows that are
-  // never stored, and columns past K are replaced by zero after the load.
-  // activations: this thread stages slice columns tid + kGT * i (fp16 x | fp16 v << 16)
-  constexpr int XI = (kSliceCols + kGT - 1) / kGT;
-  auto load_xv = [&](const Cursor c, uint32_t (&xv)[XI]) {
+  // Loads.  Every load is unconditional, from an index clamped into its
+  // array (groups past the matrix read a real group whose table entries are
+  // zero since a_j = 0 past the last column; rows past n_pad feed only rows
+  // that are never stored; values past a range are ignored after the load),
+  // so that every path through the unit loop issues the same loads and the
+  // compiler's wait counts stay exact: a wait for one value then never also
+  // waits for the next unit's weights, which are the youngest loads.
+
+  // activations: this thread stages slice column tid (kept as loaded, checked when staged)
+  static_assert(kSliceCols <= kGT, "one staged column per thread");
+  auto load_xv = [&](const Cursor c, uint16_t& xr, uint16_t& vr) {
     const GProblem& pr = P[c.m];
     const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
-#pragma unroll
-    for (int i = 0; i < XI; ++i) {
-      const uint32_t col = uint32_t(c.slice * kSliceCols + tid + kGT * i);
-      const uint32_t xb = gptr(pr.x)[col < kx ? col : kx - 1];
-      const uint32_t vb = gptr(pr.v)[col < kv ? col : kv - 1];
-      xv[i] = (col < kx ? xb : 0u) | ((col < kv ? vb : 0u) << 16);
-    }
+    const uint32_t col = uint32_t(c.slice * kSliceCols + tid);
+    xr = gptr(pr.x)[col < kx ? col : kx - 1];
+    vr = gptr(pr.v)[col < kv ? col : kv - 1];
   };
-  // row blocks finalized by this lane: t = q + 4 i, i < RF
-  constexpr int RF = RB / 4;
-  static_assert(RB % 4 == 0, "four quarters share the finalization");
+  // row scales of the row blocks this lane finalizes: t = q + 4 i
+  constexpr int RF = RB >= 4 ? RB / 4 : 1;
   auto load_alpha = [&](const Cursor c, uint16_t (&al)[RF]) {
     const GProblem& pr = P[c.m];
     const uint32_t np = uint32_t(pr.n_pad);
 #pragma unroll
     for (int i = 0; i < RF; ++i) {
-      const uint32_t rowq = uint32_t(c.panel * RP + (w + kGW * (q + 4 * i)) * 16 + l16);
+      const int t = (q + 4 * i) < RB ? q + 4 * i : 0;
+      const uint32_t rowq = uint32_t(c.panel * RP + (w + kGW * t) * 16 + l16);
       al[i] = gptr(pr.alpha)[rowq < np ? rowq : np - 1];
+    }
+  };
+  // salient residual of unit c, this lane's share: columns s = s_lo + rq + QR i
+  // of the slice, four-row group gi of the panel
+  constexpr int RES_B = 5;
+  uint32_t rv[RES_B], ri[RES_B];
+  int rs[RES_B];
+  auto load_res = [&](const Cursor c) {
+    const GProblem& pr = P[c.m];
+    const int g0 = c.slice * kSliceGroups;
+    const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
+    const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
+    const bool any = pr.nS > 0;  // without salient columns read the row scales (any valid address)
+    const int grow = c.panel * (RP / 4) + gi;
+    const uint32_t growc = uint32_t(grow * 4 < pr.n_pad ? grow : 0);
+    const uint32_t nS = uint32_t(pr.nS);
+    gu16* rvb = any ? gptr(pr.rval) : gptr(pr.alpha);
+    gu32* rib = any ? gptr(pr.ridx) : (gu32*)gptr(pr.alpha);
+    gi32* sb = any ? gptr(pr.S) : (gi32*)gptr(pr.alpha);
+    const uint32_t gofs = any ? growc * nS : 0u, tofs = any ? (growc >> 4) * nS : 0u;
+#pragma unroll
+    for (int i = 0; i < RES_B; ++i) {
+      const int s = s_lo + rq + QR * i;
+      const uint32_t sc = any ? uint32_t(max(min(s, s_hi - 1), 0)) : 0u;
+      rv[i] = rvb[gofs + sc];
+      ri[i] = rib[tofs + sc];
+      rs[i] = sb[sc];
     }
   };
   // byte offset of the 16-byte unit (row block t, group j of the quarter) of unit c
   auto w_off = [&](const Cursor c, int t, int j) -> uint32_t {
     const GProblem& pr = P[c.m];
     const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
-    const int grp0 = c.slice * kSliceGroups + q + 4 * j;
-    const int grp = grp0 < ng ? grp0 : ng - 1;
-    const int tl0 = c.panel * (RP / 64) + wt + (kGW / 4) * t;
-    const int tl = tl0 < n_tiles ? tl0 : n_tiles - 1;
+    const int grp = min(c.slice * kSliceGroups + q + 4 * j, ng - 1);
+    const int tl = min(c.panel * (RP / 64) + wt + (kGW / 4) * t, n_tiles - 1);
     return (uint32_t(tl * ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks;
-  };
-  auto load_w = [&](const Cursor c, int t, int j) -> u32x4 {
-    return __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[c.m].trits) + w_off(c, t, j)));
   };
   // Table entry at LDS byte address `a`.  The kernel has no static LDS, so
   // the dynamic allocation (the tables first) starts at address 0.
   auto tab_at = [](uint32_t a) -> float { return *(const lds_float*)(size_t(a)); };
 
   u32x4 W[RB][2];
-  uint32_t xv[XI];
-  load_xv(cur, xv);
+  uint16_t xr, vr;
+  load_xv(cur, xr, vr);
 #pragma unroll
   for (int t = 0; t < RB; ++t)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) W[t][j] = load_w(cur, t, j);
+    for (int j = 0; j < 2; ++j)
+      W[t][j] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, t, j)));
+  load_res(cur);
   uint16_t al[RF];
   load_alpha(cur, al);
 
-  float acc[RB];
+  float acc[RB], racc[4];
 #pragma unroll
   for (int t = 0; t < RB; ++t) acc[t] = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) racc[k] = 0.0f;
   int pstart_slice = cur.slice;  // first slice of the open panel in this run
 
   for (int64_t u = ub; u < ue; ++u) {
@@ -228,16 +260,13 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
     if (pstart) pstart_slice = cur.slice;
 
-    // 1. stage the slice's activations
-#pragma unroll
-    for (int i = 0; i < XI; ++i) {
-      const int col = tid + kGT * i;
-      if (col < kSliceCols) {
-        const float xf = h2f(uint16_t(xv[i] & 0xffffu));
-        const float vf = h2f(uint16_t(xv[i] >> 16));
-        a_lds[col] = vf * xf;
-        xr_lds[col] = xf;
-      }
+    // 1. stage the slice's activations: a_j = v_j x_j (exact in fp32) and x_j
+    if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
+      const int gcol = cur.slice * kSliceCols + tid;
+      const float xf = gcol < pr.K ? h2f(xr) : 0.0f;
+      const float vf = gcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
+      a_lds[tid] = vf * xf;
+      xr_lds[tid] = xf;
     }
     __syncthreads();
 
@@ -245,7 +274,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 #pragma unroll
     for (int it = 0; it < (kBuildTasks + kGT - 1) / kGT; ++it) {
       const int task = tid + it * kGT;
-      if (task < kBuildTasks) {
+      if (w * 64 + it * kGT < kBuildTasks) {  // whole waves (kBuildTasks is a multiple of 64)
         const int p = task & (kSlicePacks - 1);
         const int top = task >> 7;
         const int d4 = (top * 11) >> 5;
@@ -274,47 +303,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     }
     __syncthreads();
 
-    // 3. residual loads of this slice (issued before any load of the next unit)
-    const int g0 = cur.slice * kSliceGroups;
-    const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
-    const int s_lo = gptr(pr.spos)[g0], s_hi = gptr(pr.spos)[g1];
-    const int grow = cur.panel * (RP / 4) + gi;  // global four-row group
-    const bool grow_ok = grow * 4 < pr.n_pad;
-    constexpr int RES_B = 4;
-    uint32_t rv[RES_B], ri[RES_B];
-    int rs[RES_B];
-    if (s_hi > s_lo) {
-      const uint32_t growc = uint32_t(grow_ok ? grow : 0);
-      const uint32_t nS = uint32_t(pr.nS);
-#pragma unroll
-      for (int i = 0; i < RES_B; ++i) {
-        const int s = s_lo + rq + QR * i;
-        const bool ok = grow_ok && s < s_hi;
-        const uint32_t sc = uint32_t(s < s_hi ? s : s_hi - 1);
-        rv[i] = gptr(pr.rval)[growc * nS + sc];
-        ri[i] = gptr(pr.ridx)[(growc >> 4) * nS + sc];
-        const int sv = gptr(pr.S)[sc];
-        rs[i] = ok ? sv : -1;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < RES_B; ++i) {
-        rv[i] = 0;
-        ri[i] = 0;
-        rs[i] = -1;
-      }
-    }
+    // 3. the next unit's activations (nxt == cur after the run's last unit:
+    // harmless reloads)
+    load_xv(nxt, xr, vr);
 
-    // 4. the next unit's activations and row scales (nxt == cur after the
-    // run's last unit: harmless reloads, no branch)
-    uint32_t xv_n[XI];
-    uint16_t al_n[RF];
-    load_xv(nxt, xv_n);
-    load_alpha(nxt, al_n);
-
-    // 5. lookups; each 16-byte unit, once read, is refilled with the next
-    // unit's bytes.  After the run's last unit the refill reads one 16-byte
-    // unit for all lanes (no branch, no traffic worth counting).
+    // 4. lookups; each 16-byte unit, once read, is refilled with the next
+    // unit's bytes (after the run's last unit all lanes read one 16-byte unit)
     const GProblem& pn = P[nxt.m];
     const gu8* nbase = gptr(pn.trits);
     const int n_ng = pn.n_groups, n_nt = int(pn.n_pad >> 6);
@@ -327,53 +321,74 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const u32x4 wv = W[t][j];
+        float e[16];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            e[4 * d + k] = tab_at(__builtin_amdgcn_perm(slotreg[d], wv[d], perm_sel(k)) + j * kBlockBytes);
+        }
+        // all sixteen table reads in flight before the first add
+        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: addresses
+        __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // DS reads
+        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: sums
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[t] += e[i];
+        // keep the sums here: without a use in this block the compiler sinks
+        // a unit's adds below the residual and holds every entry in registers
+        asm volatile("" : "+v"(acc[t]));
+        __builtin_amdgcn_sched_barrier(0);
+        // refill after the last read of the old bytes, into the same registers
+        // (a load issued earlier would need other registers and a copy at the
+        // loop edge, and the copy would wait for the load)
         const int grp = min(n_g0 + 4 * j, n_ng - 1);
         const int tl = min(n_t0 + (kGW / 4) * t, n_nt - 1);
         const uint32_t noff = ((uint32_t(tl * n_ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & nmask;
         W[t][j] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(nbase + noff));
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          const uint32_t wd = wv[d];
-#pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            const uint32_t addr = __builtin_amdgcn_perm(slotreg[d], wd, perm_sel(k));
-            acc[t] += tab_at(addr + j * kBlockBytes);
-          }
-        }
-        // keep the sums here: without a use in this block the compiler sinks
-        // all of a unit's adds below the residual and holds every table
-        // entry of the unit in registers
-        asm volatile("" : "+v"(acc[t]));
         __builtin_amdgcn_sched_barrier(0);
       }
     }
 
-    // 6. residual: each lane adds into its own slots (program order: deterministic)
-    float* myres = rres + rq * RPS + 4 * gi;
-    if (pstart) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) myres[i] = 0.0f;
-    }
+    // 5. residual of this slice: each lane's four rows accumulate in registers
+    // over the panel's slices (fixed order: deterministic)
+    const int g0 = cur.slice * kSliceGroups;
+    const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
+    const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
+    const int grow = cur.panel * (RP / 4) + gi;  // global four-row group
+    const bool grow_ok = grow * 4 < pr.n_pad;
     const int col0 = cur.slice * kSliceCols;
     const uint32_t gsh = 2u * uint32_t(grow & 15);
 #pragma unroll
+    for (int k = 0; k < 4; ++k) racc[k] = pstart ? 0.0f : racc[k];
+#pragma unroll
     for (int i = 0; i < RES_B; ++i) {
-      const bool ok = rs[i] >= 0;
-      const float xs = xr_lds[ok ? rs[i] - col0 : 0];
-      const float t = ok ? h2f(uint16_t(rv[i])) * xs : 0.0f;
+      // opaque here: keeps the compiler from reading the loaded values (and
+      // waiting for them) anywhere earlier
+      asm volatile("" : "+v"(rv[i]), "+v"(ri[i]), "+v"(rs[i]));
+      const int s = s_lo + rq + QR * i;
+      const bool ok = grow_ok && s < s_hi;
+      const float t = ok ? h2f(uint16_t(rv[i])) * xr_lds[ok ? rs[i] - col0 : 0] : 0.0f;
       const uint32_t idx = (ri[i] >> gsh) & 3u;
-      myres[idx] += t;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
     }
-    if (grow_ok) {
-      for (int s = s_lo + rq + QR * RES_B; s < s_hi; s += QR) {  // more than RES_B per lane (rare)
-        const float t = h2f(gptr(pr.rval)[grow * pr.nS + s]) * xr_lds[gptr(pr.S)[s] - col0];
-        const uint32_t idx = (gptr(pr.ridx)[(grow >> 4) * pr.nS + s] >> gsh) & 3u;
-        myres[idx] += t;
+    if (s_hi - s_lo > QR * RES_B) {  // more than RES_B columns per lane (rare; uniform branch)
+      for (int s = s_lo + rq + QR * RES_B; s < s_hi; s += QR) {
+        if (grow_ok) {
+          const float t = h2f(gptr(pr.rval)[grow * pr.nS + s]) * xr_lds[gptr(pr.S)[s] - col0];
+          const uint32_t idx = (gptr(pr.ridx)[(grow >> 4) * pr.nS + s] >> gsh) & 3u;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+        }
       }
+    }
+    if (pend) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) rres[rq * RPS + 4 * gi + k] = racc[k];
     }
     __syncthreads();
 
-    // 7. panel end: y = alpha * acc + residual (or a partial of a split panel)
+    // 6. panel end: y = alpha * acc + residual (or a partial of a split panel)
     if (pend) {
       float tot[RB];
 #pragma unroll
@@ -383,25 +398,28 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       }
       float val[RF];
       int prow[RF];
+      bool live[RF];
 #pragma unroll
       for (int i = 0; i < RF; ++i) {
-        float mine = tot[4 * i];
+        const int tq = q + 4 * i;
+        live[i] = tq < RB;
+        float mine = tot[0];
 #pragma unroll
-        for (int k = 1; k < 4; ++k)
-          if (q == k) mine = tot[4 * i + k];
-        prow[i] = (w + kGW * (q + 4 * i)) * 16 + l16;
+        for (int t = 1; t < RB; ++t)
+          if (tq == t) mine = tot[t];
+        prow[i] = (w + kGW * (live[i] ? tq : 0)) * 16 + l16;
         float r = 0.0f;
 #pragma unroll
         for (int k = 0; k < QR; ++k) r += rres[k * RPS + prow[i]];
         val[i] = h2f(al[i]) * mine + r;
       }
-      float* y = pr.y;
+      gf32* y = (gf32*)pr.y;
       const int64_t row0 = int64_t(cur.panel) * RP;
       const bool owned = pstart_slice == 0 && cur.slice == pr.n_slices - 1;
       if (owned) {
 #pragma unroll
         for (int i = 0; i < RF; ++i)
-          if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
+          if (live[i] && row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
       } else {
         // split panel: parts are the runs that hold any of its units
         const int64_t p0 = pr.unit_base + int64_t(cur.panel) * pr.n_slices;
@@ -419,7 +437,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         }
         float* slot = part + (int64_t(ga) * H->max_parts) * RP;
 #pragma unroll
-        for (int i = 0; i < RF; ++i) store_coherent(slot + int64_t(mypart) * RP + prow[i], val[i]);
+        for (int i = 0; i < RF; ++i)
+          if (live[i]) store_coherent(slot + int64_t(mypart) * RP + prow[i], val[i]);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (tid == 0) {
@@ -430,6 +449,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         if (*flag) {
 #pragma unroll
           for (int i = 0; i < RF; ++i) {
+            if (!live[i]) continue;
             float sum = 0.0f;
             for (int k = 0; k < nparts; ++k) sum += load_coherent(slot + int64_t(k) * RP + prow[i]);
             if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = sum;
@@ -438,10 +458,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         }
       }
     }
-#pragma unroll
-    for (int i = 0; i < XI; ++i) xv[i] = xv_n[i];
-#pragma unroll
-    for (int i = 0; i < RF; ++i) al[i] = al_n[i];
+    load_res(nxt);        // after the last use of this unit's residual values
+    load_alpha(nxt, al);  // and of its row scales
     cur = nxt;
   }
 }
@@ -449,7 +467,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 // ---------------------------------------------------------------------------
 // Host planning.
 // ---------------------------------------------------------------------------
-constexpr int kMaxRB = 8;
+constexpr int kMaxRB = 4;
 
 int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   *n_slices = int(cdiv(d.n_groups, kSliceGroups));
@@ -505,7 +523,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
 
   // rows per panel: the largest that still gives every workgroup several units
   int RB = kMaxRB;
-  for (; RB > 4; RB /= 2) {
+  for (; RB > 2; RB /= 2) {
     int64_t units = 0;
     for (int m = 0; m < n_problems; ++m) {
       int ns, np;
@@ -620,8 +638,8 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
   switch (info->rows_per_panel) {
+    case GLds<2>::RP: e = launch_grouped<2>(pl, info->grid, part, counters, st); break;
     case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, part, counters, st); break;
-    case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, part, counters, st); break;
     default: return QTEA_ERR_INVALID_ARG;
   }
   return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
