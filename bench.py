@@ -120,7 +120,7 @@ def time_graph(g, stream, reps, warmup):
 
 def kernel_name(B, grouped=False, rows_per_panel=1024):
     if grouped:
-        return f"grouped_gemv_kernel<{rows_per_panel // 128}>"
+        return f"grouped_gemv_kernel<{rows_per_panel // 256}>"  # 256 rows per row block
     return f"fk_gemv_kernel<{B}>" if B <= 4 else f"lut_gemv_kernel<{B}, 2>"
 
 
@@ -131,8 +131,7 @@ def traffic_per_launch(kernel, algorithmic_bytes):
 
     name = "grouped_gemv" if kernel.startswith("grouped") else "fk_gemv"
     path = os.path.join(ROOT, "profiles", f"traffic_{name}_b1_llama3_8b_stack.txt")
-    src = os.path.join(ROOT, "paper_2609_00224_amd", "csrc",
-                       "grouped.hip" if kernel.startswith("grouped") else "qtea.hip")
+    srcs = ["grouped.hip" if kernel.startswith("grouped") else "qtea.hip", "qtea_internal.h"]
     if not os.path.exists(path):
         return None
     kv = {}
@@ -140,7 +139,10 @@ def traffic_per_launch(kernel, algorithmic_bytes):
         if "=" in line and not line.lstrip().startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for f in srcs:  # the kernel's source file, then the shared header
+        h.update(open(os.path.join(ROOT, "paper_2609_00224_amd", "csrc", f), "rb").read())
+    digest = h.hexdigest()
     if kv.get("kernel") != kernel or kv.get("source_sha256") != digest:
         return None
     try:

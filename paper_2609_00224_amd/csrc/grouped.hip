@@ -15,9 +15,11 @@
 //   - add the slice's salient residual;
 //   - at the panel's last slice, write y = alpha * acc + residual.
 //
-// While a unit is processed, the next unit's packed bytes, activations and
-// row scales are already in flight (two register buffers, ping-pong), so
-// the weight stream does not stop at unit, panel or problem boundaries.
+// While a unit is processed, the next unit's packed bytes, activations,
+// residual and row scales are already in flight: each 16-byte register of
+// packed bytes is refilled with the next unit's bytes as soon as its lookups
+// have been issued, so the weight stream does not stop at unit, panel or
+// problem boundaries.
 // A panel whose slices are split between two runs is reduced through the
 // workspace: each part stores its partial rows, the last part to arrive
 // sums the parts in run order and writes y (fixed order: deterministic).
