@@ -120,7 +120,7 @@ def time_graph(g, stream, reps, warmup):
 
 def kernel_name(B, grouped=False, rows_per_panel=1024):
     if grouped:
-        return f"grouped_gemv_kernel<{rows_per_panel // 256}>"  # 256 rows per row block
+        return f"grouped_gemv_kernel<{rows_per_panel // 128}>"  # 8 waves x 16 rows per row block
     return f"fk_gemv_kernel<{B}>" if B <= 4 else f"lut_gemv_kernel<{B}, 2>"
 
 

@@ -177,7 +177,7 @@ typedef struct qtea_grouped_info {
   uint32_t magic;          /* set by qtea_grouped_plan                    */
   int32_t n_problems;
   int32_t batch;           /* activation rows per problem (only 1 so far) */
-  int32_t grid;            /* workgroups of the launch (one per CU)       */
+  int32_t grid;            /* workgroups of the launch (two per CU)       */
   int32_t rows_per_panel;  /* output rows of one work unit               */
   int32_t max_parts;       /* runs sharing one panel, at most            */
   int64_t n_units;
@@ -197,8 +197,9 @@ int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes);
  *   batch                must be 1 (QTEA_ERR_BATCH otherwise)
  *   plan                 device buffer, >= qtea_grouped_plan_bytes(n_problems)
  *   info                 host, filled on success
- * Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_BATCH, QTEA_ERR_WORKSPACE (plan
- * buffer too small), QTEA_ERR_HIP.
+ * Errors: QTEA_ERR_INVALID_ARG (also for a matrix whose packed codes or
+ * residual values take 2 GiB or more: the kernel uses 32-bit offsets),
+ * QTEA_ERR_BATCH, QTEA_ERR_WORKSPACE (plan buffer too small), QTEA_ERR_HIP.
  */
 int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const uint16_t* const* x,
                       float* const* y, int n_problems, int batch, void* plan, int64_t plan_bytes,

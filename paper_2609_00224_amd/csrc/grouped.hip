@@ -2,14 +2,17 @@
 // persistent launch (Eq. 10 with one group and zero bias, plus the Eq. 11
 // residual, for every problem of the list).
 //
-// Work unit = (problem, panel of kRowsPerPanel rows, K slice of 8 sixteen-pack
-// groups = 128 packs = 640 columns).  Units are ordered (problem, panel,
-// slice) with the slice fastest and cut into one contiguous run per
-// workgroup, balanced by weight bytes.  A workgroup walks its run:
+// Work unit = (problem, panel of RP rows, K slice of 4 sixteen-pack groups =
+// 64 packs = 320 columns).  Units are ordered (problem, panel, slice) with
+// the slice fastest and cut into one contiguous run per workgroup, balanced
+// by weight bytes.  Two 512-thread workgroups share each CU (about 79 KB of
+// LDS each): while one builds its tables the other streams and looks up, so
+// the phases of one workgroup's units hide behind the other's.  A workgroup
+// walks its run:
 //
 //   - stage a_j = v_j x_j and x_j of the slice in LDS;
-//   - build the full 243-entry table of each of the slice's 128 packs
-//     (124,416 bytes of LDS, one fp32 entry per code and pack);
+//   - build the full 243-entry table of each of the slice's 64 packs
+//     (62,208 bytes of LDS, one fp32 entry per code and pack);
 //   - add one table entry per packed byte of the panel's rows, the entry
 //     address formed from the byte by a single v_perm_b32;
 //   - add the slice's salient residual;
@@ -35,16 +38,18 @@ namespace {
 
 using namespace qtea_detail;
 
-constexpr int kGT = 1024;                                 // threads per workgroup
+constexpr int kGT = 512;                                  // threads per workgroup
 constexpr int kGW = kGT / 64;                             // waves per workgroup
-constexpr int kSliceGroups = 8;                           // groups per K slice
-constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 128
-constexpr int kSliceCols = kSliceGroups * kGroupCols;     // 640
-constexpr int kBlockBytes = kCodes * 256;                 // tables of 64 packs: code row = 256 B
-constexpr int kTabBytes = 2 * kBlockBytes;                // 124,416
+constexpr int kWgPerCu = 2;                               // workgroups sharing a CU
+constexpr int kSliceGroups = 4;                           // groups per K slice (one per quarter-wave)
+constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 64
+constexpr int kSliceCols = kSliceGroups * kGroupCols;     // 320
+constexpr int kTabBytes = kCodes * 256;                   // 62,208: code row = 64 packs x 4 bytes
 constexpr int kBuildTasks = kSlicePacks * 9;              // (pack, two leading digits)
+constexpr int kResCols = 16;  // salient columns of a slice staged per wave (more: direct loads)
 constexpr uint32_t kGPlanMagic = 0x51475250u;            // "QGRP"
 constexpr int64_t kPlanProblemsOff = 256;
+static_assert(kSlicePacks * 4 == 256, "one table row of 256 bytes per code");
 
 struct GProblem {
   const uint8_t* trits;
@@ -63,6 +68,7 @@ struct GProblem {
 };
 static_assert(sizeof(GProblem) == 128, "plan record size");
 static_assert(kSliceCols % 64 == 0 && kBuildTasks % 64 == 0, "passes of whole waves");
+static_assert(kSliceCols <= kGT, "one staged column per thread");
 
 struct GPlanHeader {
   uint32_t magic, version;
@@ -72,15 +78,21 @@ struct GPlanHeader {
 
 template <int RB>
 struct GLds {
-  static constexpr int RP = kGW * 16 * RB;  // rows per panel
-  static constexpr int QR = kGT / (RP / 4);  // residual lanes per four-row group
-  static constexpr int RPS = RP + 1;     // row stride of the residual slots
-  static constexpr int A = kTabBytes;                     // a_j, fp32 [640]
-  static constexpr int XR = A + 4 * kSliceCols;           // x_j, fp32 [640]
-  static constexpr int RR = XR + 4 * kSliceCols;          // residual slots fp32 [QR][RPS]
-  static constexpr int FLAG = RR + 4 * QR * RPS;          // one int
+  static constexpr int RP = kGW * 16 * RB;   // rows per panel
+  static constexpr int TPW = RP / 64 / kGW;  // 64-row tiles per wave in the residual phase
+  static constexpr int GPW = 16 * TPW;       // four-row groups per wave
+  static constexpr int QR = 64 / GPW;        // residual lanes per group
+  static constexpr int A = kTabBytes;                     // a_j, fp32 [320]
+  static constexpr int XR = A + 4 * kSliceCols;           // x_j, fp32 [320]
+  static constexpr int RR = XR + 4 * kSliceCols;          // residual row sums, fp32 [RP]
+  static constexpr int RV = RR + 4 * RP;                  // per wave: fp16 values [TPW][kResCols][16]
+  static constexpr int RI = RV + kGW * 1024;              // per wave: u32 positions [2][16], fp32 x [32]
+  static constexpr int FLAG = RI + kGW * 256;             // one int
   static constexpr int BYTES = FLAG + 16;
 };
+static_assert(GLds<4>::TPW == 1 && GLds<8>::TPW == 2, "one or two tiles per wave");
+static_assert(2 * kResCols * 32 == 1024, "one 16-byte load per lane stages two tiles' values");
+static_assert(kWgPerCu * GLds<8>::BYTES <= 160 * 1024, "two workgroups per CU");
 
 typedef __attribute__((address_space(1))) const uint8_t gu8;
 typedef __attribute__((address_space(1))) const uint16_t gu16;
@@ -126,7 +138,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
                                                            float* __restrict__ part,
                                                            uint32_t* __restrict__ counters) {
   using L = GLds<RB>;
-  constexpr int RP = L::RP, QR = L::QR, RPS = L::RPS;
+  constexpr int RP = L::RP, TPW = L::TPW, GPW = L::GPW, QR = L::QR;
+  constexpr int TPP = RP / 64;  // tiles per panel
   extern __shared__ float smem[];
   char* lds = reinterpret_cast<char*>(smem);
   float* a_lds = reinterpret_cast<float*>(lds + L::A);
@@ -144,8 +157,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, l16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wt = w >> 2, wr = w & 3;  // tile of the wave's first row block, block in its tile
-  // residual lane mapping: four-row group gi of the panel, lane rq among its QR lanes
-  const int gi = tid / QR, rq = tid - gi * QR;
+  // residual lane mapping: wave w takes the TPW tiles w*TPW.. of the panel,
+  // one four-row group per lane (gw), the QR lanes of a group (rq) taking its
+  // salient columns round-robin
+  const int gw = lane & (GPW - 1), rq = lane / GPW;
+  const int gi = w * GPW + gw;  // group in the panel
+  const int rtile = gw >> 4, g16 = gw & 15;
 
   // table slot bytes of this lane: byte k of slotreg[d] = 4 * (16 q + ((4 d + k + l16) mod 16))
   uint32_t slotreg[4];
@@ -176,7 +193,6 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // waits for the next unit's weights, which are the youngest loads.
 
   // activations: this thread stages slice column tid (kept as loaded, checked when staged)
-  static_assert(kSliceCols <= kGT, "one staged column per thread");
   auto load_xv = [&](const Cursor c, uint16_t& xr, uint16_t& vr) {
     const GProblem& pr = P[c.m];
     const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
@@ -185,65 +201,82 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     vr = gptr(pr.v)[col < kv ? col : kv - 1];
   };
   // row scales of the row blocks this lane finalizes: t = q + 4 i
-  constexpr int RF = RB >= 4 ? RB / 4 : 1;
+  constexpr int RF = RB / 4;
+  static_assert(RB % 4 == 0, "row blocks in multiples of the quarters");
   auto load_alpha = [&](const Cursor c, uint16_t (&al)[RF]) {
     const GProblem& pr = P[c.m];
     const uint32_t np = uint32_t(pr.n_pad);
 #pragma unroll
     for (int i = 0; i < RF; ++i) {
-      const int t = (q + 4 * i) < RB ? q + 4 * i : 0;
-      const uint32_t rowq = uint32_t(c.panel * RP + (w + kGW * t) * 16 + l16);
+      const uint32_t rowq = uint32_t(c.panel * RP + (w + kGW * (q + 4 * i)) * 16 + l16);
       al[i] = gptr(pr.alpha)[rowq < np ? rowq : np - 1];
     }
   };
-  // salient residual of unit c, this lane's share: columns s = s_lo + rq + QR i
-  // of the slice, four-row group gi of the panel
-  constexpr int RES_B = 5;
-  uint32_t rv[RES_B], ri[RES_B];
-  int rs[RES_B];
-  auto load_res = [&](const Cursor c) {
+  // salient residual of unit c: this wave's tiles over the slice's first
+  // kResCols salient columns, fetched as two loads per lane and staged in
+  // the wave's LDS area in the residual phase.  rvq: 16 bytes of a tile's
+  // value run (32 bytes per column; lanes 0..31 the first tile, 32..63 the
+  // second); ris: lanes 0..31 the position words of the tiles (16 per tile),
+  // lanes 32..63 the salient column indices.  Indices are clamped into their
+  // regions (without salient columns both read the row scales).
+  u32x4 rvq;
+  uint32_t ris;
+  auto load_res = [&](const Cursor c, const int s_lo, const int s_hi) {
+    const GProblem& pr = P[c.m];
+    const bool any = pr.nS > 0;
+    const uint32_t nS = uint32_t(pr.nS), n_tiles = uint32_t(pr.n_pad >> 6);
+    const uint32_t tile0 = uint32_t(c.panel * TPP + w * TPW);
+    const uint32_t Tv = min(tile0 + (TPW == 2 ? uint32_t(lane >> 5) : 0u), n_tiles - 1u);
+    const uint32_t ncs = uint32_t(min(s_hi - s_lo, kResCols));
+    const uint32_t len = ncs * 32u;
+    const uint32_t lofs = min(uint32_t(lane & 31) * 16u, len >= 16u ? len - 16u : 0u);
+    const uint32_t vofs = any ? min((Tv * nS + uint32_t(s_lo)) * 32u + lofs, n_tiles * nS * 32u - 16u) : 0u;
+    rvq = *reinterpret_cast<const gu32x4*>(
+        (any ? reinterpret_cast<gu8*>(gptr(pr.rval)) : reinterpret_cast<gu8*>(gptr(pr.alpha))) + vofs);
+    const uint32_t Ti = min(tile0 + (TPW == 2 ? uint32_t((lane >> 4) & 1) : 0u), n_tiles - 1u);
+    const uint32_t sc = any ? min(uint32_t(s_lo) + uint32_t(lane & 15), nS - 1u) : 0u;
+    gu32* ib = !any ? reinterpret_cast<gu32*>(gptr(pr.alpha))
+                    : (lane < 32 ? gptr(pr.ridx) + Ti * nS : reinterpret_cast<gu32*>(gptr(pr.S)));
+    ris = ib[sc];
+  };
+  // salient range [spos[g0], spos[g1]) of unit c's groups, as a vector load
+  // (lane 0 reads the first bound, the other lanes the second): a scalar load
+  // here would be waited for at once, and the salient list is read from HBM
+  auto load_spos = [&](const Cursor c) -> int {
     const GProblem& pr = P[c.m];
     const int g0 = c.slice * kSliceGroups;
     const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
-    const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
-    const bool any = pr.nS > 0;  // without salient columns read the row scales (any valid address)
-    const int grow = c.panel * (RP / 4) + gi;
-    const uint32_t growc = uint32_t(grow * 4 < pr.n_pad ? grow : 0);
-    const uint32_t nS = uint32_t(pr.nS);
-    gu16* rvb = any ? gptr(pr.rval) : gptr(pr.alpha);
-    gu32* rib = any ? gptr(pr.ridx) : (gu32*)gptr(pr.alpha);
-    gi32* sb = any ? gptr(pr.S) : (gi32*)gptr(pr.alpha);
-    const uint32_t gofs = any ? growc * nS : 0u, tofs = any ? (growc >> 4) * nS : 0u;
-#pragma unroll
-    for (int i = 0; i < RES_B; ++i) {
-      const int s = s_lo + rq + QR * i;
-      const uint32_t sc = any ? uint32_t(max(min(s, s_hi - 1), 0)) : 0u;
-      rv[i] = rvb[gofs + sc];
-      ri[i] = rib[tofs + sc];
-      rs[i] = sb[sc];
-    }
+    return gptr(pr.spos)[lane == 0 ? g0 : g1];
   };
-  // byte offset of the 16-byte unit (row block t, group j of the quarter) of unit c
-  auto w_off = [&](const Cursor c, int t, int j) -> uint32_t {
+  // byte offset of the 16-byte unit (row block t, group of the quarter) of unit c
+  auto w_off = [&](const Cursor c, int t) -> uint32_t {
     const GProblem& pr = P[c.m];
     const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
-    const int grp = min(c.slice * kSliceGroups + q + 4 * j, ng - 1);
-    const int tl = min(c.panel * (RP / 64) + wt + (kGW / 4) * t, n_tiles - 1);
+    const int grp = min(c.slice * kSliceGroups + q, ng - 1);
+    const int tl = min(c.panel * TPP + wt + (kGW / 4) * t, n_tiles - 1);
     return (uint32_t(tl * ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks;
   };
   // Table entry at LDS byte address `a`.  The kernel has no static LDS, so
   // the dynamic allocation (the tables first) starts at address 0.
   auto tab_at = [](uint32_t a) -> float { return *(const lds_float*)(size_t(a)); };
 
-  u32x4 W[RB][2];
+  u32x4 W[RB];
   uint16_t xr, vr;
   load_xv(cur, xr, vr);
 #pragma unroll
-  for (int t = 0; t < RB; ++t)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      W[t][j] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, t, j)));
-  load_res(cur);
+  for (int t = 0; t < RB; ++t) {
+    W[t] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, t)));
+    __builtin_amdgcn_sched_barrier(0);  // the loop's order of the weight loads
+  }
+  int s_lo_c, s_hi_c;  // salient range of the current unit
+  {
+    const GProblem& pr = P[cur.m];
+    const int g0 = cur.slice * kSliceGroups;
+    const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
+    s_lo_c = cptr(pr.spos)[g0];
+    s_hi_c = cptr(pr.spos)[g1];
+  }
+  load_res(cur, s_lo_c, s_hi_c);
   uint16_t al[RF];
   load_alpha(cur, al);
 
@@ -261,10 +294,11 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const bool pstart = (cur.slice == 0) || (u == ub);
     const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
     if (pstart) pstart_slice = cur.slice;
+    const int col0 = cur.slice * kSliceCols;
 
     // 1. stage the slice's activations: a_j = v_j x_j (exact in fp32) and x_j
     if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
-      const int gcol = cur.slice * kSliceCols + tid;
+      const int gcol = col0 + tid;
       const float xf = gcol < pr.K ? h2f(xr) : 0.0f;
       const float vf = gcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
       a_lds[tid] = vf * xf;
@@ -278,7 +312,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       const int task = tid + it * kGT;
       if (w * 64 + it * kGT < kBuildTasks) {  // whole waves (kBuildTasks is a multiple of 64)
         const int p = task & (kSlicePacks - 1);
-        const int top = task >> 7;
+        const int top = task / kSlicePacks;
         const int d4 = (top * 11) >> 5;
         const int d3 = top - 3 * d4;
         const float a0 = a_lds[5 * p], a1 = a_lds[5 * p + 1], a2 = a_lds[5 * p + 2];
@@ -286,7 +320,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         const float t4 = d4 == 0 ? -a4 : (d4 == 2 ? a4 : 0.0f);
         const float t3 = d3 == 0 ? -a3 : (d3 == 2 ? a3 : 0.0f);
         const float base = t4 + t3;
-        lds_char* dst = (lds_char*)smem + (p >> 6) * kBlockBytes + (p & 63) * 4 + (27 * d3 + 81 * d4) * 256;
+        lds_char* dst = (lds_char*)smem + p * 4 + (27 * d3 + 81 * d4) * 256;
 #pragma unroll
         for (int e2 = 0; e2 < 3; ++e2) {
           const float u2 = e2 == 0 ? base - a2 : (e2 == 1 ? base : base + a2);
@@ -305,88 +339,102 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     }
     __syncthreads();
 
-    // 3. the next unit's activations (nxt == cur after the run's last unit:
-    // harmless reloads)
+    // 3. the next unit's activations and salient range (nxt == cur after the
+    // run's last unit: harmless reloads)
     load_xv(nxt, xr, vr);
+    const int spv = load_spos(nxt);
 
     // 4. lookups; each 16-byte unit, once read, is refilled with the next
     // unit's bytes (after the run's last unit all lanes read one 16-byte unit)
     const GProblem& pn = P[nxt.m];
     const gu8* nbase = gptr(pn.trits);
     const int n_ng = pn.n_groups, n_nt = int(pn.n_pad >> 6);
-    const int n_g0 = nxt.slice * kSliceGroups + q, n_t0 = nxt.panel * (RP / 64) + wt;
+    const int n_grp = min(nxt.slice * kSliceGroups + q, n_ng - 1), n_t0 = nxt.panel * TPP + wt;
     const uint32_t nmask = has_next ? 0xffffffffu : 0u;
 #pragma unroll
     for (int t = 0; t < RB; ++t) acc[t] = pstart ? 0.0f : acc[t];
 #pragma unroll
     for (int t = 0; t < RB; ++t) {
+      const u32x4 wv = W[t];
+      float e[16];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const u32x4 wv = W[t][j];
-        float e[16];
+      for (int d = 0; d < 4; ++d) {
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            e[4 * d + k] = tab_at(__builtin_amdgcn_perm(slotreg[d], wv[d], perm_sel(k)) + j * kBlockBytes);
-        }
-        // all sixteen table reads in flight before the first add
-        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: addresses
-        __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // DS reads
-        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: sums
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[t] += e[i];
-        // keep the sums here: without a use in this block the compiler sinks
-        // a unit's adds below the residual and holds every entry in registers
-        asm volatile("" : "+v"(acc[t]));
-        __builtin_amdgcn_sched_barrier(0);
-        // refill after the last read of the old bytes, into the same registers
-        // (a load issued earlier would need other registers and a copy at the
-        // loop edge, and the copy would wait for the load)
-        const int grp = min(n_g0 + 4 * j, n_ng - 1);
-        const int tl = min(n_t0 + (kGW / 4) * t, n_nt - 1);
-        const uint32_t noff = ((uint32_t(tl * n_ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & nmask;
-        W[t][j] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(nbase + noff));
-        __builtin_amdgcn_sched_barrier(0);
+        for (int k = 0; k < 4; ++k) e[4 * d + k] = tab_at(__builtin_amdgcn_perm(slotreg[d], wv[d], perm_sel(k)));
       }
+      // all sixteen table reads in flight before the first add
+      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: addresses
+      __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // DS reads
+      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: sums
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[t] += e[i];
+      // keep the sums here: without a use in this block the compiler sinks
+      // a unit's adds below the residual and holds every entry in registers
+      asm volatile("" : "+v"(acc[t]));
+      __builtin_amdgcn_sched_barrier(0);
+      // refill after the last read of the old bytes, into the same registers
+      // (a load issued earlier would need other registers and a copy at the
+      // loop edge, and the copy would wait for the load)
+      const int tl = min(n_t0 + (kGW / 4) * t, n_nt - 1);
+      const uint32_t noff = ((uint32_t(tl * n_ng + n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & nmask;
+      W[t] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(nbase + noff));
+      __builtin_amdgcn_sched_barrier(0);
     }
 
     // 5. residual of this slice: each lane's four rows accumulate in registers
     // over the panel's slices (fixed order: deterministic)
-    const int g0 = cur.slice * kSliceGroups;
-    const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
-    const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
+    const int s_lo = s_lo_c, s_hi = s_hi_c;
+    const int ncol = s_hi - s_lo;
     const int grow = cur.panel * (RP / 4) + gi;  // global four-row group
     const bool grow_ok = grow * 4 < pr.n_pad;
-    const int col0 = cur.slice * kSliceCols;
-    const uint32_t gsh = 2u * uint32_t(grow & 15);
+    const uint32_t gsh = 2u * uint32_t(g16);
 #pragma unroll
     for (int k = 0; k < 4; ++k) racc[k] = pstart ? 0.0f : racc[k];
+    {
+      // stage in this wave's own LDS area: only this wave reads it back, and a
+      // wave's LDS accesses complete in order, so no barrier is needed.  The
+      // column indices are replaced by the columns' activations.
+      char* rv_w = lds + L::RV + w * 1024;
+      uint32_t* ri_w = reinterpret_cast<uint32_t*>(lds + L::RI + w * 256);
+      *reinterpret_cast<u32x4*>(rv_w + 16 * lane) = rvq;
+      const int xc = int(ris) - col0;
+      const uint32_t xw = __float_as_uint(xr_lds[xc >= 0 && xc < kSliceCols ? xc : 0]);
+      ri_w[lane] = lane < 32 ? ris : xw;
+      asm volatile("" ::: "memory");
+      const int nc = ncol < kResCols ? ncol : kResCols;
+      for (int c = rq; c < nc; c += QR) {
+        const uint16_t hv = reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16];
+        const uint32_t idx = (ri_w[16 * rtile + c] >> gsh) & 3u;
+        const float xv = __uint_as_float(ri_w[32 + c]);
+        const float t = grow_ok ? h2f(hv) * xv : 0.0f;
 #pragma unroll
-    for (int i = 0; i < RES_B; ++i) {
-      // opaque here: keeps the compiler from reading the loaded values (and
-      // waiting for them) anywhere earlier
-      asm volatile("" : "+v"(rv[i]), "+v"(ri[i]), "+v"(rs[i]));
-      const int s = s_lo + rq + QR * i;
-      const bool ok = grow_ok && s < s_hi;
-      const float t = ok ? h2f(uint16_t(rv[i])) * xr_lds[ok ? rs[i] - col0 : 0] : 0.0f;
-      const uint32_t idx = (ri[i] >> gsh) & 3u;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+        for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+      }
     }
-    if (s_hi - s_lo > QR * RES_B) {  // more than RES_B columns per lane (rare; uniform branch)
-      for (int s = s_lo + rq + QR * RES_B; s < s_hi; s += QR) {
+    if (ncol > kResCols) {  // a slice with many salient columns (uniform branch)
+      const int64_t T = int64_t(grow >> 4);
+      for (int s = s_lo + kResCols + rq; s < s_hi; s += QR) {
         if (grow_ok) {
-          const float t = h2f(gptr(pr.rval)[grow * pr.nS + s]) * xr_lds[gptr(pr.S)[s] - col0];
-          const uint32_t idx = (gptr(pr.ridx)[(grow >> 4) * pr.nS + s] >> gsh) & 3u;
+          const float t = h2f(gptr(pr.rval)[rval_index(grow, s, pr.nS)]) * xr_lds[gptr(pr.S)[s] - col0];
+          const uint32_t idx = (gptr(pr.ridx)[T * pr.nS + s] >> gsh) & 3u;
 #pragma unroll
           for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
         }
       }
     }
     if (pend) {
+      // the group's four row sums over its QR lanes (shuffles, fixed order)
+      float r4[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) rres[rq * RPS + 4 * gi + k] = racc[k];
+      for (int k = 0; k < 4; ++k) {
+        float h = racc[k];
+        if (QR == 4) h += __shfl_xor(h, 16);
+        r4[k] = h + __shfl_xor(h, 32);
+      }
+      if (rq == 0) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) rres[4 * gi + k] = r4[k];
+      }
     }
     __syncthreads();
 
@@ -400,20 +448,15 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       }
       float val[RF];
       int prow[RF];
-      bool live[RF];
 #pragma unroll
       for (int i = 0; i < RF; ++i) {
         const int tq = q + 4 * i;
-        live[i] = tq < RB;
         float mine = tot[0];
 #pragma unroll
         for (int t = 1; t < RB; ++t)
           if (tq == t) mine = tot[t];
-        prow[i] = (w + kGW * (live[i] ? tq : 0)) * 16 + l16;
-        float r = 0.0f;
-#pragma unroll
-        for (int k = 0; k < QR; ++k) r += rres[k * RPS + prow[i]];
-        val[i] = h2f(al[i]) * mine + r;
+        prow[i] = (w + kGW * tq) * 16 + l16;
+        val[i] = h2f(al[i]) * mine + rres[prow[i]];
       }
       gf32* y = (gf32*)pr.y;
       const int64_t row0 = int64_t(cur.panel) * RP;
@@ -421,7 +464,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       if (owned) {
 #pragma unroll
         for (int i = 0; i < RF; ++i)
-          if (live[i] && row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
+          if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
       } else {
         // split panel: parts are the runs that hold any of its units
         const int64_t p0 = pr.unit_base + int64_t(cur.panel) * pr.n_slices;
@@ -439,8 +482,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         }
         float* slot = part + (int64_t(ga) * H->max_parts) * RP;
 #pragma unroll
-        for (int i = 0; i < RF; ++i)
-          if (live[i]) store_coherent(slot + int64_t(mypart) * RP + prow[i], val[i]);
+        for (int i = 0; i < RF; ++i) store_coherent(slot + int64_t(mypart) * RP + prow[i], val[i]);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (tid == 0) {
@@ -451,7 +493,6 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         if (*flag) {
 #pragma unroll
           for (int i = 0; i < RF; ++i) {
-            if (!live[i]) continue;
             float sum = 0.0f;
             for (int k = 0; k < nparts; ++k) sum += load_coherent(slot + int64_t(k) * RP + prow[i]);
             if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = sum;
@@ -460,8 +501,10 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         }
       }
     }
-    load_res(nxt);        // after the last use of this unit's residual values
-    load_alpha(nxt, al);  // and of its row scales
+    s_lo_c = __builtin_amdgcn_readlane(spv, 0);
+    s_hi_c = __builtin_amdgcn_readlane(spv, 1);
+    load_res(nxt, s_lo_c, s_hi_c);  // after the last use of this unit's residual values
+    load_alpha(nxt, al);            // and of its row scales
     cur = nxt;
   }
 }
@@ -469,7 +512,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 // ---------------------------------------------------------------------------
 // Host planning.
 // ---------------------------------------------------------------------------
-constexpr int kMaxRB = 4;
+constexpr int kMaxRB = 8;
 
 int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   *n_slices = int(cdiv(d.n_groups, kSliceGroups));
@@ -477,22 +520,36 @@ int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   return *n_slices * *n_panels;
 }
 
-int cu_count() {
-  int dev = 0, n = 0;
+template <int RB>
+hipError_t set_lds_attr() {
+  static bool done = false;
+  if (!done) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, GLds<RB>::BYTES);
+    if (e != hipSuccess) return e;
+    done = true;
+  }
+  return hipSuccess;
+}
+
+// Workgroups of the launch: kWgPerCu per CU when that many fit (they do on
+// gfx950: 160 KB of LDS, 16 waves of at most 128 VGPRs), else one per CU.
+// The kernel never waits for another workgroup, so any grid is correct.
+int grid_size() {
+  int dev = 0, n = 0, per = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  return n;
+  if (set_lds_attr<kMaxRB>() != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, reinterpret_cast<const void*>(&grouped_gemv_kernel<kMaxRB>),
+                                                   kGT, GLds<kMaxRB>::BYTES) != hipSuccess)
+    return 0;
+  return n * std::max(1, std::min(per, kWgPerCu));
 }
 
 template <int RB>
 hipError_t launch_grouped(const uint8_t* plan, int grid, float* part, uint32_t* counters, hipStream_t st) {
-  static bool attr = false;
-  if (!attr) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, GLds<RB>::BYTES);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  const hipError_t e = set_lds_attr<RB>();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(grouped_gemv_kernel<RB>, dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan, part, counters);
   return hipGetLastError();
 }
@@ -503,7 +560,7 @@ extern "C" {
 
 int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes) {
   if (!out_bytes || n_problems < 1) return QTEA_ERR_INVALID_ARG;
-  const int G = cu_count();
+  const int G = grid_size();
   if (G < 1) return QTEA_ERR_HIP;
   *out_bytes = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign) + 8 * int64_t(G + 1);
   return QTEA_OK;
@@ -519,13 +576,18 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   const int st_plan = qtea_grouped_plan_bytes(n_problems, &need);
   if (st_plan != QTEA_OK) return st_plan;
   if (plan_bytes < need) return QTEA_ERR_WORKSPACE;
-  const int G = cu_count();
-  for (int m = 0; m < n_problems; ++m)
+  const int G = grid_size();
+  for (int m = 0; m < n_problems; ++m) {
     if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
+    // the kernel addresses the packed bytes and the residual with 32-bit offsets
+    const int64_t trit_bytes = descs[m].n_pad * descs[m].n_groups * kGroupPacks;
+    const int64_t resid_bytes = (descs[m].n_pad / 4) * descs[m].n_salient * 2;
+    if (trit_bytes >= (int64_t(1) << 31) || resid_bytes >= (int64_t(1) << 31)) return QTEA_ERR_INVALID_ARG;
+  }
 
   // rows per panel: the largest that still gives every workgroup several units
   int RB = kMaxRB;
-  for (; RB > 2; RB /= 2) {
+  for (; RB > 4; RB /= 2) {
     int64_t units = 0;
     for (int m = 0; m < n_problems; ++m) {
       int ns, np;
@@ -572,7 +634,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
       const int64_t rows = std::min<int64_t>(RP, d.n_pad - int64_t(p) * RP);
       for (int s = 0; s < ns; ++s) {
         const int64_t groups = std::min<int64_t>(kSliceGroups, d.n_groups - int64_t(s) * kSliceGroups);
-        unit_cost.push_back(rows * groups * kGroupPacks + 16384);
+        unit_cost.push_back(rows * groups * kGroupPacks + 8192);
       }
     }
     total_units += int64_t(ns) * np;
@@ -640,8 +702,8 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
   switch (info->rows_per_panel) {
-    case GLds<2>::RP: e = launch_grouped<2>(pl, info->grid, part, counters, st); break;
     case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, part, counters, st); break;
+    case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, part, counters, st); break;
     default: return QTEA_ERR_INVALID_ARG;
   }
   return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;

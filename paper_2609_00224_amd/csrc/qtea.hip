@@ -1,7 +1,7 @@
 // Compressed ternary GEMV for gfx950: packing, the lookup-table GEMV and
 // the C ABI declared in include/qtea.h.
 //
-// Device layout (layout version 1), all regions 256-byte aligned:
+// Device layout (layout version 2), all regions 256-byte aligned:
 //   header   256 B: magic, layout, sizes; a validation flag word at +128.
 //   trits    [n_pad/64 tiles][n_groups][64 rows][16 bytes]
 //            One 16-byte unit holds the sixteen packs of one 16-pack group
@@ -14,8 +14,10 @@
 //   v        fp16 [n_groups * 80]      (zero in the column padding)
 //   salient  int32 [n_salient]
 //   spos     int32 [n_groups + 1]      first s with S_s >= 80 * g
-//   rval     fp16 [n_pad/4][n_salient]  residual of four-row group g (row-group major:
-//            the rows of a workgroup read one contiguous run)
+//   rval     fp16 [n_pad/64][n_salient][16]  residual of four-row group g in salient
+//            column s at ((g / 16) * n_salient + s) * 16 + g % 16: the sixteen
+//            groups of a tile are contiguous per column, and a tile's residual
+//            over a run of salient columns is one contiguous run
 //   ridx     u32  [n_pad/64][n_salient] 2-bit positions of 16 consecutive groups
 //
 // GEMV (one launch): workgroup = (row block, K slice).  For each chunk of
@@ -112,7 +114,8 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
   }
   const int64_t G = N / 4, Gp = n_pad / 4, Wp = n_pad / 64;
   for (int64_t i = t0; i < nS * Gp; i += stride) {
-    const int64_t g = i / nS, s = i % nS;
+    const int64_t tile = i / (16 * nS), rem = i - tile * 16 * nS;
+    const int64_t s = rem >> 4, g = 16 * tile + (rem & 15);
     o_rval[i] = g < G ? rval[s * G + g] : 0;
   }
   for (int64_t i = t0; i < nS * Wp; i += stride) {
@@ -359,7 +362,7 @@ __global__ __launch_bounds__(kThreads) void lut_gemv_kernel(const GemvArgs p) {
         for (int j = 0; j < TPW; ++j) {
           const int64_t r = int64_t(tile[j]) * kTileRows + lane;
           r_word[j][u] = ok && valid[j] ? p.ridx[int64_t(tile[j]) * p.nS + s] : 0u;
-          r_val[j][u] = ok && valid[j] ? p.rval[(r >> 2) * p.nS + s] : uint16_t(0);
+          r_val[j][u] = ok && valid[j] ? p.rval[rval_index(r >> 2, s, p.nS)] : uint16_t(0);
         }
       }
     };
@@ -504,236 +507,6 @@ __global__ __launch_bounds__(kThreads) void lut_gemv_kernel(const GemvArgs p) {
           if (q0 + u < p.nslices) sum += t[u];
       }
       p.y[b * p.N + r] = sum;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Batch-1 streaming kernel.
-//
-// Workgroup = (K slice of 4 groups = 64 packs, block of `rbt` row tiles),
-// WAVES wavefronts sharing the slice's table.  Order of work:
-//   1. load the slice's activations and rescales and wait for them (before
-//      any weight request, so they return at unloaded latency);
-//   2. request the packed bytes of each wave's first PD tiles, then build
-//      the table while they stream in;
-//   3. each wave walks its tiles (every WAVES-th tile of the block), keeping
-//      the next PD tiles' bytes, alpha and residual metadata in flight, and
-//      stores one partial per row and slice;
-//   4. the last workgroup of the row block to arrive sums the slices' partials
-//      in slice order.
-// ---------------------------------------------------------------------------
-struct B1Args {
-  const uint8_t* trits;
-  const uint16_t* alpha;
-  const uint16_t* v;
-  const int32_t* S;
-  const int32_t* spos;
-  const uint16_t* rval;
-  const uint32_t* ridx;
-  const uint16_t* x;
-  float* y;
-  float* part;
-  uint32_t* counters;
-  int64_t N, K, n_pad;
-  int n_groups, n_tiles, nS;
-  int nslices, rbt;
-};
-
-template <int PD, int WAVES, bool ACCUM>
-__global__ __launch_bounds__(WAVES * 64) void lut_gemv_b1_kernel(const B1Args p) {
-  constexpr int KC = 4, COLS = KC * kGroupCols, ROW = KC * kGroupPacks;
-  constexpr int NT = WAVES * 64;
-  __shared__ float lut[kCodes * ROW];
-  __shared__ float x_lds[COLS];
-  __shared__ float v_lds[COLS];
-  __shared__ int s_last;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int quarter = lane >> 4;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int ks = blockIdx.x % p.nslices;
-  const int rb = blockIdx.x / p.nslices;
-  const int c0 = ks * KC;
-  const int nk = min(KC, p.n_groups - c0);
-  const int64_t col0 = int64_t(c0) * kGroupCols;
-  const int tile_lo = rb * p.rbt;
-  const int tile_hi = min(p.n_tiles, tile_lo + p.rbt);
-  // tiles of this wave: tile_lo + wave + WAVES i
-  const int ntw = tile_hi - tile_lo > wave ? (tile_hi - tile_lo - wave + WAVES - 1) / WAVES : 0;
-
-  // (1) activations, rescales, salient range
-  for (int c = tid; c < COLS; c += NT) {
-    const bool ok = c < nk * kGroupCols;
-    x_lds[c] = ok && col0 + c < p.K ? h2f(p.x[col0 + c]) : 0.0f;
-    v_lds[c] = ok ? h2f(p.v[col0 + c]) : 0.0f;
-  }
-  const int sb = p.spos[c0], se = p.spos[c0 + nk];
-  const int nsal = min(se - sb, kResBatch);
-  __syncthreads();
-
-  // quarter-staggered group order (distinct table banks per quarter)
-  int grp[KC];
-#pragma unroll
-  for (int k = 0; k < KC; ++k) {
-    int gk = k + quarter;
-    gk = gk >= nk ? gk - nk : gk;
-    gk = gk >= nk ? gk - nk : gk;
-    gk = gk >= nk ? gk - nk : gk;
-    grp[k] = gk;
-  }
-
-  // (2) per-tile streamed state, PD tiles deep.  Every streamed value is a
-  // vector load (counted by vmcnt): a scalar load here would share the
-  // counter that table lookups wait on and stall them for a memory round
-  // trip.  Lane u < nsal carries salient column sb + u's position word.
-  u32x4 wb[PD][KC];
-  uint16_t alb[PD];
-  uint32_t rwl[PD];
-  uint16_t rvb[PD][kResBatch];
-  auto fetch = [&](int slot, int i) {
-    const int tile = tile_lo + wave + WAVES * i;
-    const bool ok = i < ntw;
-    const int64_t r = int64_t(tile) * kTileRows + lane;
-#pragma unroll
-    for (int k = 0; k < KC; ++k) {
-      if (ok && k < nk) {
-        const u32x4* src = reinterpret_cast<const u32x4*>(
-            p.trits + ((int64_t(tile) * p.n_groups + c0 + grp[k]) * kTileRows + lane) * 16);
-        wb[slot][k] = __builtin_nontemporal_load(src);
-      } else {
-        wb[slot][k] = u32x4(kZeroCode4);
-      }
-    }
-    alb[slot] = ok ? p.alpha[r] : uint16_t(0);
-    rwl[slot] = ok && lane < nsal ? p.ridx[int64_t(tile) * p.nS + sb + lane] : 0u;
-#pragma unroll
-    for (int u = 0; u < kResBatch; ++u)
-      rvb[slot][u] = ok && u < nsal ? p.rval[(r >> 2) * p.nS + sb + u] : uint16_t(0);
-  };
-  fetch(0, 0);  // one tile in flight during the table build, the rest after it
-  // salient columns relative to the slice's first column (lane u < nsal)
-  const int rcol_l = lane < nsal ? p.S[sb + lane] - int(col0) : 0;
-
-  uint32_t lowb[KC][4];
-#pragma unroll
-  for (int k = 0; k < KC; ++k)
-#pragma unroll
-    for (int q4 = 0; q4 < 4; ++q4) {
-      uint32_t v4 = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v4 |= uint32_t(grp[k] * 64 + ((q4 * 4 + e + lane) & 15) * 4) << (8 * e);
-      lowb[k][q4] = v4;
-    }
-
-  // Table build: entry (group k, slot, code) = sum_i (d_i(code) - 1) v_j x_j,
-  // j = 5 pack + i.  Task = (pack, leading digit d4), 81 codes each.
-  for (int task = tid; task < nk * kGroupPacks * 3; task += NT) {
-    const int pk = task % (nk * kGroupPacks);
-    const int d4 = task / (nk * kGroupPacks);
-    const int k = pk >> 4, slot = pk & 15, cb = pk * 5;
-    float a[5][1];
-#pragma unroll
-    for (int i = 0; i < 5; ++i) a[i][0] = v_lds[cb + i] * x_lds[cb + i];
-    float t[1] = {d4 == 0 ? -a[4][0] : (d4 == 2 ? a[4][0] : 0.0f)};
-    tree<3, 0, 1, ROW>(lut + (d4 * 81 * KC + k) * kGroupPacks + slot, t, a);
-  }
-#pragma unroll
-  for (int u = 1; u < PD; ++u) fetch(u, u);
-  __syncthreads();
-
-  // (3) stream the tiles
-  for (int i0 = 0; i0 < ntw; i0 += PD) {
-#pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      const int i = i0 + u;
-      if (i >= ntw) break;
-      const int tile = tile_lo + wave + WAVES * i;
-      const int64_t r = int64_t(tile) * kTileRows + lane;
-      float acc = 0.0f;
-#pragma unroll
-      for (int k = 0; k < KC; ++k) {
-        if (k >= nk) break;
-        const uint32_t ww[4] = {wb[u][k].x, wb[u][k].y, wb[u][k].z, wb[u][k].w};
-        float e[kGroupPacks];
-#pragma unroll
-        for (int b8 = 0; b8 < kGroupPacks; ++b8) {
-          // [byte0 = low byte, byte1 = code, bytes 2-3 = 0] = code * 256 + low
-          const uint32_t sel = 0x0c0c0000u | (uint32_t(4 + (b8 & 3)) << 8) | uint32_t(b8 & 3);
-          const uint32_t addr = __builtin_amdgcn_perm(ww[b8 >> 2], lowb[k][b8 >> 2], sel);
-          e[b8] = *reinterpret_cast<const float*>(reinterpret_cast<const char*>(lut) + addr);
-        }
-#pragma unroll
-        for (int h = kGroupPacks / 2; h >= 1; h /= 2)
-#pragma unroll
-          for (int q = 0; q < h; ++q) e[q] += e[q + h];
-        acc += e[0];
-      }
-      const float al = h2f(alb[u]);
-      float racc = 0.0f;
-      const uint32_t shift = 2 * ((r >> 2) & 15);
-#pragma unroll
-      for (int s = 0; s < kResBatch; ++s) {
-        if (s >= nsal) break;
-        const uint32_t word = __builtin_amdgcn_readlane(rwl[u], s);
-        const int col = __builtin_amdgcn_readlane(rcol_l, s);
-        if (((word >> shift) & 3u) == uint32_t(r & 3)) racc += h2f(rvb[u][s]) * x_lds[col];
-      }
-      fetch(u, i + PD);  // refill slot u
-      for (int s = sb + kResBatch; s < se; ++s) {  // salient columns beyond one batch
-        const uint32_t word = p.ridx[int64_t(tile) * p.nS + s];
-        if (((word >> shift) & 3u) == uint32_t(r & 3)) racc += h2f(p.rval[(r >> 2) * p.nS + s]) * x_lds[p.S[s] - int(col0)];
-      }
-      const float v = al * acc + racc;
-      if constexpr (ACCUM) {
-        if (r < p.N) __hip_atomic_fetch_add(p.y + r, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      } else if (p.nslices == 1) {
-        if (r < p.N) p.y[r] = v;
-      } else {
-        store_coherent(p.part + int64_t(ks) * p.n_pad + r, v);
-      }
-    }
-  }
-  if (ACCUM || p.nslices == 1) return;
-
-  // (4) last workgroup of the row block to arrive sums the slices in order
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(p.counters + rb, 1u, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-    s_last = prev == uint32_t(p.nslices - 1);
-  }
-  __syncthreads();
-  if (!s_last) return;
-  if (tid == 0)
-    __hip_atomic_store(p.counters + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const int64_t row_lo = int64_t(tile_lo) * kTileRows;
-  const int64_t row_hi = min(p.N, int64_t(tile_hi) * kTileRows);
-  // Every partial of this thread's rows is requested before any is summed.
-  constexpr int RPT = 4, QMAX = 16;  // rows per thread, slices per batch
-  for (int64_t r0 = row_lo + tid; r0 < row_hi; r0 += int64_t(RPT) * NT) {
-    float sum[RPT] = {};
-    for (int q0 = 0; q0 < p.nslices; q0 += QMAX) {
-      float t[RPT][QMAX];
-#pragma unroll
-      for (int h = 0; h < RPT; ++h)
-#pragma unroll
-        for (int u = 0; u < QMAX; ++u) {
-          const int64_t r = r0 + int64_t(h) * NT;
-          t[h][u] = (r < row_hi && q0 + u < p.nslices) ? load_coherent(p.part + int64_t(q0 + u) * p.n_pad + r) : 0.0f;
-        }
-#pragma unroll
-      for (int h = 0; h < RPT; ++h)
-#pragma unroll
-        for (int u = 0; u < QMAX; ++u)
-          if (q0 + u < p.nslices) sum[h] += t[h][u];
-    }
-#pragma unroll
-    for (int h = 0; h < RPT; ++h) {
-      const int64_t r = r0 + int64_t(h) * NT;
-      if (r < row_hi) p.y[r] = sum[h];
     }
   }
 }
@@ -911,7 +684,7 @@ __global__ __launch_bounds__(kFkMaxThreads) void fk_gemv_kernel(const FkArgs p) 
         const bool ok = row_ok && s < se;
         rs_col[u] = ok ? p.S[s] : -1;
         rs_word[u] = ok ? p.ridx[tile * p.nS + s] : 0u;
-        rs_val[u] = ok ? p.rval[(row >> 2) * p.nS + s] : uint16_t(0);
+        rs_val[u] = ok ? p.rval[rval_index(row >> 2, s, p.nS)] : uint16_t(0);
       }
     };
     load_res(0);
@@ -1008,8 +781,6 @@ __global__ __launch_bounds__(kFkMaxThreads) void fk_gemv_kernel(const FkArgs p) 
 // ---------------------------------------------------------------------------
 struct Plan {
   int tpw, nrb, nslices, ks_groups;
-  int rbt;    // batch-1 kernel: row tiles per workgroup
-  int waves;  // batch-1 kernel: wavefronts per workgroup
 };
 
 int kc_for_batch(int B) {
@@ -1017,27 +788,10 @@ int kc_for_batch(int B) {
   return bt == 1 ? 4 : (bt == 2 ? 2 : 1);
 }
 
-constexpr int kB1Target = 512;  // workgroups (two resident per CU)
-
 Plan make_plan(const qtea_desc& d, int B) {
   Plan pl;
   const int64_t n_tiles = d.n_pad / kTileRows;
   const int kc = kc_for_batch(B);
-  if (B == 1) {
-    // One 64-pack slice per workgroup; row tiles split so that about
-    // kB1Target workgroups cover the matrix.
-    pl.ks_groups = kc;
-    pl.nslices = int(cdiv(d.n_groups, kc));
-    const int64_t per_wg = cdiv(n_tiles * pl.nslices, kB1Target);
-    pl.waves = 4;  // two 4-wave workgroups share a CU (each holds a 62 KB table)
-    const int64_t rbt = cdiv(per_wg, pl.waves) * pl.waves;
-    pl.rbt = int(rbt);
-    pl.nrb = int(cdiv(n_tiles, rbt));
-    pl.tpw = 0;
-    return pl;
-  }
-  pl.rbt = 0;
-  pl.waves = kWaves;
   pl.tpw = n_tiles >= 256 ? 2 : 1;
   pl.nrb = int(cdiv(n_tiles, int64_t(kWaves) * pl.tpw));
   const int64_t target_wgs = 640;
@@ -1054,10 +808,14 @@ Plan make_plan(const qtea_desc& d, int B) {
   return pl;
 }
 
+// Batches up to 4 run the factored-table kernel (whole rows per workgroup,
+// no partial sums); larger batches the K-split table kernel.
+bool use_fk(int B) { return B <= 4; }
+
 int64_t workspace_need(const qtea_desc& d, int B) {
   const Plan pl = make_plan(d, B);
   const int64_t counters = align_up(4 * cdiv(d.n_pad / kTileRows, kWaves), kAlign);
-  const int64_t parts = pl.nslices > 1 ? 4 * int64_t(pl.nslices) * B * d.n_pad : 0;
+  const int64_t parts = !use_fk(B) && pl.nslices > 1 ? 4 * int64_t(pl.nslices) * B * d.n_pad : 0;
   return counters + parts;
 }
 
@@ -1157,7 +915,6 @@ hipError_t launch_fk_b(const FkArgs& a, const FkPlan& f, int B, hipStream_t st) 
   }
 }
 
-bool use_fk(int B) { return B <= 4; }
 
 }  // namespace
 
@@ -1317,31 +1074,6 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
     return launch_fk_b(k, f, batch, static_cast<hipStream_t>(stream)) == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
   }
   const int grid = pl.nrb * pl.nslices;
-  if (batch == 1) {
-    B1Args b;
-    b.trits = a.trits;
-    b.alpha = a.alpha;
-    b.v = a.v;
-    b.S = a.S;
-    b.spos = a.spos;
-    b.rval = a.rval;
-    b.ridx = a.ridx;
-    b.x = a.x;
-    b.y = a.y;
-    b.part = a.part;
-    b.counters = a.counters;
-    b.N = a.N;
-    b.K = a.K;
-    b.n_pad = a.n_pad;
-    b.n_groups = a.n_groups;
-    b.n_tiles = a.n_tiles;
-    b.nS = a.nS;
-    b.nslices = pl.nslices;
-    b.rbt = pl.rbt;
-    hipLaunchKernelGGL((lut_gemv_b1_kernel<2, 4, false>), dim3(grid), dim3(256), 0,
-                       static_cast<hipStream_t>(stream), b);
-    return hipGetLastError() == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
-  }
   if (launch_gemv(a, batch, pl.tpw, grid, static_cast<hipStream_t>(stream)) != hipSuccess)
     return QTEA_ERR_HIP;
   return QTEA_OK;

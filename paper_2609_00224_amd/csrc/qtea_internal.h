@@ -1,5 +1,5 @@
 // Internal definitions shared by the library's translation units: layout
-// constants, the device layout arithmetic (layout version 1) and small
+// constants, the device layout arithmetic (layout version 2) and small
 // device helpers.  Not part of the public ABI.
 #ifndef QTEA_INTERNAL_H_
 #define QTEA_INTERNAL_H_
@@ -19,7 +19,7 @@ constexpr int kCodes = 243;      // 3^5
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr uint32_t kZeroCode4 = 0x79797979u;  // four copies of code 121 (all-zero trits)
-constexpr int kLayout = 1;
+constexpr int kLayout = 2;
 constexpr int64_t kAlign = 256;
 constexpr int64_t kHeaderBytes = 256;
 constexpr int kFlagOffset = 128;
@@ -33,6 +33,14 @@ typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) float lds_float;
 
 inline int64_t align_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+// Residual values are stored tile-major: [n_pad/64 tiles][n_salient][16], the
+// sixteen four-row groups of a 64-row tile contiguous for each salient
+// column, so the residual of one tile over a run of salient columns is one
+// contiguous run of 32 bytes per column.  Index of group g, column s:
+__host__ __device__ __forceinline__ int64_t rval_index(int64_t g, int64_t s, int64_t nS) {
+  return ((g >> 4) * nS + s) * 16 + (g & 15);
+}
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 __device__ __forceinline__ float h2f(uint16_t h) {
