@@ -45,7 +45,6 @@ constexpr int kSliceGroups = 4;                           // groups per K slice 
 constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 64
 constexpr int kSliceCols = kSliceGroups * kGroupCols;     // 320
 constexpr int kTabBytes = kCodes * 256;                   // 62,208: code row = 64 packs x 4 bytes
-constexpr int kBuildTasks = kSlicePacks * 9;              // (pack, two leading digits)
 constexpr int kResCols = 16;  // salient columns of a slice staged per wave (more: direct loads)
 constexpr uint32_t kGPlanMagic = 0x51475250u;            // "QGRP"
 constexpr int64_t kPlanProblemsOff = 256;
@@ -67,7 +66,8 @@ struct GProblem {
   int64_t reserved;
 };
 static_assert(sizeof(GProblem) == 128, "plan record size");
-static_assert(kSliceCols % 64 == 0 && kBuildTasks % 64 == 0, "passes of whole waves");
+static_assert(kSliceCols % 64 == 0, "staging by whole waves");
+static_assert(kSlicePacks * 8 == kGT, "one 27-code build task per thread, codes 0..215");
 static_assert(kSliceCols <= kGT, "one staged column per thread");
 
 struct GPlanHeader {
@@ -82,9 +82,9 @@ struct GLds {
   static constexpr int TPW = RP / 64 / kGW;  // 64-row tiles per wave in the residual phase
   static constexpr int GPW = 16 * TPW;       // four-row groups per wave
   static constexpr int QR = 64 / GPW;        // residual lanes per group
-  static constexpr int A = kTabBytes;                     // a_j, fp32 [320]
-  static constexpr int XR = A + 4 * kSliceCols;           // x_j, fp32 [320]
-  static constexpr int RR = XR + 4 * kSliceCols;          // residual row sums, fp32 [RP]
+  static constexpr int ST = kTabBytes;                    // two buffers: a_j fp32 [320], x_j fp32 [320]
+  static constexpr int STB = 8 * kSliceCols;              // bytes of one buffer
+  static constexpr int RR = ST + 2 * STB;                 // residual row sums, fp32 [RP]
   static constexpr int RV = RR + 4 * RP;                  // per wave: fp16 values [TPW][kResCols][16]
   static constexpr int RI = RV + kGW * 1024;              // per wave: u32 positions [2][16], fp32 x [32]
   static constexpr int FLAG = RI + kGW * 256;             // one int
@@ -128,6 +128,11 @@ __device__ __forceinline__ Cursor advance(Cursor c, const GProblem* P) {
   return c;
 }
 
+// Buffer resources (gfx9 family): word 3 of the descriptor for raw byte
+// buffers, and the non-temporal bit of a buffer load's cache policy.
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kAuxNT = 2;
+
 // Selector of v_perm_b32 that forms (byte k of src1) << 8 | (byte k of src0).
 __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
   return 0x0C0C0000u | (uint32_t(k) << 8) | uint32_t(4 + k);
@@ -142,8 +147,6 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   constexpr int TPP = RP / 64;  // tiles per panel
   extern __shared__ float smem[];
   char* lds = reinterpret_cast<char*>(smem);
-  float* a_lds = reinterpret_cast<float*>(lds + L::A);
-  float* xr_lds = reinterpret_cast<float*>(lds + L::XR);
   float* rres = reinterpret_cast<float*>(lds + L::RR);
   int* flag = reinterpret_cast<int*>(lds + L::FLAG);
 
@@ -280,6 +283,21 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   uint16_t al[RF];
   load_alpha(cur, al);
 
+  // stage a slice's activations in buffer b: a_j = v_j x_j (exact in fp32) and x_j
+  auto stage = [&](const Cursor c, int b) {
+    if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
+      const GProblem& pr = P[c.m];
+      const int gcol = c.slice * kSliceCols + tid;
+      const float xf = gcol < pr.K ? h2f(xr) : 0.0f;
+      const float vf = gcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
+      float* st = reinterpret_cast<float*>(lds + L::ST + b * L::STB);
+      st[tid] = vf * xf;
+      st[kSliceCols + tid] = xf;
+    }
+  };
+  stage(cur, 0);
+  __syncthreads();
+
   float acc[RB], racc[4];
 #pragma unroll
   for (int t = 0; t < RB; ++t) acc[t] = 0.0f;
@@ -295,62 +313,74 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
     if (pstart) pstart_slice = cur.slice;
     const int col0 = cur.slice * kSliceCols;
+    const int sb = int((u - ub) & 1);  // staging buffer of this unit
+    const float* a_lds = reinterpret_cast<const float*>(lds + L::ST + sb * L::STB);
+    const float* xr_lds = a_lds + kSliceCols;
 
-    // 1. stage the slice's activations: a_j = v_j x_j (exact in fp32) and x_j
-    if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
-      const int gcol = col0 + tid;
-      const float xf = gcol < pr.K ? h2f(xr) : 0.0f;
-      const float vf = gcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
-      a_lds[tid] = vf * xf;
-      xr_lds[tid] = xf;
-    }
-    __syncthreads();
-
-    // 2. tables: task (pack p, leading digits d4 d3) writes the 27 codes sharing them
+    // 1. tables (the slice's activations were staged before the last barrier).
+    // The 243 codes of a pack are (d4 d3 d2 d1 d0); pass 0: task (pack,
+    // d4 d3) for d4 d3 < 22 writes 27 codes; pass 1: task (pack, d2) writes
+    // the nine codes 22 d2 d1 d0, so that no wave does two 27-code tasks.
+    {
+      const int p = tid & (kSlicePacks - 1);
+      const float a0 = a_lds[5 * p], a1 = a_lds[5 * p + 1], a2 = a_lds[5 * p + 2];
+      const float a3 = a_lds[5 * p + 3], a4 = a_lds[5 * p + 4];
+      const int top = tid / kSlicePacks;  // 0..7: d4 d3 in base 3
+      const int d4 = (top * 11) >> 5;
+      const int d3 = top - 3 * d4;
+      const float t4 = d4 == 0 ? -a4 : (d4 == 2 ? a4 : 0.0f);
+      const float t3 = d3 == 0 ? -a3 : (d3 == 2 ? a3 : 0.0f);
+      const float base = t4 + t3;
+      lds_char* dst = (lds_char*)smem + p * 4 + (27 * d3 + 81 * d4) * 256;
 #pragma unroll
-    for (int it = 0; it < (kBuildTasks + kGT - 1) / kGT; ++it) {
-      const int task = tid + it * kGT;
-      if (w * 64 + it * kGT < kBuildTasks) {  // whole waves (kBuildTasks is a multiple of 64)
-        const int p = task & (kSlicePacks - 1);
-        const int top = task / kSlicePacks;
-        const int d4 = (top * 11) >> 5;
-        const int d3 = top - 3 * d4;
-        const float a0 = a_lds[5 * p], a1 = a_lds[5 * p + 1], a2 = a_lds[5 * p + 2];
-        const float a3 = a_lds[5 * p + 3], a4 = a_lds[5 * p + 4];
-        const float t4 = d4 == 0 ? -a4 : (d4 == 2 ? a4 : 0.0f);
-        const float t3 = d3 == 0 ? -a3 : (d3 == 2 ? a3 : 0.0f);
-        const float base = t4 + t3;
-        lds_char* dst = (lds_char*)smem + p * 4 + (27 * d3 + 81 * d4) * 256;
+      for (int e2 = 0; e2 < 3; ++e2) {
+        const float u2 = e2 == 0 ? base - a2 : (e2 == 1 ? base : base + a2);
 #pragma unroll
-        for (int e2 = 0; e2 < 3; ++e2) {
-          const float u2 = e2 == 0 ? base - a2 : (e2 == 1 ? base : base + a2);
+        for (int e1 = 0; e1 < 3; ++e1) {
+          const float u1 = e1 == 0 ? u2 - a1 : (e1 == 1 ? u2 : u2 + a1);
 #pragma unroll
-          for (int e1 = 0; e1 < 3; ++e1) {
-            const float u1 = e1 == 0 ? u2 - a1 : (e1 == 1 ? u2 : u2 + a1);
-#pragma unroll
-            for (int e0 = 0; e0 < 3; ++e0) {
-              const float u0 = e0 == 0 ? u1 - a0 : (e0 == 1 ? u1 : u1 + a0);
-              *(lds_float*)(dst + (9 * e2 + 3 * e1 + e0) * 256) = u0;
-            }
+          for (int e0 = 0; e0 < 3; ++e0) {
+            const float u0 = e0 == 0 ? u1 - a0 : (e0 == 1 ? u1 : u1 + a0);
+            *(lds_float*)(dst + (9 * e2 + 3 * e1 + e0) * 256) = u0;
           }
-          __builtin_amdgcn_sched_barrier(0);  // nine entries at a time (register pressure)
+        }
+        __builtin_amdgcn_sched_barrier(0);  // nine entries at a time (register pressure)
+      }
+      if (w < 3) {  // codes 216..242 (d4 = d3 = 2): whole waves, task (pack, d2 = w)
+        const float u2 = a4 + a3 + (w == 0 ? -a2 : (w == 1 ? 0.0f : a2));
+        lds_char* dst2 = (lds_char*)smem + p * 4 + (216 + 9 * w) * 256;
+#pragma unroll
+        for (int e1 = 0; e1 < 3; ++e1) {
+          const float u1 = e1 == 0 ? u2 - a1 : (e1 == 1 ? u2 : u2 + a1);
+#pragma unroll
+          for (int e0 = 0; e0 < 3; ++e0) {
+            const float u0 = e0 == 0 ? u1 - a0 : (e0 == 1 ? u1 : u1 + a0);
+            *(lds_float*)(dst2 + (3 * e1 + e0) * 256) = u0;
+          }
         }
       }
     }
     __syncthreads();
 
-    // 3. the next unit's activations and salient range (nxt == cur after the
+    // 2. the next unit's activations and salient range (nxt == cur after the
     // run's last unit: harmless reloads)
     load_xv(nxt, xr, vr);
     const int spv = load_spos(nxt);
 
-    // 4. lookups; each 16-byte unit, once read, is refilled with the next
+    // 3. lookups; each 16-byte unit, once read, is refilled with the next
     // unit's bytes (after the run's last unit all lanes read one 16-byte unit)
+    // Next unit's byte offsets: a uniform per-tile part (scalar offset) plus
+    // this lane's part (group and row within the tile, one vector offset for
+    // all refills), through a buffer resource over the next matrix's packed
+    // bytes (loads past its end would return zeros).  After the run's last
+    // unit every lane reads the first 16 bytes of the matrix.
     const GProblem& pn = P[nxt.m];
-    const gu8* nbase = gptr(pn.trits);
     const int n_ng = pn.n_groups, n_nt = int(pn.n_pad >> 6);
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(pn.trits), 0, int(uint32_t(n_nt) * uint32_t(n_ng) * (kTileRows * kGroupPacks)), kBufferWord3);
     const int n_grp = min(nxt.slice * kSliceGroups + q, n_ng - 1), n_t0 = nxt.panel * TPP + wt;
-    const uint32_t nmask = has_next ? 0xffffffffu : 0u;
+    const uint32_t smask = has_next ? 0xffffffffu : 0u;
+    const uint32_t lane_off = ((uint32_t(n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & smask;
 #pragma unroll
     for (int t = 0; t < RB; ++t) acc[t] = pstart ? 0.0f : acc[t];
 #pragma unroll
@@ -375,13 +405,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       // refill after the last read of the old bytes, into the same registers
       // (a load issued earlier would need other registers and a copy at the
       // loop edge, and the copy would wait for the load)
-      const int tl = min(n_t0 + (kGW / 4) * t, n_nt - 1);
-      const uint32_t noff = ((uint32_t(tl * n_ng + n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & nmask;
-      W[t] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(nbase + noff));
+      const uint32_t tile_off = (uint32_t(min(n_t0 + (kGW / 4) * t, n_nt - 1)) * uint32_t(n_ng) * (kTileRows * kGroupPacks)) & smask;
+      W[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, int(lane_off), int(tile_off), kAuxNT));
       __builtin_amdgcn_sched_barrier(0);
     }
 
-    // 5. residual of this slice: each lane's four rows accumulate in registers
+    // 4. residual of this slice: each lane's four rows accumulate in registers
     // over the panel's slices (fixed order: deterministic)
     const int s_lo = s_lo_c, s_hi = s_hi_c;
     const int ncol = s_hi - s_lo;
@@ -401,12 +430,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       const uint32_t xw = __float_as_uint(xr_lds[xc >= 0 && xc < kSliceCols ? xc : 0]);
       ri_w[lane] = lane < 32 ? ris : xw;
       asm volatile("" ::: "memory");
-      const int nc = ncol < kResCols ? ncol : kResCols;
+      const int nc = grow_ok ? (ncol < kResCols ? ncol : kResCols) : 0;
       for (int c = rq; c < nc; c += QR) {
         const uint16_t hv = reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16];
         const uint32_t idx = (ri_w[16 * rtile + c] >> gsh) & 3u;
         const float xv = __uint_as_float(ri_w[32 + c]);
-        const float t = grow_ok ? h2f(hv) * xv : 0.0f;
+        const float t = h2f(hv) * xv;
 #pragma unroll
         for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
       }
@@ -422,6 +451,9 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         }
       }
     }
+    // the next unit's activations into the other buffer (its last readers,
+    // the previous unit's build and residual, are behind the last barrier)
+    stage(nxt, sb ^ 1);
     if (pend) {
       // the group's four row sums over its QR lanes (shuffles, fixed order)
       float r4[4];
@@ -438,7 +470,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     }
     __syncthreads();
 
-    // 6. panel end: y = alpha * acc + residual (or a partial of a split panel)
+    // 5. panel end: y = alpha * acc + residual (or a partial of a split panel)
     if (pend) {
       float tot[RB];
 #pragma unroll
