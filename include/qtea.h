@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 1
+#define QTEA_ABI_VERSION 2
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -179,7 +179,9 @@ typedef struct qtea_grouped_info {
   int32_t batch;           /* activation rows per problem (only 1 so far) */
   int32_t grid;            /* workgroups of the launch (two per CU)       */
   int32_t rows_per_panel;  /* output rows of one work unit               */
-  int32_t max_parts;       /* runs sharing one panel, at most            */
+  int32_t max_parts;       /* chunks sharing one panel, at most          */
+  int32_t n_chunks;        /* chunks of work units (scheduling grain)    */
+  int32_t n_split_panels;  /* panels whose parts are summed by a second launch */
   int64_t n_units;
   int64_t plan_bytes;      /* device plan buffer size                    */
   int64_t workspace_bytes; /* workspace needed by qtea_grouped_gemv      */
@@ -206,11 +208,14 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
                       qtea_grouped_info* info, void* stream);
 
 /*
- * Run a planned grouped GEMV.  `workspace` (>= info->workspace_bytes) holds
- * the partial rows and arrival counters of panels split between two
- * workgroups; it must be zero-filled before first use and is left
- * zero-filled by every completed call (as for qtea_gemv).  fp32
- * accumulation, run-to-run deterministic.
+ * Run a planned grouped GEMV: one persistent launch, followed by a small
+ * second launch that sums the parts of split panels (when the plan has
+ * any, info->n_split_panels).  `workspace` (>= info->workspace_bytes) holds
+ * the chunk queue counter (its first 4 bytes) and the partial rows of split
+ * panels.  The counter must be zero before the first call (zero-fill the
+ * workspace once); every completed call leaves it at zero.  Calls that may
+ * overlap in time must not share a workspace.  fp32 accumulation, run-to-run
+ * deterministic (parts are summed in a fixed order).
  */
 int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* workspace,
                       int64_t workspace_bytes, void* stream);

@@ -57,7 +57,7 @@ class QteaGroupedInfo(ctypes.Structure):
     _fields_ = [
         ("magic", ctypes.c_uint32), ("n_problems", ctypes.c_int32), ("batch", ctypes.c_int32),
         ("grid", ctypes.c_int32), ("rows_per_panel", ctypes.c_int32), ("max_parts", ctypes.c_int32),
-        ("n_units", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+        ("n_chunks", ctypes.c_int32), ("n_split_panels", ctypes.c_int32), ("n_units", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
     ]
 
 

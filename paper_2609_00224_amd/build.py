@@ -16,6 +16,10 @@ HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
     # keep hand-written and compiler-formed packed fp32 VALU ops out of the code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the library's atomics are single-lane counter updates whose results are
+    # used much later; the wave-level atomic rewrite would wait for every
+    # outstanding load right after each of them
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-Wall", "-Wno-unused-result",
 ]
 

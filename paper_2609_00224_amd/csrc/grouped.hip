@@ -4,29 +4,36 @@
 //
 // Work unit = (problem, panel of RP rows, K slice of 4 sixteen-pack groups =
 // 64 packs = 320 columns).  Units are ordered (problem, panel, slice) with
-// the slice fastest and cut into one contiguous run per workgroup, balanced
-// by weight bytes.  Two 512-thread workgroups share each CU (about 79 KB of
+// the slice fastest.  Two 512-thread workgroups share each CU (about 79 KB of
 // LDS each): while one builds its tables the other streams and looks up, so
-// the phases of one workgroup's units hide behind the other's.  A workgroup
-// walks its run:
+// the phases of one workgroup's units hide behind the other's.  Per unit a
+// workgroup:
 //
-//   - stage a_j = v_j x_j and x_j of the slice in LDS;
-//   - build the full 243-entry table of each of the slice's 64 packs
+//   - stages a_j = v_j x_j and x_j of the slice in LDS;
+//   - builds the full 243-entry table of each of the slice's 64 packs
 //     (62,208 bytes of LDS, one fp32 entry per code and pack);
-//   - add one table entry per packed byte of the panel's rows, the entry
+//   - adds one table entry per packed byte of the panel's rows, the entry
 //     address formed from the byte by a single v_perm_b32;
-//   - add the slice's salient residual;
-//   - at the panel's last slice, write y = alpha * acc + residual.
+//   - adds the slice's salient residual;
+//   - at the panel's last slice, writes y = alpha * acc + residual.
 //
 // While a unit is processed, the next unit's packed bytes, activations,
 // residual and row scales are already in flight: each 16-byte register of
 // packed bytes is refilled with the next unit's bytes as soon as its lookups
-// have been issued, so the weight stream does not stop at unit, panel or
-// problem boundaries.
-// A panel whose slices are split between two runs is reduced through the
-// workspace: each part stores its partial rows, the last part to arrive
-// sums the parts in run order and writes y (fixed order: deterministic).
-// No workgroup ever waits for another one.
+// have been issued, so the weight stream does not stop at unit, panel,
+// problem or chunk boundaries.
+//
+// Scheduling.  The two workgroups of a CU do not progress at the same rate
+// (the older one's waves win instruction issue), so equal static shares
+// leave half of the CUs' workgroups idle long before the launch ends.  The
+// unit list is therefore cut into chunks whose sizes shrink from large to a
+// single unit (guided self-scheduling, planned on the host), and after its
+// first two chunks a workgroup takes the next chunk from a queue counter in
+// the workspace, one chunk ahead of need.  A panel whose slices fall in
+// more than one chunk is split: each part stores its partial rows in the
+// workspace and grouped_reduce_kernel, launched right after, sums the parts
+// in chunk order (fixed order: deterministic whichever workgroup ran which
+// chunk).  No workgroup ever waits for another one.
 #include <stdlib.h>
 
 #include <algorithm>
@@ -72,8 +79,21 @@ static_assert(kSliceCols <= kGT, "one staged column per thread");
 
 struct GPlanHeader {
   uint32_t magic, version;
-  int32_t n_problems, n_wg, rows_per_panel, max_parts, batch, reserved0;
-  int64_t n_units, off_ranges;
+  int32_t n_problems, n_wg, rows_per_panel, max_parts, batch, n_chunks;
+  int64_t n_units, off_chunks, n_grabs, off_splits, n_splits;
+};
+
+// A chunk: units [ub, ue), the first of them at (problem m, panel, slice).
+struct GChunk {
+  int32_t ub, ue, m, panel, slice, reserved[3];
+};
+static_assert(sizeof(GChunk) == 32, "one scalar load per chunk record");
+
+// A panel whose slices fall in more than one chunk: its parts are in the
+// partial slots of chunks ga..gb (slot 2k, except 2ga + 1 when the part in
+// chunk ga starts after that chunk's first unit).
+struct GSplit {
+  int32_t m, panel, ga, gb, ga_odd, reserved[3];
 };
 
 template <int RB>
@@ -152,10 +172,17 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 
   const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
   const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
-  const int64_t* ranges = reinterpret_cast<const int64_t*>(plan + H->off_ranges);
-  const int g = blockIdx.x;
-  const int64_t ub = ranges[g], ue = ranges[g + 1];
-  if (ub >= ue) return;
+  const GChunk* CR = reinterpret_cast<const GChunk*>(plan + H->off_chunks);
+  const int g = blockIdx.x, G = H->n_wg, NC = H->n_chunks;
+  // Chunks g, g + G and g + 2G are this workgroup's first three; every later
+  // chunk is taken from the queue counters[0] (3G + the count before the
+  // increment) at the first unit of a chunk, two chunks ahead of need.  A
+  // chunk's record is loaded one unit before it is used (the loads complete
+  // by the unit's barriers), so a chunk switch never waits for memory.
+  if (g >= NC) return;
+  int c = g, cn = g + G, cnn = g + 2 * G;
+  const uint32_t last_take = uint32_t(H->n_grabs - 1);
+  int* cnext_lds = flag + 1;  // chunk taken from the queue, published at the unit's last barrier
 
   const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, l16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -177,15 +204,10 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     slotreg[d] = r;
   }
 
-  Cursor cur;
-  {
-    int m = 0;
-    while (P[m].unit_base + int64_t(P[m].n_slices) * P[m].n_panels <= ub) ++m;
-    const int64_t local = ub - P[m].unit_base;
-    cur.m = m;
-    cur.panel = int(local / P[m].n_slices);
-    cur.slice = int(local - int64_t(cur.panel) * P[m].n_slices);
-  }
+  GChunk rec_c = CR[c];
+  GChunk rec_cn = CR[min(cn, NC - 1)];
+  int u = rec_c.ub, ue = rec_c.ue;
+  Cursor cur{rec_c.m, rec_c.panel, rec_c.slice};
 
   // Loads.  Every load is unconditional, from an index clamped into its
   // array (groups past the matrix read a real group whose table entries are
@@ -303,17 +325,30 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   for (int t = 0; t < RB; ++t) acc[t] = 0.0f;
 #pragma unroll
   for (int k = 0; k < 4; ++k) racc[k] = 0.0f;
-  int pstart_slice = cur.slice;  // first slice of the open panel in this run
+  int pstart_slice = cur.slice;     // first slice of the open panel part
+  bool part_at_chunk_start = true;  // the open panel part began at its chunk's first unit
+  bool chunk_first = true;
+  int ctaken = NC;  // chunk taken at the current chunk's first unit (NC: none)
 
-  for (int64_t u = ub; u < ue; ++u) {
+  for (int it = 0;; ++it) {
     const GProblem& pr = P[cur.m];
-    const bool has_next = u + 1 < ue;
-    const Cursor nxt = has_next ? advance(cur, P) : cur;
-    const bool pstart = (cur.slice == 0) || (u == ub);
-    const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
-    if (pstart) pstart_slice = cur.slice;
+    const bool chunk_last = u + 1 == ue;
+    const bool has_next = !chunk_last || cn < NC;
+    const Cursor nxt = !chunk_last ? advance(cur, P) : (has_next ? Cursor{rec_cn.m, rec_cn.panel, rec_cn.slice} : cur);
+    // record of the chunk after the next one, used at the next chunk switch
+    const GChunk rec_cnn = CR[min(cnn, NC - 1)];
+    const bool pstart = (cur.slice == 0) || chunk_first;
+    const bool pend = (cur.slice == pr.n_slices - 1) || chunk_last;
+    if (pstart) {
+      pstart_slice = cur.slice;
+      part_at_chunk_start = chunk_first;
+    }
+    // at a chunk's first unit, take the chunk after the next one from the queue
+    const bool take = chunk_first && cnn < NC;
+    uint32_t taken = 0;
+    if (take && tid == 0) taken = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int col0 = cur.slice * kSliceCols;
-    const int sb = int((u - ub) & 1);  // staging buffer of this unit
+    const int sb = it & 1;  // staging buffer of this unit
     const float* a_lds = reinterpret_cast<const float*>(lds + L::ST + sb * L::STB);
     const float* xr_lds = a_lds + kSliceCols;
 
@@ -454,6 +489,11 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     // the next unit's activations into the other buffer (its last readers,
     // the previous unit's build and residual, are behind the last barrier)
     stage(nxt, sb ^ 1);
+    if (take && tid == 0) {
+      *cnext_lds = 3 * G + int(taken);
+      // the last of the launch's takes resets the queue for the next launch
+      if (taken == last_take) __hip_atomic_store(counters, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     if (pend) {
       // the group's four row sums over its QR lanes (shuffles, fixed order)
       float r4[4];
@@ -498,40 +538,28 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         for (int i = 0; i < RF; ++i)
           if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
       } else {
-        // split panel: parts are the runs that hold any of its units
-        const int64_t p0 = pr.unit_base + int64_t(cur.panel) * pr.n_slices;
-        const int64_t p1 = p0 + pr.n_slices;
-        int ga = g;
-        while (ranges[ga] > p0) --ga;
-        int gb = g;
-        while (ranges[gb + 1] < p1) ++gb;
-        int nparts = 0, mypart = 0;
-        for (int k = ga; k <= gb; ++k) {
-          if (ranges[k] < ranges[k + 1]) {
-            if (k == g) mypart = nparts;
-            ++nparts;
-          }
-        }
-        float* slot = part + (int64_t(ga) * H->max_parts) * RP;
+        // split panel: this chunk's part goes to its partial slot (2c for a
+        // part holding the chunk's first unit, 2c + 1 for a part starting
+        // later in the chunk); grouped_reduce_kernel sums the parts after
+        // the launch, in chunk order
+        gf32* dst = (gf32*)(part + (2 * int64_t(c) + (part_at_chunk_start ? 0 : 1)) * RP);
 #pragma unroll
-        for (int i = 0; i < RF; ++i) store_coherent(slot + int64_t(mypart) * RP + prow[i], val[i]);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (tid == 0) {
-          const uint32_t prev = __hip_atomic_fetch_add(counters + ga, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          *flag = prev == uint32_t(nparts - 1);
-        }
-        __syncthreads();
-        if (*flag) {
-#pragma unroll
-          for (int i = 0; i < RF; ++i) {
-            float sum = 0.0f;
-            for (int k = 0; k < nparts; ++k) sum += load_coherent(slot + int64_t(k) * RP + prow[i]);
-            if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = sum;
-          }
-          if (tid == 0) __hip_atomic_store(counters + ga, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+        for (int i = 0; i < RF; ++i) dst[prow[i]] = val[i];
       }
+    }
+    if (!has_next) break;
+    if (take) ctaken = __builtin_amdgcn_readfirstlane(*cnext_lds);  // written before the last barrier
+    chunk_first = chunk_last;
+    if (chunk_last) {
+      c = cn;
+      u = rec_cn.ub;
+      ue = rec_cn.ue;
+      cn = cnn;
+      rec_cn = rec_cnn;
+      cnn = ctaken;
+      ctaken = NC;
+    } else {
+      ++u;
     }
     s_lo_c = __builtin_amdgcn_readlane(spv, 0);
     s_hi_c = __builtin_amdgcn_readlane(spv, 1);
@@ -541,10 +569,50 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   }
 }
 
+// Sums the parts of every split panel in chunk order (deterministic) and
+// writes its rows of y: one workgroup per split panel, four consecutive
+// rows per thread (16-byte loads of every part), kRedBatch parts' loads in
+// flight at a time.
+constexpr int kRedBatch = 8;
+
+template <int RP>
+__global__ __launch_bounds__(RP / 4) void grouped_reduce_kernel(const uint8_t* __restrict__ plan,
+                                                                const float* __restrict__ part) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
+  const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
+  const GSplit sd = reinterpret_cast<const GSplit*>(plan + H->off_splits)[blockIdx.x];
+  const int row = 4 * threadIdx.x;
+  f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int k0 = sd.ga; k0 <= sd.gb; k0 += kRedBatch) {
+    f32x4 t[kRedBatch];
+#pragma unroll
+    for (int j = 0; j < kRedBatch; ++j) {
+      const int k = min(k0 + j, sd.gb);
+      const int64_t slot = 2 * int64_t(k) + (k == sd.ga ? sd.ga_odd : 0);
+      t[j] = *reinterpret_cast<const f32x4*>(part + slot * RP + row);
+    }
+#pragma unroll
+    for (int j = 0; j < kRedBatch; ++j)
+      if (k0 + j <= sd.gb) sum += t[j];
+  }
+  const GProblem& pr = P[sd.m];
+  const int64_t r = int64_t(sd.panel) * RP + row;
+  float* y = pr.y;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (r + i < pr.N) y[r + i] = sum[i];
+}
+
 // ---------------------------------------------------------------------------
 // Host planning.
 // ---------------------------------------------------------------------------
 constexpr int kMaxRB = 8;
+// Chunks: the unit list is cut into chunks whose sizes shrink from about
+// 1/(kGuide G) of the remaining work to a single unit (guided self-
+// scheduling), at most kMaxChunksPerWg per workgroup on average.
+constexpr int kGuide = 3;
+constexpr int kMaxChunksPerWg = 16;
 
 int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   *n_slices = int(cdiv(d.n_groups, kSliceGroups));
@@ -579,10 +647,15 @@ int grid_size() {
 }
 
 template <int RB>
-hipError_t launch_grouped(const uint8_t* plan, int grid, float* part, uint32_t* counters, hipStream_t st) {
+hipError_t launch_grouped(const uint8_t* plan, int grid, int n_splits, float* part, uint32_t* counters,
+                          hipStream_t st) {
   const hipError_t e = set_lds_attr<RB>();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(grouped_gemv_kernel<RB>, dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan, part, counters);
+  if (n_splits > 0) {
+    constexpr int RP = GLds<RB>::RP;
+    hipLaunchKernelGGL(grouped_reduce_kernel<RP>, dim3(n_splits), dim3(RP / 4), 0, st, plan, part);
+  }
   return hipGetLastError();
 }
 
@@ -594,7 +667,9 @@ int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes) {
   if (!out_bytes || n_problems < 1) return QTEA_ERR_INVALID_ARG;
   const int G = grid_size();
   if (G < 1) return QTEA_ERR_HIP;
-  *out_bytes = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign) + 8 * int64_t(G + 1);
+  const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
+  *out_bytes = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign) +
+               align_up(int64_t(sizeof(GChunk)) * max_chunks, kAlign) + int64_t(sizeof(GSplit)) * max_chunks;
   return QTEA_OK;
 }
 
@@ -629,19 +704,34 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   }
   const int RP = GLds<kMaxRB>::RP / kMaxRB * RB;
 
-  const int64_t off_ranges = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
+  const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
+  const int64_t off_chunks = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
+  const int64_t off_splits = off_chunks + align_up(int64_t(sizeof(GChunk)) * max_chunks, kAlign);
   uint8_t* hbuf = static_cast<uint8_t*>(calloc(1, size_t(need)));
   if (!hbuf) return QTEA_ERR_INVALID_ARG;
   GPlanHeader* H = reinterpret_cast<GPlanHeader*>(hbuf);
   GProblem* P = reinterpret_cast<GProblem*>(hbuf + kPlanProblemsOff);
-  int64_t* ranges = reinterpret_cast<int64_t*>(hbuf + off_ranges);
+  GChunk* chunks = reinterpret_cast<GChunk*>(hbuf + off_chunks);
+  std::vector<int64_t> ranges(size_t(max_chunks) + 1, 0);  // chunk k holds units [ranges[k], ranges[k + 1])
+  GSplit* splits = reinterpret_cast<GSplit*>(hbuf + off_splits);
 
-  // unit costs: packed bytes of the unit plus a fixed table-build share
-  std::vector<int64_t> unit_cost;
+  // unit costs: packed bytes of the unit plus a fixed table-build share;
+  // prefix sums of the costs, and the end (exclusive) of each unit's panel
+  std::vector<int64_t> prefix(1, 0), panel_end;
+  std::vector<GChunk> ucur;
   int64_t total_units = 0;
+  // Problems are laid out with the most K slices per panel first (stable),
+  // so that the small chunks at the end of the unit list split panels of
+  // few slices.  The kernel only needs each problem's units to be
+  // contiguous; outputs are addressed through each problem's own record.
+  std::vector<int> order(static_cast<size_t>(n_problems));
+  for (int m = 0; m < n_problems; ++m) order[size_t(m)] = m;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int a, int b) { return descs[a].n_groups > descs[b].n_groups; });
   for (int m = 0; m < n_problems; ++m) {
-    const qtea_desc& d = descs[m];
-    const uint8_t* pk = static_cast<const uint8_t*>(packed[m]);
+    const int src = order[size_t(m)];
+    const qtea_desc& d = descs[src];
+    const uint8_t* pk = static_cast<const uint8_t*>(packed[src]);
     GProblem& pr = P[m];
     pr.trits = pk + d.off_trits;
     pr.alpha = reinterpret_cast<const uint16_t*>(pk + d.off_alpha);
@@ -650,8 +740,8 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
     pr.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
     pr.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
     pr.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
-    pr.x = x[m];
-    pr.y = y[m];
+    pr.x = x[src];
+    pr.y = y[src];
     pr.N = d.N;
     pr.K = d.K;
     pr.n_pad = d.n_pad;
@@ -664,46 +754,87 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
     pr.unit_base = total_units;
     for (int p = 0; p < np; ++p) {
       const int64_t rows = std::min<int64_t>(RP, d.n_pad - int64_t(p) * RP);
+      const int64_t pe = total_units + int64_t(p + 1) * ns;
       for (int s = 0; s < ns; ++s) {
         const int64_t groups = std::min<int64_t>(kSliceGroups, d.n_groups - int64_t(s) * kSliceGroups);
-        unit_cost.push_back(rows * groups * kGroupPacks + 8192);
+        prefix.push_back(prefix.back() + rows * groups * kGroupPacks + 8192);
+        panel_end.push_back(pe);
+        ucur.push_back(GChunk{0, 0, m, p, s, {0, 0, 0}});
       }
     }
     total_units += int64_t(ns) * np;
   }
-  // contiguous runs of balanced cost
-  int64_t total_cost = 0;
-  for (int64_t c : unit_cost) total_cost += c;
-  {
-    int64_t acc = 0, u = 0;
-    ranges[0] = 0;
-    for (int k = 1; k < G; ++k) {
-      const int64_t target = (total_cost * k) / G;
-      while (u < total_units && acc + unit_cost[size_t(u)] / 2 <= target) acc += unit_cost[size_t(u++)];
-      ranges[k] = u;
-    }
-    ranges[G] = total_units;
+  if (total_units >= (int64_t(1) << 31)) {  // unit indices are 32-bit on the device
+    free(hbuf);
+    return QTEA_ERR_INVALID_ARG;
   }
-  // largest number of runs sharing one panel
+  // chunks: guided sizes, a chunk that reaches the end of its panel (or
+  // several panels) within half a target taking them whole, so that most
+  // small panels are not split
+  int64_t n_chunks = 0;
+  {
+    const int64_t total_cost = prefix.back();
+    const int64_t unit_min = prefix[1] - prefix[0];
+    int64_t u = 0;
+    ranges[0] = 0;
+    while (u < total_units) {
+      const int64_t rem = total_cost - prefix[size_t(u)];
+      const int64_t target = std::max<int64_t>(unit_min, rem / (int64_t(kGuide) * G));
+      int64_t e = u;
+      if (n_chunks + 1 == max_chunks) {
+        e = total_units;  // chunk budget spent: the rest is one chunk
+      } else {
+        while (e < total_units) {
+          const int64_t pe = panel_end[size_t(e)];
+          const int64_t have = prefix[size_t(e)] - prefix[size_t(u)];
+          if (have + prefix[size_t(pe)] - prefix[size_t(e)] <= target + target / 2) {
+            e = pe;  // the rest of this panel fits
+            if (prefix[size_t(e)] - prefix[size_t(u)] >= target) break;
+            continue;
+          }
+          if (e > u && have >= target / 2) break;  // cut at the panel boundary
+          while (e < pe && prefix[size_t(e)] - prefix[size_t(u)] < target) ++e;
+          break;
+        }
+      }
+      chunks[n_chunks] = ucur[size_t(u)];
+      chunks[n_chunks].ub = int32_t(u);
+      chunks[n_chunks].ue = int32_t(e);
+      ranges[size_t(++n_chunks)] = e;
+      u = e;
+    }
+  }
+  // split panels (a chunk is the first chunk of at most one of them, so
+  // there are at most n_chunks), and the largest number of parts of one
   int max_parts = 1;
+  int64_t n_splits = 0;
   for (int m = 0; m < n_problems; ++m) {
     for (int p = 0; p < P[m].n_panels; ++p) {
       const int64_t p0 = P[m].unit_base + int64_t(p) * P[m].n_slices, p1 = p0 + P[m].n_slices;
-      int parts = 0;
-      for (int k = 0; k < G; ++k)
-        if (ranges[k] < ranges[k + 1] && ranges[k] < p1 && ranges[k + 1] > p0) ++parts;
-      if (parts > max_parts) max_parts = parts;
+      const auto rb = ranges.begin(), re = ranges.begin() + n_chunks + 1;
+      const int ga = int(std::upper_bound(rb, re, p0) - rb) - 1;
+      const int gb = int(std::lower_bound(rb, re, p1) - rb) - 1;
+      if (gb > ga) splits[n_splits++] = GSplit{m, p, ga, gb, p0 > ranges[size_t(ga)] ? 1 : 0, {0, 0, 0}};
+      max_parts = std::max(max_parts, gb - ga + 1);
     }
   }
+  // queue takes of one launch: every chunk past the first 3G, plus one
+  // final take by each workgroup that has a third chunk
+  const int64_t n_grabs = std::max<int64_t>(0, n_chunks - 3 * int64_t(G)) +
+                          std::min<int64_t>(G, std::max<int64_t>(0, n_chunks - 2 * int64_t(G)));
   H->magic = kGPlanMagic;
-  H->version = 1;
+  H->version = 2;
   H->n_problems = n_problems;
   H->n_wg = G;
   H->rows_per_panel = RP;
   H->max_parts = max_parts;
   H->batch = batch;
+  H->n_chunks = int32_t(n_chunks);
   H->n_units = total_units;
-  H->off_ranges = off_ranges;
+  H->off_chunks = off_chunks;
+  H->n_grabs = n_grabs;
+  H->off_splits = off_splits;
+  H->n_splits = n_splits;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(plan, hbuf, size_t(need), hipMemcpyHostToDevice, st);
@@ -717,9 +848,11 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   info->grid = G;
   info->rows_per_panel = RP;
   info->max_parts = max_parts;
+  info->n_chunks = int32_t(n_chunks);
+  info->n_split_panels = int32_t(n_splits);
   info->n_units = total_units;
   info->plan_bytes = need;
-  info->workspace_bytes = align_up(4 * int64_t(G), kAlign) + int64_t(G) * max_parts * RP * 4;
+  info->workspace_bytes = kAlign + 2 * n_chunks * RP * 4;
   return QTEA_OK;
 }
 
@@ -729,13 +862,13 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   if (!workspace || workspace_bytes < info->workspace_bytes) return QTEA_ERR_WORKSPACE;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
-  float* part = reinterpret_cast<float*>(ws + align_up(4 * int64_t(info->grid), kAlign));
+  float* part = reinterpret_cast<float*>(ws + kAlign);
   const uint8_t* pl = static_cast<const uint8_t*>(plan);
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
   switch (info->rows_per_panel) {
-    case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, part, counters, st); break;
-    case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, part, counters, st); break;
+    case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+    case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, info->n_split_panels, part, counters, st); break;
     default: return QTEA_ERR_INVALID_ARG;
   }
   return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
