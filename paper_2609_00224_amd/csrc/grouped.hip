@@ -174,13 +174,13 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
   const GChunk* CR = reinterpret_cast<const GChunk*>(plan + H->off_chunks);
   const int g = blockIdx.x, G = H->n_wg, NC = H->n_chunks;
-  // Chunks g, g + G and g + 2G are this workgroup's first three; every later
-  // chunk is taken from the queue counters[0] (3G + the count before the
-  // increment) at the first unit of a chunk, two chunks ahead of need.  A
-  // chunk's record is loaded one unit before it is used (the loads complete
-  // by the unit's barriers), so a chunk switch never waits for memory.
+  // Chunks g and g + G are this workgroup's first two; every later chunk is
+  // taken from the queue counters[0] (2G + the count before the increment)
+  // at the first unit of a chunk, one chunk ahead of need.  The next chunk's
+  // record is loaded at the top of every unit and first used after the
+  // table build's barrier, so a chunk switch does not wait for it.
   if (g >= NC) return;
-  int c = g, cn = g + G, cnn = g + 2 * G;
+  int c = g, cn = g + G;
   const uint32_t last_take = uint32_t(H->n_grabs - 1);
   int* cnext_lds = flag + 1;  // chunk taken from the queue, published at the unit's last barrier
 
@@ -205,7 +205,6 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   }
 
   GChunk rec_c = CR[c];
-  GChunk rec_cn = CR[min(cn, NC - 1)];
   int u = rec_c.ub, ue = rec_c.ue;
   Cursor cur{rec_c.m, rec_c.panel, rec_c.slice};
 
@@ -334,9 +333,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const GProblem& pr = P[cur.m];
     const bool chunk_last = u + 1 == ue;
     const bool has_next = !chunk_last || cn < NC;
+    const GChunk rec_cn = CR[min(cn, NC - 1)];
     const Cursor nxt = !chunk_last ? advance(cur, P) : (has_next ? Cursor{rec_cn.m, rec_cn.panel, rec_cn.slice} : cur);
-    // record of the chunk after the next one, used at the next chunk switch
-    const GChunk rec_cnn = CR[min(cnn, NC - 1)];
     const bool pstart = (cur.slice == 0) || chunk_first;
     const bool pend = (cur.slice == pr.n_slices - 1) || chunk_last;
     if (pstart) {
@@ -344,7 +342,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       part_at_chunk_start = chunk_first;
     }
     // at a chunk's first unit, take the chunk after the next one from the queue
-    const bool take = chunk_first && cnn < NC;
+    const bool take = chunk_first && cn < NC;
     uint32_t taken = 0;
     if (take && tid == 0) taken = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int col0 = cur.slice * kSliceCols;
@@ -490,7 +488,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     // the previous unit's build and residual, are behind the last barrier)
     stage(nxt, sb ^ 1);
     if (take && tid == 0) {
-      *cnext_lds = 3 * G + int(taken);
+      *cnext_lds = 2 * G + int(taken);
       // the last of the launch's takes resets the queue for the next launch
       if (taken == last_take) __hip_atomic_store(counters, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -554,9 +552,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       c = cn;
       u = rec_cn.ub;
       ue = rec_cn.ue;
-      cn = cnn;
-      rec_cn = rec_cnn;
-      cnn = ctaken;
+      cn = ctaken;
       ctaken = NC;
     } else {
       ++u;
@@ -818,10 +814,10 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
       max_parts = std::max(max_parts, gb - ga + 1);
     }
   }
-  // queue takes of one launch: every chunk past the first 3G, plus one
-  // final take by each workgroup that has a third chunk
-  const int64_t n_grabs = std::max<int64_t>(0, n_chunks - 3 * int64_t(G)) +
-                          std::min<int64_t>(G, std::max<int64_t>(0, n_chunks - 2 * int64_t(G)));
+  // queue takes of one launch: every chunk past the first 2G, plus one
+  // final take by each workgroup that has a second chunk
+  const int64_t n_grabs = std::max<int64_t>(0, n_chunks - 2 * int64_t(G)) +
+                          std::min<int64_t>(G, std::max<int64_t>(0, n_chunks - G));
   H->magic = kGPlanMagic;
   H->version = 2;
   H->n_problems = n_problems;
