@@ -119,6 +119,8 @@ def time_graph(g, stream, reps, warmup):
 
 
 def kernel_name(B, grouped=False, rows_per_panel=1024):
+    if grouped and B > 1:
+        return f"grouped_mma_kernel<{1 if B <= 8 else 2}>"  # hi/lo activation halves in one or two MFMAs
     if grouped:
         return f"grouped_gemv_kernel<{rows_per_panel // 128}>"  # 8 waves x 16 rows per row block
     return f"fk_gemv_kernel<{B}>" if B <= 4 else f"lut_gemv_kernel<{B}, 2>"
@@ -262,9 +264,9 @@ def main():
         f"({gbs_chain / HBM_PEAK_GBS:.1%} of peak)")
     del g
 
-    grouped = B == 1 and not args.chained_only
+    grouped = not args.chained_only
     if grouped:
-        gp = q.plan_grouped([m["pm"] for m in mats], [m["x"] for m in mats], [m["y"] for m in mats])
+        gp = q.plan_grouped([m["pm"] for m in mats], [m["x"] for m in mats], [m["y"] for m in mats], batch=B)
         gg = capture_grouped(gp, stream)
         ms = time_graph(gg, stream, args.steps, args.warmup)
         log(f"{wl.name} B={B} grouped: {ms * 1e3:.1f} us/token ({gp.info.n_units} units, "

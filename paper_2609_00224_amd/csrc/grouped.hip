@@ -39,62 +39,24 @@
 #include <algorithm>
 #include <vector>
 
-#include "qtea_internal.h"
+#include "grouped_plan.h"
 
 namespace {
 
 using namespace qtea_detail;
+using namespace qtea_grouped;
 
 constexpr int kGT = 512;                                  // threads per workgroup
 constexpr int kGW = kGT / 64;                             // waves per workgroup
 constexpr int kWgPerCu = 2;                               // workgroups sharing a CU
-constexpr int kSliceGroups = 4;                           // groups per K slice (one per quarter-wave)
-constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 64
-constexpr int kSliceCols = kSliceGroups * kGroupCols;     // 320
 constexpr int kTabBytes = kCodes * 256;                   // 62,208: code row = 64 packs x 4 bytes
 constexpr int kResCols = 16;  // salient columns of a slice staged per wave (more: direct loads)
-constexpr uint32_t kGPlanMagic = 0x51475250u;            // "QGRP"
-constexpr int64_t kPlanProblemsOff = 256;
 static_assert(kSlicePacks * 4 == 256, "one table row of 256 bytes per code");
 
-struct GProblem {
-  const uint8_t* trits;
-  const uint16_t* alpha;
-  const uint16_t* v;
-  const int32_t* S;
-  const int32_t* spos;
-  const uint16_t* rval;
-  const uint32_t* ridx;
-  const uint16_t* x;
-  float* y;
-  int64_t N, K, n_pad;
-  int32_t n_groups, nS, n_slices, n_panels;
-  int64_t unit_base;
-  int64_t reserved;
-};
-static_assert(sizeof(GProblem) == 128, "plan record size");
 static_assert(kSliceCols % 64 == 0, "staging by whole waves");
 static_assert(kSlicePacks * 8 == kGT, "one 27-code build task per thread, codes 0..215");
 static_assert(kSliceCols <= kGT, "one staged column per thread");
 
-struct GPlanHeader {
-  uint32_t magic, version;
-  int32_t n_problems, n_wg, rows_per_panel, max_parts, batch, n_chunks;
-  int64_t n_units, off_chunks, n_grabs, off_splits, n_splits;
-};
-
-// A chunk: units [ub, ue), the first of them at (problem m, panel, slice).
-struct GChunk {
-  int32_t ub, ue, m, panel, slice, reserved[3];
-};
-static_assert(sizeof(GChunk) == 32, "one scalar load per chunk record");
-
-// A panel whose slices fall in more than one chunk: its parts are in the
-// partial slots of chunks ga..gb (slot 2k, except 2ga + 1 when the part in
-// chunk ga starts after that chunk's first unit).
-struct GSplit {
-  int32_t m, panel, ga, gb, ga_odd, reserved[3];
-};
 
 template <int RB>
 struct GLds {
@@ -114,44 +76,7 @@ static_assert(GLds<4>::TPW == 1 && GLds<8>::TPW == 2, "one or two tiles per wave
 static_assert(2 * kResCols * 32 == 1024, "one 16-byte load per lane stages two tiles' values");
 static_assert(kWgPerCu * GLds<8>::BYTES <= 160 * 1024, "two workgroups per CU");
 
-typedef __attribute__((address_space(1))) const uint8_t gu8;
-typedef __attribute__((address_space(1))) const uint16_t gu16;
-typedef __attribute__((address_space(1))) const uint32_t gu32;
-typedef __attribute__((address_space(1))) const int32_t gi32;
-typedef __attribute__((address_space(1))) const u32x4 gu32x4;
-typedef __attribute__((address_space(1))) float gf32;
 
-// Pointers read from the plan are generic; loads through them would be flat
-// loads (which also hold the LDS wait counter).  They all point to global
-// memory, so they are cast to the global address space.
-__device__ __forceinline__ gu8* gptr(const uint8_t* p) { return (gu8*)p; }
-__device__ __forceinline__ gu16* gptr(const uint16_t* p) { return (gu16*)p; }
-__device__ __forceinline__ gu32* gptr(const uint32_t* p) { return (gu32*)p; }
-__device__ __forceinline__ gi32* gptr(const int32_t* p) { return (gi32*)p; }
-// Read-only and read with a uniform index: the constant address space lets
-// the compiler use scalar loads, which do not wait behind the vector loads.
-typedef __attribute__((address_space(4))) const int32_t ci32;
-__device__ __forceinline__ ci32* cptr(const int32_t* p) { return (ci32*)p; }
-
-struct Cursor {
-  int m, panel, slice;
-};
-
-__device__ __forceinline__ Cursor advance(Cursor c, const GProblem* P) {
-  if (++c.slice == P[c.m].n_slices) {
-    c.slice = 0;
-    if (++c.panel == P[c.m].n_panels) {
-      c.panel = 0;
-      ++c.m;
-    }
-  }
-  return c;
-}
-
-// Buffer resources (gfx9 family): word 3 of the descriptor for raw byte
-// buffers, and the non-temporal bit of a buffer load's cache policy.
-constexpr int kBufferWord3 = 0x00020000;
-constexpr int kAuxNT = 2;
 
 // Selector of v_perm_b32 that forms (byte k of src1) << 8 | (byte k of src0).
 __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
@@ -567,8 +492,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 
 // Sums the parts of every split panel in chunk order (deterministic) and
 // writes its rows of y: one workgroup per split panel, four consecutive
-// rows per thread (16-byte loads of every part), kRedBatch parts' loads in
-// flight at a time.
+// rows per thread and batch row (16-byte loads of every part), kRedBatch
+// parts' loads in flight at a time.
 constexpr int kRedBatch = 8;
 
 template <int RP>
@@ -578,26 +503,29 @@ __global__ __launch_bounds__(RP / 4) void grouped_reduce_kernel(const uint8_t* _
   const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
   const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
   const GSplit sd = reinterpret_cast<const GSplit*>(plan + H->off_splits)[blockIdx.x];
+  const int B = H->batch;
   const int row = 4 * threadIdx.x;
-  f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int k0 = sd.ga; k0 <= sd.gb; k0 += kRedBatch) {
-    f32x4 t[kRedBatch];
-#pragma unroll
-    for (int j = 0; j < kRedBatch; ++j) {
-      const int k = min(k0 + j, sd.gb);
-      const int64_t slot = 2 * int64_t(k) + (k == sd.ga ? sd.ga_odd : 0);
-      t[j] = *reinterpret_cast<const f32x4*>(part + slot * RP + row);
-    }
-#pragma unroll
-    for (int j = 0; j < kRedBatch; ++j)
-      if (k0 + j <= sd.gb) sum += t[j];
-  }
   const GProblem& pr = P[sd.m];
   const int64_t r = int64_t(sd.panel) * RP + row;
-  float* y = pr.y;
+  for (int b = 0; b < B; ++b) {  // a part's partial rows: [batch row][RP]
+    f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int k0 = sd.ga; k0 <= sd.gb; k0 += kRedBatch) {
+      f32x4 t[kRedBatch];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    if (r + i < pr.N) y[r + i] = sum[i];
+      for (int j = 0; j < kRedBatch; ++j) {
+        const int k = min(k0 + j, sd.gb);
+        const int64_t slot = 2 * int64_t(k) + (k == sd.ga ? sd.ga_odd : 0);
+        t[j] = *reinterpret_cast<const f32x4*>(part + (slot * B + b) * RP + row);
+      }
+#pragma unroll
+      for (int j = 0; j < kRedBatch; ++j)
+        if (k0 + j <= sd.gb) sum += t[j];
+    }
+    float* y = pr.y + int64_t(b) * pr.N;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (r + i < pr.N) y[r + i] = sum[i];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -626,6 +554,13 @@ hipError_t set_lds_attr() {
     done = true;
   }
   return hipSuccess;
+}
+
+int cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return n;
 }
 
 // Workgroups of the launch: kWgPerCu per CU when that many fit (they do on
@@ -674,12 +609,17 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
                       qtea_grouped_info* info, void* stream) {
   if (!descs || !packed || !x || !y || !plan || !info || n_problems < 1) return QTEA_ERR_INVALID_ARG;
   info->magic = 0;
-  if (batch != 1) return QTEA_ERR_BATCH;
+  if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
   int64_t need = 0;
   const int st_plan = qtea_grouped_plan_bytes(n_problems, &need);
   if (st_plan != QTEA_OK) return st_plan;
   if (plan_bytes < need) return QTEA_ERR_WORKSPACE;
-  const int G = grid_size();
+  // batch 1: the table kernel, two workgroups per CU and the chunk queue;
+  // batch 2..16: the matrix-core kernel, one workgroup per CU and one
+  // static run of units each
+  const bool mma = batch > 1;
+  const int G = mma ? cu_count() : grid_size();
+  if (G < 1) return QTEA_ERR_HIP;
   for (int m = 0; m < n_problems; ++m) {
     if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
     // the kernel addresses the packed bytes and the residual with 32-bit offsets
@@ -690,7 +630,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
 
   // rows per panel: the largest that still gives every workgroup several units
   int RB = kMaxRB;
-  for (; RB > 4; RB /= 2) {
+  for (; !mma && RB > 4; RB /= 2) {
     int64_t units = 0;
     for (int m = 0; m < n_problems; ++m) {
       int ns, np;
@@ -698,7 +638,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
     }
     if (units >= 4 * int64_t(G)) break;
   }
-  const int RP = GLds<kMaxRB>::RP / kMaxRB * RB;
+  const int RP = mma ? grouped_mma_rows_per_panel() : GLds<kMaxRB>::RP / kMaxRB * RB;
 
   const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
   const int64_t off_chunks = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
@@ -768,7 +708,22 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   // several panels) within half a target taking them whole, so that most
   // small panels are not split
   int64_t n_chunks = 0;
-  {
+  if (mma) {
+    // one contiguous run of balanced cost per workgroup
+    const int64_t total_cost = prefix.back();
+    int64_t u = 0;
+    ranges[0] = 0;
+    for (int k = 1; k <= G && u < total_units; ++k) {
+      int64_t e = k == G ? total_units
+                         : int64_t(std::lower_bound(prefix.begin(), prefix.end(), (total_cost * k) / G) - prefix.begin());
+      e = std::min(total_units, std::max(e, u + 1));
+      chunks[n_chunks] = ucur[size_t(u)];
+      chunks[n_chunks].ub = int32_t(u);
+      chunks[n_chunks].ue = int32_t(e);
+      ranges[size_t(++n_chunks)] = e;
+      u = e;
+    }
+  } else {
     const int64_t total_cost = prefix.back();
     const int64_t unit_min = prefix[1] - prefix[0];
     int64_t u = 0;
@@ -816,8 +771,9 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   }
   // queue takes of one launch: every chunk past the first 2G, plus one
   // final take by each workgroup that has a second chunk
-  const int64_t n_grabs = std::max<int64_t>(0, n_chunks - 2 * int64_t(G)) +
-                          std::min<int64_t>(G, std::max<int64_t>(0, n_chunks - G));
+  const int64_t n_grabs = mma ? 0
+                              : std::max<int64_t>(0, n_chunks - 2 * int64_t(G)) +
+                                    std::min<int64_t>(G, std::max<int64_t>(0, n_chunks - G));
   H->magic = kGPlanMagic;
   H->version = 2;
   H->n_problems = n_problems;
@@ -848,7 +804,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   info->n_split_panels = int32_t(n_splits);
   info->n_units = total_units;
   info->plan_bytes = need;
-  info->workspace_bytes = kAlign + 2 * n_chunks * RP * 4;
+  info->workspace_bytes = kAlign + 2 * n_chunks * RP * int64_t(batch) * 4;
   return QTEA_OK;
 }
 
@@ -862,6 +818,15 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   const uint8_t* pl = static_cast<const uint8_t*>(plan);
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
+  if (info->batch > 1) {
+    if (info->rows_per_panel != grouped_mma_rows_per_panel()) return QTEA_ERR_INVALID_ARG;
+    e = launch_grouped_mma(pl, info->grid, info->batch, part, st);
+    if (e == hipSuccess && info->n_split_panels > 0) {
+      hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, pl, part);
+      e = hipGetLastError();
+    }
+    return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+  }
   switch (info->rows_per_panel) {
     case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, info->n_split_panels, part, counters, st); break;
     case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, info->n_split_panels, part, counters, st); break;

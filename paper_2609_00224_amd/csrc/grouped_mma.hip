@@ -1,0 +1,423 @@
+// Grouped low-batch GEMM on the matrix cores: Y_m = X_m W_m^T for 2 <= B <=
+// 16 activation rows per problem (Eq. 10 with one group and zero bias, plus
+// the Eq. 11 residual), every problem of a plan in one persistent launch.
+//
+// At batch B the product is a dense contraction of the ternary weights with
+// a B-column activation block, so it runs on v_mfma_f32_16x16x32_f16 with
+// fp32 accumulation:
+//
+//   A (16 output rows x 32 columns): the ternary codes themselves as fp16
+//     -1 / 0 / +1 (exact), decoded from the packed bytes by one table lookup
+//     per byte in LDS;
+//   B (32 columns x 16): a_j = v_j x[b][j] (exact in fp32: 11-bit by 11-bit
+//     significands) split into two fp16 halves hi = fp16(a), lo = fp16(a -
+//     hi), so hi + lo reproduces a (to 2^-25 absolute for |a| < 1/8, exactly
+//     above); with B <= 8 the 16 columns hold hi of every batch row and lo of
+//     every batch row, with B <= 16 hi and lo are two MFMAs (NB = 2);
+//   y[b][r] = alpha_r (C[r][hi b] + C[r][lo b]) + residual.
+//
+// A slice whose |a| reaches the fp16 range is scaled by 2^-16 before the
+// split (and its products by 2^16 after): rare, handled on a slow path.
+//
+// Work unit = (problem, panel of 1024 rows, K slice of 4 sixteen-pack groups
+// = 320 columns), the same units and plan as the batch-1 kernel; here one
+// 1024-thread workgroup per CU takes one contiguous run of units.  Per unit:
+//
+//   - each wave owns one 64-row tile of the panel: four MFMA row tiles, tile
+//     q holding rows 16m + 4q + s (m, s < 4), whose bytes are rotated by the
+//     same 4q + s (byte i of row r is pack (i + r) mod 16 of its group): the
+//     4q part is undone by register choice, the s part by one v_perm per
+//     dword;
+//   - lane (row i, k-block kb) decodes its row's 16-byte group unit (16 packs
+//     of group kb of the slice): per byte one v_perm forms the LDS address of
+//     that code's entry (16 copies of the 243-entry table, one per lane of a
+//     quarter-wave, so a quarter's reads hit distinct banks), one 8-byte read
+//     gives digits 0-3 as two fp16 pairs (the A operand pairs as they are)
+//     and one 2-byte read gives digit 4;
+//   - ten MFMAs per row tile and column block: eight take digits 0-3 of two
+//     packs each, two take digit 4 of eight packs each; the B operands are
+//     per slice images in LDS in exactly the MFMA lane order, built one unit
+//     ahead from x and v;
+//   - at the end of a panel part: scale by alpha, add the residual of the
+//     part's salient columns with one more MFMA per 32 of them (A = the 1:4
+//     residual expanded per row, B = x at the salient columns), add hi and
+//     lo, and store y (or the part's partial rows, summed afterwards by
+//     grouped_reduce_kernel in run order).
+#include "grouped_plan.h"
+
+namespace qtea_grouped {
+namespace {
+
+constexpr int kMT = 1024;                 // threads per workgroup (one per CU)
+constexpr int kMW = kMT / 64;             // waves: one 64-row tile each
+constexpr int kMRP = kMW * 64;            // rows per panel
+constexpr int kMu = 10;                   // MFMAs per group unit and column block
+constexpr int kRowStride = 256;           // bytes per code in the decode table
+constexpr int kTab = kCodes * kRowStride; // 62,208 bytes
+constexpr int kT4Off = 128;               // digit-4 entries within a code's row
+constexpr int kImg = kMu * 64 * 16;       // one B-operand image (10 MFMAs x 64 lanes x 16 bytes)
+constexpr float kBigScale = 1.0f / 65536.0f;
+
+template <int NB>
+struct MLds {
+  static constexpr int IMG = kTab;                    // [2 buffers][NB] images
+  static constexpr int FLAG = IMG + 2 * NB * kImg;    // int [3]: slice needs scaling
+  static constexpr int BYTES = FLAG + 16;
+};
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+typedef __attribute__((address_space(3))) const _Float16 lds_h;
+
+__device__ __forceinline__ half8 as_half8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  const u32x4 v = {a, b, c, d};
+  return __builtin_bit_cast(half8, v);
+}
+
+// Column (within the slice) of k slot h of MFMA mu for k-block kb: MFMAs 0-7
+// take digits 0-3 of packs 2 mu and 2 mu + 1, MFMAs 8 and 9 digit 4 of packs
+// 0-7 and 8-15 of the group.
+__device__ __forceinline__ void slot_of_col(int c, int& kb, int& mu, int& h) {
+  kb = c / kGroupCols;
+  const int rem = c - kb * kGroupCols;
+  const int pp = rem / 5, d = rem - 5 * pp;
+  if (d < 4) {
+    mu = pp >> 1;
+    h = 4 * (pp & 1) + d;
+  } else {
+    mu = 8 + (pp >> 3);
+    h = pp & 7;
+  }
+}
+
+// fp16 hi / lo split of a (RNE both); hi + lo == a whenever a - hi is
+// representable (|a| >= 1/8), else within 2^-25.
+__device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
+  hi = (_Float16)a;
+  lo = (_Float16)(a - (float)hi);
+}
+
+template <int NB>
+__global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
+                                                          float* __restrict__ part) {
+  using L = MLds<NB>;
+  constexpr int BP = 8 * NB;  // batch rows per hi (or lo) column set
+  extern __shared__ float smem[];
+  char* lds = reinterpret_cast<char*>(smem);
+  int* bigf = reinterpret_cast<int*>(lds + L::FLAG);
+
+  const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
+  const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
+  const GChunk* CR = reinterpret_cast<const GChunk*>(plan + H->off_chunks);
+  const int g = blockIdx.x, NC = H->n_chunks, B = H->batch;
+  if (g >= NC) return;
+  const GChunk rc = CR[g];
+  const int ub = rc.ub, ue = rc.ue;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int jr = lane & 15, kb = lane >> 4;  // MFMA A row / B column, and k-block
+  const int rs = jr & 3;                     // byte rotation left after the tile's 4q
+
+  // decode table: code c at c * 256; digits 0-3 as fp16 at +8 copy, digit 4
+  // at +128 + 8 copy, copy = 0..15 (the lane's index in its quarter-wave)
+  for (int e = tid; e < kCodes * 16; e += kMT) {
+    const int c = e >> 4, cp = e & 15;
+    int d0 = c % 3, r1 = c / 3, d1 = r1 % 3, r2 = r1 / 3, d2 = r2 % 3, r3 = r2 / 3, d3 = r3 % 3, d4 = r3 / 3;
+    _Float16 t[4] = {(_Float16)(d0 - 1), (_Float16)(d1 - 1), (_Float16)(d2 - 1), (_Float16)(d3 - 1)};
+    u32x2 m;
+    __builtin_memcpy(&m, t, 8);
+    *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = m;
+    const _Float16 t4[4] = {(_Float16)(d4 - 1), (_Float16)0, (_Float16)0, (_Float16)0};
+    __builtin_memcpy(&m, t4, 8);
+    *reinterpret_cast<u32x2*>(lds + c * kRowStride + kT4Off + 8 * cp) = m;
+  }
+  if (tid < 3) bigf[tid] = 0;
+  __syncthreads();  // flags cleared before the first images can set one
+
+  // per-lane constants: table copy offset (byte 0 of lane_base), unrotation selector
+  const uint32_t lane_base = uint32_t(8 * jr);
+  const uint32_t sel_rot = 0x07060504u - 0x01010101u * uint32_t(rs);
+
+  Cursor cur{rc.m, rc.panel, rc.slice};
+
+  // x and v of the image this thread builds: pairs p = tid + kMT i of (batch
+  // row b = p / 320, slice column c = p % 320)
+  constexpr int NPAIR = (kSliceCols * BP + kMT - 1) / kMT;
+  uint16_t xr[NPAIR], vr[NPAIR];
+  auto load_xv = [&](const Cursor cc) {
+    const GProblem& pr = P[cc.m];
+    const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
+#pragma unroll
+    for (int i = 0; i < NPAIR; ++i) {
+      const int p = tid + kMT * i;
+      const int b = min(p / kSliceCols, B - 1), c = p % kSliceCols;
+      const uint32_t col = uint32_t(cc.slice * kSliceCols + c);
+      xr[i] = gptr(pr.x)[uint32_t(b) * kx + (col < kx ? col : kx - 1)];
+      vr[i] = gptr(pr.v)[col < kv ? col : kv - 1];
+    }
+  };
+  // build the B-operand images of slice cc into buffer bb (scale: 1 or 2^-16);
+  // returns whether any |a| of the slice is beyond the fp16 range at scale 1
+  auto build = [&](const Cursor cc, int bb, float scale) -> bool {
+    const GProblem& pr = P[cc.m];
+    char* img = lds + L::IMG + bb * NB * kImg;
+    bool big = false;
+#pragma unroll
+    for (int i = 0; i < NPAIR; ++i) {
+      const int p = tid + kMT * i;
+      if (p < kSliceCols * BP) {
+        const int b = p / kSliceCols, c = p - b * kSliceCols;
+        const int col = cc.slice * kSliceCols + c;
+        const float xf = (b < B && col < pr.K) ? float(__builtin_bit_cast(_Float16, xr[i])) : 0.0f;
+        const float vf = col < pr.n_groups * kGroupCols ? float(__builtin_bit_cast(_Float16, vr[i])) : 0.0f;
+        const float a = vf * xf;
+        big |= !(__builtin_fabsf(a) < 65504.0f);
+        _Float16 hi, lo;
+        split_hl(a * scale, hi, lo);
+        int qb, mu, h;
+        slot_of_col(c, qb, mu, h);
+        if (NB == 1) {
+          *reinterpret_cast<_Float16*>(img + ((mu * 64 + b + 16 * qb) * 8 + h) * 2) = hi;
+          *reinterpret_cast<_Float16*>(img + ((mu * 64 + b + 8 + 16 * qb) * 8 + h) * 2) = lo;
+        } else {
+          *reinterpret_cast<_Float16*>(img + ((mu * 64 + b + 16 * qb) * 8 + h) * 2) = hi;
+          *reinterpret_cast<_Float16*>(img + kImg + ((mu * 64 + b + 16 * qb) * 8 + h) * 2) = lo;
+        }
+      }
+    }
+    return big;
+  };
+
+  // weight bytes of unit cc, MFMA row tile q: row 16 (jr >> 2) + 4q + (jr & 3)
+  // of the wave's 64-row tile, group kb of the slice
+  auto w_off = [&](const Cursor cc, int q) -> uint32_t {
+    const GProblem& pr = P[cc.m];
+    const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
+    const int grp = min(cc.slice * kSliceGroups + kb, ng - 1);
+    const int tl = min(cc.panel * (kMRP / 64) + w, n_tiles - 1);
+    const int row = 16 * (jr >> 2) + 4 * q + (jr & 3);
+    return (uint32_t(tl * ng + grp) * kTileRows + uint32_t(row)) * kGroupPacks;
+  };
+
+  u32x4 W[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    W[q] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, q)));
+  load_xv(cur);
+  const bool big0 = build(cur, 0, 1.0f);
+  if (big0) bigf[0] = 1;
+  __syncthreads();
+
+  f32x4 C[4][NB];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) C[q][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  int pstart_slice = cur.slice;
+  bool part_first = true;  // the open panel part began at the run's first unit
+
+  for (int it = 0, u = ub; u < ue; ++it, ++u) {
+    const GProblem& pr = P[cur.m];
+    const bool has_next = u + 1 < ue;
+    const Cursor nxt = has_next ? advance(cur, P) : cur;
+    const bool pstart = (cur.slice == 0) || (u == ub);
+    const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
+    if (pstart) {
+      pstart_slice = cur.slice;
+      part_first = u == ub;
+    }
+    const int sb = it & 1;
+    const bool big = __builtin_amdgcn_readfirstlane(bigf[it % 3]) != 0;
+    if (tid == 0) bigf[(it + 2) % 3] = 0;  // flag of the unit after next
+    if (big) {
+      // rare: this slice's |a| reaches the fp16 range; rebuild its images
+      // at 2^-16 and scale the running sums around its products
+      load_xv(cur);
+      build(cur, sb, kBigScale);
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) C[q][nb] *= kBigScale;
+    }
+    load_xv(nxt);
+
+    // next unit's weight bytes through a buffer resource over its matrix
+    const GProblem& pn = P[nxt.m];
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(pn.trits), 0,
+        int(uint32_t(pn.n_pad >> 6) * uint32_t(pn.n_groups) * (kTileRows * kGroupPacks)), kBufferWord3);
+
+    const char* img = lds + L::IMG + sb * NB * kImg;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      half8 Bv[5][NB];
+#pragma unroll
+      for (int i = 0; i < 5; ++i) {
+        const int mu = i < 4 ? 4 * half + i : 8 + half;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          Bv[i][nb] = __builtin_bit_cast(half8, *(lds_u32x4*)(size_t(img + nb * kImg + (mu * 64 + lane) * 16)));
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // packs 8 half .. 8 half + 7 of this lane's row, unrotated
+        const uint32_t U0 = __builtin_amdgcn_perm(W[q][(2 * half - q) & 3], W[q][(2 * half - q - 1) & 3], sel_rot);
+        const uint32_t U1 = __builtin_amdgcn_perm(W[q][(2 * half + 1 - q) & 3], W[q][(2 * half - q) & 3], sel_rot);
+        uint32_t ad[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t sel = 0x0C0C0004u | (uint32_t(k) << 8);
+          ad[k] = __builtin_amdgcn_perm(lane_base, U0, sel);
+          ad[4 + k] = __builtin_amdgcn_perm(lane_base, U1, sel);
+        }
+        u32x2 d03[8];
+        _Float16 d4[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          d03[k] = *(lds_u32x2*)(size_t(ad[k]));
+          d4[k] = *(lds_h*)(size_t(ad[k] + kT4Off));
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const half8 A = as_half8(d03[2 * i].x, d03[2 * i].y, d03[2 * i + 1].x, d03[2 * i + 1].y);
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) C[q][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, Bv[i][nb], C[q][nb], 0, 0, 0);
+        }
+        const half8 A4 = {d4[0], d4[1], d4[2], d4[3], d4[4], d4[5], d4[6], d4[7]};
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) C[q][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A4, Bv[4][nb], C[q][nb], 0, 0, 0);
+        if (half == 1) {
+          // refill after the last use of the old bytes (the last unit of the
+          // run reloads its own first bytes: harmless)
+          const uint32_t off = has_next ? w_off(nxt, q) : 0u;
+          W[q] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, int(off), 0, kAuxNT));
+        }
+      }
+    }
+    if (big) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) C[q][nb] *= 65536.0f;
+    }
+
+    // the next unit's images into the other buffer
+    if (has_next) {
+      if (build(nxt, sb ^ 1, 1.0f)) bigf[(it + 1) % 3] = 1;
+    }
+
+    if (pend) {
+      // 1. alpha of the lane's four rows (slot v of tile q is row 16 kb + 4q + v)
+      const int tl = cur.panel * (kMRP / 64) + w;
+      const int n_tiles = int(pr.n_pad >> 6);
+      const int tlc = min(tl, n_tiles - 1);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r0 = tlc * 64 + 16 * kb + 4 * q;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float al = float(__builtin_bit_cast(_Float16, gptr(pr.alpha)[r0 + v]));
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) C[q][nb][v] *= al;
+        }
+      }
+      // 2. residual of the part's salient columns: one MFMA per 32 of them
+      const int g0 = pstart_slice * kSliceGroups;
+      const int g1 = min((cur.slice + 1) * kSliceGroups, pr.n_groups);
+      const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
+      for (int s0 = s_lo; s0 < s_hi; s0 += 32) {
+        // B: x[j][S_s] in the hi columns (j < min(B, BP)), zero elsewhere
+        _Float16 bx[8];
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const int s = s0 + 8 * kb + h;
+          const int sc = min(s, s_hi - 1);
+          const int col = gptr(pr.S)[sc];
+          const _Float16 xv = __builtin_bit_cast(_Float16, gptr(pr.x)[uint32_t(min(jr, B - 1)) * uint32_t(pr.K) + uint32_t(col)]);
+          bx[h] = (s < s_hi && jr < B && jr < BP) ? xv : (_Float16)0;
+        }
+        const half8 Bx = {bx[0], bx[1], bx[2], bx[3], bx[4], bx[5], bx[6], bx[7]};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // A: row i = jr of tile q is row 16 (jr >> 2) + 4q + (jr & 3): four-row
+          // group 4 (jr >> 2) + q of the 64-row tile, position jr & 3
+          const int gg = 4 * (jr >> 2) + q;
+          _Float16 ar[8];
+#pragma unroll
+          for (int h = 0; h < 8; ++h) {
+            const int s = s0 + 8 * kb + h;
+            const int sc = min(s, s_hi - 1);
+            const int64_t ti = int64_t(tlc) * pr.nS + sc;
+            const _Float16 rv = __builtin_bit_cast(_Float16, gptr(pr.rval)[ti * 16 + gg]);
+            const uint32_t pos = (gptr(pr.ridx)[ti] >> (2 * gg)) & 3u;
+            ar[h] = (s < s_hi && pos == uint32_t(jr & 3)) ? rv : (_Float16)0;
+          }
+          const half8 Ar = {ar[0], ar[1], ar[2], ar[3], ar[4], ar[5], ar[6], ar[7]};
+          C[q][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ar, Bx, C[q][0], 0, 0, 0);
+        }
+      }
+      // 3. hi + lo, and the store: lane jr < B holds rows 16 kb + 4q + v of batch row jr
+      const int64_t row0 = int64_t(cur.panel) * kMRP + int64_t(w) * 64;
+      const bool owned = pstart_slice == 0 && cur.slice == pr.n_slices - 1;
+      float* dst = owned ? nullptr : part + (2 * int64_t(g) + (part_first ? 0 : 1)) * int64_t(kMRP) * B;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f32x4 yv;
+        if (NB == 1) {
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const float lo = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(
+                __builtin_bit_cast(int, C[q][0][v]), 0x128, 0xf, 0xf, false));  // row_ror:8
+            yv[v] = C[q][0][v] + lo;
+          }
+        } else {
+          yv = C[q][0] + C[q][NB - 1];
+        }
+        const int rl = 16 * kb + 4 * q;  // row within the wave's tile
+        if (jr < B) {
+          if (owned) {
+            if (row0 + rl < pr.N) {  // N % 4 == 0: the four rows are all in or all out
+              gf32* yp = (gf32*)(pr.y + int64_t(jr) * pr.N + row0 + rl);
+#pragma unroll
+              for (int v = 0; v < 4; ++v) yp[v] = yv[v];
+            }
+          } else {
+            *reinterpret_cast<f32x4*>(dst + int64_t(jr) * kMRP + w * 64 + rl) = yv;
+          }
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) C[q][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+    }
+    __syncthreads();  // the next unit's images are complete; this unit's are free
+    cur = nxt;
+  }
+}
+
+template <int NB>
+hipError_t launch(const uint8_t* plan, int grid, float* part, hipStream_t st) {
+  static bool done = false;
+  if (!done) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_mma_kernel<NB>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, MLds<NB>::BYTES);
+    if (e != hipSuccess) return e;
+    done = true;
+  }
+  hipLaunchKernelGGL(grouped_mma_kernel<NB>, dim3(grid), dim3(kMT), MLds<NB>::BYTES, st, plan, part);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int grouped_mma_rows_per_panel() { return kMRP; }
+
+hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, float* part, hipStream_t st) {
+  return batch <= 8 ? launch<1>(plan, grid, part, st) : launch<2>(plan, grid, part, st);
+}
+
+}  // namespace qtea_grouped

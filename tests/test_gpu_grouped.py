@@ -187,9 +187,10 @@ def test_grouped_errors():
     x = to_dev(c["x"])
     y = torch.empty((1, 256), dtype=torch.float32, device="cuda")
     plan = torch.empty(q.qtea_grouped_plan_bytes(1), dtype=torch.uint8, device="cuda")
-    with pytest.raises(q.QteaError) as e:
-        q.qtea_grouped_plan([m.desc], [m.packed], [x], [y], 2, plan)
-    assert e.value.status == q.QTEA_ERR_BATCH
+    for bad in (0, 17):
+        with pytest.raises(q.QteaError) as e:
+            q.qtea_grouped_plan([m.desc], [m.packed], [x], [y], bad, plan)
+        assert e.value.status == q.QTEA_ERR_BATCH
     with pytest.raises(q.QteaError) as e:
         q.qtea_grouped_plan([m.desc], [m.packed], [x], [y], 1, plan[:16])
     assert e.value.status == q.QTEA_ERR_WORKSPACE
