@@ -229,6 +229,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--chained-only", action="store_true", help="time only the per-GEMV launches")
+    ap.add_argument("--grouped-only", action="store_true",
+                    help="skip the per-GEMV launches (profiling the grouped kernel)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="after the bench, copy this many bytes device-to-device 3 times "
                          "(known-size reference for HBM counters)")
@@ -257,12 +259,14 @@ def main():
     stream = torch.cuda.Stream(device=dev)
 
     token_bytes = sum(m["bytes"] for m in mats)
-    g = capture(mats, B, ws, stream)
-    ms_chain = time_graph(g, stream, args.steps, args.warmup)
+    ms_chain = float("nan")
+    if not args.grouped_only:
+        g = capture(mats, B, ws, stream)
+        ms_chain = time_graph(g, stream, args.steps, args.warmup)
+        del g
     gbs_chain = token_bytes / (ms_chain * 1e-3) / 1e9
     log(f"{wl.name} B={B} chained: {ms_chain * 1e3:.1f} us/token, {gbs_chain:.1f} GB/s "
         f"({gbs_chain / HBM_PEAK_GBS:.1%} of peak)")
-    del g
 
     grouped = not args.chained_only
     if grouped:
@@ -278,7 +282,7 @@ def main():
 
     # Per-role timing: a graph of one role's launches over all layers.
     roles = {}
-    if not args.no_kernel_timing:
+    if not args.no_kernel_timing and not args.grouped_only:
         for mat, (role, N, K) in enumerate(wl.shapes):
             sub = [m for m in mats if m["mat"] == mat]
             gr = capture(sub, B, ws, stream)
@@ -305,7 +309,7 @@ def main():
     chained = {"us_per_token": round(ms_chain * 1e3, 2), "value": round(gbs_chain, 2), "unit": "GB/s",
                "frac_hbm_peak": round(gbs_chain / HBM_PEAK_GBS, 4), "kernel": kernel_name(B),
                "launches_per_step": len(mats), "us_per_launch": round(ms_chain * 1e3 / len(mats), 3),
-               "per_role": roles}
+               "per_role": roles} if not args.grouped_only else None
 
     if grouped:  # leave the grouped outputs in y for the oracle comparison
         with torch.cuda.stream(stream):

@@ -30,10 +30,11 @@
 //     dword;
 //   - lane (row i, k-block kb) decodes its row's 16-byte group unit (16 packs
 //     of group kb of the slice): per byte one v_perm forms the LDS address of
-//     that code's entry (16 copies of the 243-entry table, one per lane of a
-//     quarter-wave, so a quarter's reads hit distinct banks), one 8-byte read
-//     gives digits 0-3 as two fp16 pairs (the A operand pairs as they are)
-//     and one 2-byte read gives digit 4;
+//     that code's entry (32 copies of the 243-entry table, one per lane of a
+//     half-wave, so a half-wave's reads hit distinct banks), one 8-byte read
+//     gives digits 0-3 as two fp16 pairs (the A operand pairs as they are),
+//     and a 2-byte read from a 32-copy digit-4 table at half that address
+//     gives digit 4 straight into its half of the operand register;
 //   - ten MFMAs per row tile and column block: eight take digits 0-3 of two
 //     packs each, two take digit 4 of eight packs each; the B operands are
 //     per slice images in LDS in exactly the MFMA lane order, built one unit
@@ -52,15 +53,25 @@ constexpr int kMT = 1024;                 // threads per workgroup (one per CU)
 constexpr int kMW = kMT / 64;             // waves: one 64-row tile each
 constexpr int kMRP = kMW * 64;            // rows per panel
 constexpr int kMu = 10;                   // MFMAs per group unit and column block
-constexpr int kRowStride = 256;           // bytes per code in the decode table
+constexpr int kRowStride = 256;           // bytes per code in the digit 0-3 table (32 copies x 8)
 constexpr int kTab = kCodes * kRowStride; // 62,208 bytes
-constexpr int kT4Off = 128;               // digit-4 entries within a code's row
+// Digit-4 table, either mirrored (code c, copy k at kTab + c * 256 + 8 k: the
+// digit 0-3 entry's address plus a constant) or compact (kTab + c * 128 +
+// 4 k: half that address plus a constant, one shift more per byte, half the
+// space); the mirror leaves no room for two column blocks' images.
+template <int NB>
+struct T4 {
+  static constexpr bool kMirror = NB == 1;
+  static constexpr int kBytes = kMirror ? kCodes * 256 : kCodes * 128;
+  static constexpr int kStride = kMirror ? 8 : 4;  // bytes per copy
+};
 constexpr int kImg = kMu * 64 * 16;       // one B-operand image (10 MFMAs x 64 lanes x 16 bytes)
 constexpr float kBigScale = 1.0f / 65536.0f;
 
 template <int NB>
 struct MLds {
-  static constexpr int IMG = kTab;                    // [2 buffers][NB] images
+  static constexpr int T4OFF = kTab;
+  static constexpr int IMG = kTab + T4<NB>::kBytes;  // [2 buffers][NB] images
   static constexpr int FLAG = IMG + 2 * NB * kImg;    // int [3]: slice needs scaling
   static constexpr int BYTES = FLAG + 16;
 };
@@ -71,6 +82,15 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) const _Float16 lds_h;
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+// Two table halves into one dword (the second into the high half).
+__device__ __forceinline__ uint32_t lds_pair(uint32_t a0, uint32_t a1) {
+  half2_t r;
+  r.x = *(lds_h*)(size_t(a0));
+  r.y = *(lds_h*)(size_t(a1));
+  return __builtin_bit_cast(uint32_t, r);
+}
 
 __device__ __forceinline__ half8 as_half8(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
   const u32x4 v = {a, b, c, d};
@@ -91,6 +111,11 @@ __device__ __forceinline__ void slot_of_col(int c, int& kb, int& mu, int& h) {
     mu = 8 + (pp >> 3);
     h = pp & 7;
   }
+}
+
+// The value of lane (l + 8) mod 16 of the lane's row of 16 (row_ror:8).
+__device__ __forceinline__ float dpp_ror8(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x128, 0xf, 0xf, false));
 }
 
 // fp16 hi / lo split of a (RNE both); hi + lo == a whenever a - hi is
@@ -122,71 +147,80 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   const int jr = lane & 15, kb = lane >> 4;  // MFMA A row / B column, and k-block
   const int rs = jr & 3;                     // byte rotation left after the tile's 4q
 
-  // decode table: code c at c * 256; digits 0-3 as fp16 at +8 copy, digit 4
-  // at +128 + 8 copy, copy = 0..15 (the lane's index in its quarter-wave)
-  for (int e = tid; e < kCodes * 16; e += kMT) {
-    const int c = e >> 4, cp = e & 15;
+  // decode tables, copy = the lane's index in its half-wave: digits 0-3 of
+  // code c as fp16 at c * 256 + 8 copy, digit 4 in the T4 table
+  for (int e = tid; e < kCodes * 32; e += kMT) {
+    const int c = e >> 5, cp = e & 31;
     int d0 = c % 3, r1 = c / 3, d1 = r1 % 3, r2 = r1 / 3, d2 = r2 % 3, r3 = r2 / 3, d3 = r3 % 3, d4 = r3 / 3;
     _Float16 t[4] = {(_Float16)(d0 - 1), (_Float16)(d1 - 1), (_Float16)(d2 - 1), (_Float16)(d3 - 1)};
     u32x2 m;
     __builtin_memcpy(&m, t, 8);
     *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = m;
-    const _Float16 t4[4] = {(_Float16)(d4 - 1), (_Float16)0, (_Float16)0, (_Float16)0};
-    __builtin_memcpy(&m, t4, 8);
-    *reinterpret_cast<u32x2*>(lds + c * kRowStride + kT4Off + 8 * cp) = m;
+    const _Float16 t4[2] = {(_Float16)(d4 - 1), (_Float16)0};
+    uint32_t m4;
+    __builtin_memcpy(&m4, t4, 4);
+    *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * (32 * T4<NB>::kStride) + T4<NB>::kStride * cp) = m4;
   }
   if (tid < 3) bigf[tid] = 0;
   __syncthreads();  // flags cleared before the first images can set one
 
   // per-lane constants: table copy offset (byte 0 of lane_base), unrotation selector
-  const uint32_t lane_base = uint32_t(8 * jr);
+  const uint32_t lane_base = uint32_t(8 * (lane & 31));
   const uint32_t sel_rot = 0x07060504u - 0x01010101u * uint32_t(rs);
 
   Cursor cur{rc.m, rc.panel, rc.slice};
 
   // x and v of the image this thread builds: pairs p = tid + kMT i of (batch
-  // row b = p / 320, slice column c = p % 320)
+  // row b = p / 320, slice column c = p % 320); their image byte offsets (hi
+  // and lo halves) are fixed per thread
   constexpr int NPAIR = (kSliceCols * BP + kMT - 1) / kMT;
+  uint32_t img_hi[NPAIR], img_lo[NPAIR];
+  int pb[NPAIR], pc[NPAIR];
+#pragma unroll
+  for (int i = 0; i < NPAIR; ++i) {
+    const int p = tid + kMT * i;
+    pb[i] = p / kSliceCols;
+    pc[i] = p - pb[i] * kSliceCols;
+    int qb, mu, h;
+    slot_of_col(pc[i], qb, mu, h);
+    const int bb = pb[i] < BP ? pb[i] : 0;  // pairs past the image are not built
+    img_hi[i] = uint32_t(((mu * 64 + bb + 16 * qb) * 8 + h) * 2);
+    img_lo[i] = NB == 1 ? uint32_t(((mu * 64 + bb + 8 + 16 * qb) * 8 + h) * 2) : img_hi[i] + uint32_t(kImg);
+  }
+  // loads through buffer resources over x [B][K] and v [n_groups * 80]:
+  // reads past either return zero, which is the padding the images need
   uint16_t xr[NPAIR], vr[NPAIR];
   auto load_xv = [&](const Cursor cc) {
     const GProblem& pr = P[cc.m];
-    const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(pr.x), 0, int(2 * uint32_t(B) * uint32_t(pr.K)), kBufferWord3);
+    const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(pr.v), 0, int(2 * uint32_t(pr.n_groups) * kGroupCols), kBufferWord3);
+    const int col0 = cc.slice * kSliceCols;
 #pragma unroll
     for (int i = 0; i < NPAIR; ++i) {
-      const int p = tid + kMT * i;
-      const int b = min(p / kSliceCols, B - 1), c = p % kSliceCols;
-      const uint32_t col = uint32_t(cc.slice * kSliceCols + c);
-      xr[i] = gptr(pr.x)[uint32_t(b) * kx + (col < kx ? col : kx - 1)];
-      vr[i] = gptr(pr.v)[col < kv ? col : kv - 1];
+      const int col = col0 + pc[i];
+      // a column past K would read the next batch row: send it past the buffer instead
+      const uint32_t xo = (pb[i] < B && col < pr.K) ? uint32_t(2 * (pb[i] * pr.K + col)) : 0x7ffffff0u;
+      xr[i] = __builtin_amdgcn_raw_buffer_load_b16(xres, int(xo), 0, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b16(vres, 2 * col, 0, 0);
     }
   };
   // build the B-operand images of slice cc into buffer bb (scale: 1 or 2^-16);
   // returns whether any |a| of the slice is beyond the fp16 range at scale 1
   auto build = [&](const Cursor cc, int bb, float scale) -> bool {
-    const GProblem& pr = P[cc.m];
+    (void)cc;
     char* img = lds + L::IMG + bb * NB * kImg;
     bool big = false;
 #pragma unroll
     for (int i = 0; i < NPAIR; ++i) {
-      const int p = tid + kMT * i;
-      if (p < kSliceCols * BP) {
-        const int b = p / kSliceCols, c = p - b * kSliceCols;
-        const int col = cc.slice * kSliceCols + c;
-        const float xf = (b < B && col < pr.K) ? float(__builtin_bit_cast(_Float16, xr[i])) : 0.0f;
-        const float vf = col < pr.n_groups * kGroupCols ? float(__builtin_bit_cast(_Float16, vr[i])) : 0.0f;
-        const float a = vf * xf;
+      if (tid + kMT * i < kSliceCols * BP) {
+        const float a = float(__builtin_bit_cast(_Float16, vr[i])) * float(__builtin_bit_cast(_Float16, xr[i]));
         big |= !(__builtin_fabsf(a) < 65504.0f);
         _Float16 hi, lo;
         split_hl(a * scale, hi, lo);
-        int qb, mu, h;
-        slot_of_col(c, qb, mu, h);
-        if (NB == 1) {
-          *reinterpret_cast<_Float16*>(img + ((mu * 64 + b + 16 * qb) * 8 + h) * 2) = hi;
-          *reinterpret_cast<_Float16*>(img + ((mu * 64 + b + 8 + 16 * qb) * 8 + h) * 2) = lo;
-        } else {
-          *reinterpret_cast<_Float16*>(img + ((mu * 64 + b + 16 * qb) * 8 + h) * 2) = hi;
-          *reinterpret_cast<_Float16*>(img + kImg + ((mu * 64 + b + 16 * qb) * 8 + h) * 2) = lo;
-        }
+        *reinterpret_cast<_Float16*>(img + img_hi[i]) = hi;
+        *reinterpret_cast<_Float16*>(img + img_lo[i]) = lo;
       }
     }
     return big;
@@ -276,11 +310,15 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
           ad[4 + k] = __builtin_amdgcn_perm(lane_base, U1, sel);
         }
         u32x2 d03[8];
-        _Float16 d4[8];
+        uint32_t d4[4];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          d03[k] = *(lds_u32x2*)(size_t(ad[k]));
-          d4[k] = *(lds_h*)(size_t(ad[k] + kT4Off));
+        for (int k = 0; k < 8; ++k) d03[k] = *(lds_u32x2*)(size_t(ad[k]));
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if constexpr (T4<NB>::kMirror)
+            d4[k] = lds_pair(ad[2 * k] + L::T4OFF, ad[2 * k + 1] + L::T4OFF);
+          else
+            d4[k] = lds_pair((ad[2 * k] >> 1) + L::T4OFF, (ad[2 * k + 1] >> 1) + L::T4OFF);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -288,7 +326,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) C[q][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, Bv[i][nb], C[q][nb], 0, 0, 0);
         }
-        const half8 A4 = {d4[0], d4[1], d4[2], d4[3], d4[4], d4[5], d4[6], d4[7]};
+        const half8 A4 = as_half8(d4[0], d4[1], d4[2], d4[3]);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) C[q][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A4, Bv[4][nb], C[q][nb], 0, 0, 0);
         if (half == 1) {
@@ -371,9 +409,10 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
         if (NB == 1) {
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            const float lo = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(
-                __builtin_bit_cast(int, C[q][0][v]), 0x128, 0xf, 0xf, false));  // row_ror:8
-            yv[v] = C[q][0][v] + lo;
+            // the element goes through a scalar first: a bit cast of a vector
+            // element reads element 0 whatever the index (frontend bug)
+            const float cv = C[q][0][v];
+            yv[v] = cv + dpp_ror8(cv);
           }
         } else {
           yv = C[q][0] + C[q][NB - 1];

@@ -35,6 +35,26 @@ def dyadic_case(seed, N, K, B, nS):
     }
 
 
+def fine_case(seed, N, K, B):
+    """Exact inputs whose a_j = v_j x_j need both fp16 halves of the
+    low-batch kernel's activation split: x = k / 1024 (|k| < 2048, 11 bits),
+    v in {1, 1.25, 1.5, 1.75}, alpha = 1, no salient columns.  Every product
+    is a multiple of 2^-12 below 4 in magnitude, so for K <= 1000 every
+    partial sum is exact in fp32 and the GPU result equals the oracle's."""
+    assert K <= 1000
+    rng = np.random.default_rng(seed)
+    return {
+        "N": N, "K": K,
+        "trits": rng.integers(-1, 2, size=(N, K)).astype(np.int8),
+        "alpha": np.ones(N, np.float16),
+        "v": rng.choice([1.0, 1.25, 1.5, 1.75], size=K).astype(np.float16),
+        "S": np.zeros(0, np.int32),
+        "R": np.zeros((0, N // 4), np.float16),
+        "idx": np.zeros((0, N // 4), np.uint8),
+        "x": (rng.integers(-2047, 2048, size=(B, K)) / 1024.0).astype(np.float16),
+    }
+
+
 def synth_case(seed, N, K, B, p0=Fraction(2, 5), frac=Fraction(2, 100), layer=0, mat=0, nS=None):
     L = synth.layer_inputs(seed, layer, mat, N, K, p0=p0, frac=frac)
     if nS is not None:  # override the salient count (edge cases)
@@ -111,6 +131,22 @@ def oracle_rows(case, rows=None, codes=None, need_wmax=True, block=512):
         W = oracle.dense_rows(N, K, codes[sl], *args[3:], rows=rows[sl])
         wmax[sl] = np.abs(W).max(axis=1)
     return y, wmax
+
+
+# The kernels' own precision on synthetic inputs (fp32 sums of ~1e4 terms,
+# and the fp16 activation halves of the low-batch kernel) is about 1e-7
+# relative; this bar, far tighter than the acceptance bound, catches a lost
+# term or half that the acceptance bound would let through.
+REL_L2_PRECISE = 1e-5
+
+
+def assert_precise(y_gpu, y_ref, what=""):
+    y_gpu = np.asarray(y_gpu, dtype=np.float64)
+    for b in range(y_ref.shape[0]):
+        nrm = np.linalg.norm(y_ref[b])
+        if nrm > 0:
+            rel = np.linalg.norm(y_gpu[b] - y_ref[b]) / nrm
+            assert rel <= REL_L2_PRECISE, f"{what}: batch {b} relative L2 error {rel:.3e} above {REL_L2_PRECISE}"
 
 
 def assert_close(y_gpu, y_ref, x, wmax, what=""):

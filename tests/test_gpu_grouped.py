@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 from synth.workloads import WORKLOADS
-from tests.gpu_cases import assert_close, dyadic_case, gpu_pack, oracle_rows, synth_case, to_dev
+from tests.gpu_cases import assert_close, assert_precise, dyadic_case, gpu_pack, oracle_rows, synth_case, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -107,6 +107,7 @@ def test_grouped_synth_8b_layer():
     for c, y in zip(cases, outs):
         ref, wmax = oracle_rows(c)
         assert_close(y, ref, c["x"], wmax, f"grouped {c['N']}x{c['K']}")
+        assert_precise(y, ref, f"grouped {c['N']}x{c['K']}")
 
 
 def test_grouped_synth_8b_eight_layers():
@@ -117,6 +118,7 @@ def test_grouped_synth_8b_eight_layers():
     for c, y in zip(cases, outs):
         ref, wmax = oracle_rows(c)
         assert_close(y, ref, c["x"], wmax, f"grouped {c['N']}x{c['K']}")
+        assert_precise(y, ref, f"grouped {c['N']}x{c['K']}")
 
 
 def test_grouped_matches_gemv_and_is_deterministic():
@@ -140,6 +142,7 @@ def test_grouped_matches_gemv_and_is_deterministic():
         ref, wmax = oracle_rows(c)
         assert_close(Y.cpu().numpy(), ref, c["x"], wmax, "gemv")
         assert_close(y, ref, c["x"], wmax, "grouped")
+        assert_precise(y, ref, "grouped")
 
 
 def test_grouped_graph_replay():

@@ -15,7 +15,8 @@ import numpy as np
 import pytest
 
 from synth.workloads import WORKLOADS
-from tests.gpu_cases import assert_close, dyadic_case, gpu_pack, oracle_rows, synth_case, to_dev
+from tests.gpu_cases import (assert_close, assert_precise, dyadic_case, fine_case, gpu_pack, oracle_rows,
+                             synth_case, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -70,6 +71,21 @@ def test_grouped_batch_dyadic_exact(B):
         assert bad.size == 0, f"{c['N']}x{c['K']} B={B}: {len(bad)} outputs differ, first {bad[:4].tolist()}"
 
 
+FINE_GROUP = [(256, 1000), (4160, 640), (1024, 999), (64, 7)]
+
+
+@pytest.mark.parametrize("B", [2, 5, 8, 9, 16])
+def test_grouped_batch_both_halves_exact(B):
+    # a_j needs both fp16 halves (hi and lo): the result is still exact
+    cases = [fine_case(900 + 7 * B + i, N, K, B) for i, (N, K) in enumerate(FINE_GROUP)]
+    _report(f"grouped batch {B}, activations split in two halves, {FINE_GROUP}")
+    (outs,), _ = _run_group(cases, B)
+    for c, y in zip(cases, outs):
+        ref, _ = oracle_rows(c, need_wmax=False)
+        bad = np.argwhere(y.astype(np.float64) != ref)
+        assert bad.size == 0, f"{c['N']}x{c['K']} B={B}: {len(bad)} outputs differ, first {bad[:4].tolist()}"
+
+
 def test_grouped_batch_single_small_problem():
     c = dyadic_case(41, 64, 1, 4, 1)
     _report("grouped batch 4, 64x1")
@@ -98,6 +114,7 @@ def test_grouped_batch_synth_layer(B, name):
     for c, y in zip(cases, outs):
         ref, wmax = oracle_rows(c)
         assert_close(y, ref, c["x"], wmax, f"grouped B={B} {c['N']}x{c['K']}")
+        assert_precise(y, ref, f"grouped B={B} {c['N']}x{c['K']}")
 
 
 def test_grouped_batch_deterministic_and_queue_left_zero():

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.gpu_cases import (assert_close, dyadic_case, gpu_gemm, gpu_pack, gpu_unpack, oracle_rows,
+from tests.gpu_cases import (assert_close, assert_precise, dyadic_case, gpu_gemm, gpu_pack, gpu_unpack, oracle_rows,
                              synth_case, to_dev)
 from tests.golden import load_worked_example
 
@@ -124,6 +124,7 @@ def test_random_within_tolerance(N, K, B, nS):
     y = gpu_gemm(pm, case["x"])
     ref, wmax = oracle_rows(case)
     assert_close(y, ref, case["x"], wmax, f"N={N} K={K} B={B}")
+    assert_precise(y, ref, f"N={N} K={K} B={B}")
 
 
 @pytest.mark.parametrize("B", list(range(1, 17)))
@@ -134,6 +135,7 @@ def test_every_batch_size(B):
     y = gpu_gemm(pm, case["x"])
     ref, wmax = oracle_rows(case)
     assert_close(y, ref, case["x"], wmax, f"B={B}")
+    assert_precise(y, ref, f"B={B}")
 
 
 # ---------------------------------------------------------------------------
@@ -162,6 +164,7 @@ def test_residual_only():
     y = gpu_gemm(gpu_pack(case), case["x"])
     ref, wmax = oracle_rows(case)
     assert_close(y, ref, case["x"], wmax, "residual only")
+    assert_precise(y, ref, "residual only")
     assert np.array_equal(y != 0, ref != 0)
 
 
@@ -194,6 +197,7 @@ def test_workspace_shared_across_matrices():
             y = gpu_gemm(pm, c["x"], ws=ws)
             ref, wmax = oracle_rows(c)
             assert_close(y, ref, c["x"], wmax, f"shared ws rep {rep}")
+            assert_precise(y, ref, f"shared ws rep {rep}")
     n_counters = max(((c["N"] + 63) // 64 + 3) // 4 for c in cases)  # one per 4-tile row block
     counters = ws[: 4 * n_counters].cpu().numpy()
     assert np.all(counters == 0)
