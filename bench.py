@@ -118,6 +118,25 @@ def time_graph(g, stream, reps, warmup):
     return e0.elapsed_time(e1) / reps  # ms per replay
 
 
+def replay_spread(g, stream, reps):
+    """Median, p10 and p90 of single replays, each between its own pair of
+    events (a separate pass after the timed one)."""
+    import numpy as np
+    import torch
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    with torch.cuda.stream(stream):
+        ev[0].record(stream)
+        for i in range(reps):
+            g.replay()
+            ev[i + 1].record(stream)
+    ev[-1].synchronize()
+    us = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(reps)])
+    p10, p50, p90 = np.percentile(us, [10, 50, 90])
+    return {"median": round(float(p50), 2), "p10": round(float(p10), 2), "p90": round(float(p90), 2),
+            "replays": reps}
+
+
 def kernel_name(B, grouped=False, rows_per_panel=1024):
     if grouped and B > 1:
         return f"grouped_mma_kernel<{1 if B <= 8 else 2}>"  # hi/lo activation halves in one or two MFMAs
@@ -273,10 +292,13 @@ def main():
         gp = q.plan_grouped([m["pm"] for m in mats], [m["x"] for m in mats], [m["y"] for m in mats], batch=B)
         gg = capture_grouped(gp, stream)
         ms = time_graph(gg, stream, args.steps, args.warmup)
+        spread = replay_spread(gg, stream, min(args.steps, 200))
         log(f"{wl.name} B={B} grouped: {ms * 1e3:.1f} us/token ({gp.info.n_units} units, "
-            f"{gp.info.rows_per_panel}-row panels, {gp.info.grid} workgroups)")
+            f"{gp.info.rows_per_panel}-row panels, {gp.info.grid} workgroups); single replays "
+            f"median {spread['median']} p10 {spread['p10']} p90 {spread['p90']} us")
     else:
         ms = ms_chain
+        spread = None
     gbs = token_bytes / (ms * 1e-3) / 1e9
     log(f"{wl.name} B={B}: {ms * 1e3:.1f} us/token, {gbs:.1f} GB/s ({gbs / HBM_PEAK_GBS:.1%} of peak)")
 
@@ -337,6 +359,7 @@ def main():
         "config": {"workload": wl.name, "layers": n_layers, "matrices_per_token": len(mats),
                    "batch": B, "weight_bytes_per_token": token_bytes, "seed": seed},
         "us_per_token": round(ms * 1e3, 2),
+        "us_per_token_single_replays": spread,
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "execution": "grouped" if grouped else "chained",
         "chained": chained,
