@@ -80,6 +80,7 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
+typedef __attribute__((address_space(1))) const u32x2 gu32x2;
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) const _Float16 lds_h;
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
@@ -350,52 +351,77 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     }
 
     if (pend) {
-      // 1. alpha of the lane's four rows (slot v of tile q is row 16 kb + 4q + v)
+      // 1. alpha of the lane's rows: slot v of tile q is row 16 kb + 4q + v
+      // of the wave's tile, sixteen consecutive rows per lane
       const int tl = cur.panel * (kMRP / 64) + w;
       const int n_tiles = int(pr.n_pad >> 6);
       const int tlc = min(tl, n_tiles - 1);
+      {
+        gu32x4* ap = reinterpret_cast<gu32x4*>(gptr(pr.alpha) + tlc * 64 + 16 * kb);
+        const u32x4 a01 = ap[0], a23 = ap[1];
+        const uint32_t aw[8] = {a01.x, a01.y, a01.z, a01.w, a23.x, a23.y, a23.z, a23.w};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r0 = tlc * 64 + 16 * kb + 4 * q;
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float al = float(__builtin_bit_cast(_Float16, gptr(pr.alpha)[r0 + v]));
+          for (int v = 0; v < 4; ++v) {
+            const uint32_t wd = aw[2 * q + (v >> 1)];
+            const float al = float(__builtin_bit_cast(_Float16, uint16_t((v & 1) ? wd >> 16 : wd & 0xffffu)));
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) C[q][nb][v] *= al;
-        }
+            for (int nb = 0; nb < NB; ++nb) C[q][nb][v] *= al;
+          }
       }
-      // 2. residual of the part's salient columns: one MFMA per 32 of them
+      // 2. residual of the part's salient columns: one MFMA per 32 of them.
+      // Row jr of tile q is row 16 (jr >> 2) + 4q + (jr & 3) of the 64-row
+      // tile: four-row group 4 (jr >> 2) + q, position jr & 3; the lane's four
+      // groups (q = 0..3) are consecutive, 8 bytes of the tile's residual
+      // values of a column, and 8 bits of its position word.
       const int g0 = pstart_slice * kSliceGroups;
       const int g1 = min((cur.slice + 1) * kSliceGroups, pr.n_groups);
       const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
+      // Every load of an iteration is issued before any of its values is
+      // used (indices clamped into the part's range, unused slots masked
+      // afterwards), so an iteration waits on memory twice: S and the
+      // residual words, then x at the salient columns.
+      gi32* Sp = gptr(pr.S);
+      gu16* xp = gptr(pr.x) + uint32_t(min(jr, B - 1)) * uint32_t(pr.K);
+      gu16* rvp = gptr(pr.rval) + uint32_t(tlc) * uint32_t(pr.nS) * 16u + 4u * uint32_t(jr >> 2);
+      gu32* rip = gptr(pr.ridx) + uint32_t(tlc) * uint32_t(pr.nS);
+      const uint32_t psh = 8u * uint32_t(jr >> 2);
+      const uint32_t bmask = (jr < B && jr < BP) ? 0xffffu : 0u;
       for (int s0 = s_lo; s0 < s_hi; s0 += 32) {
-        // B: x[j][S_s] in the hi columns (j < min(B, BP)), zero elsewhere
-        _Float16 bx[8];
+        int col[8];
+        u32x2 rv[8];
+        uint32_t pw[8];
 #pragma unroll
         for (int h = 0; h < 8; ++h) {
-          const int s = s0 + 8 * kb + h;
-          const int sc = min(s, s_hi - 1);
-          const int col = gptr(pr.S)[sc];
-          const _Float16 xv = __builtin_bit_cast(_Float16, gptr(pr.x)[uint32_t(min(jr, B - 1)) * uint32_t(pr.K) + uint32_t(col)]);
-          bx[h] = (s < s_hi && jr < B && jr < BP) ? xv : (_Float16)0;
+          const uint32_t sc = uint32_t(min(s0 + 8 * kb + h, s_hi - 1));
+          col[h] = Sp[sc];
+          rv[h] = *reinterpret_cast<gu32x2*>(rvp + 16u * sc);
+          pw[h] = rip[sc];
+        }
+        uint16_t xb[8];
+#pragma unroll
+        for (int h = 0; h < 8; ++h) xb[h] = xp[uint32_t(col[h])];
+        // B: x[j][S_s] in the hi columns (j < min(B, BP)), zero elsewhere;
+        // A: the value of four-row group 4 (jr >> 2) + q in row jr & 3 only
+        _Float16 bx[8], ar[4][8];
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const uint32_t in = (s0 + 8 * kb + h < s_hi) ? 0xffffu : 0u;
+          bx[h] = __builtin_bit_cast(_Float16, uint16_t(xb[h] & (in & bmask)));
+          const uint32_t pwh = pw[h] >> psh;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t wd = q < 2 ? rv[h].x : rv[h].y;
+            const uint32_t val = (q & 1) ? wd >> 16 : wd & 0xffffu;
+            const uint32_t hit = (((pwh >> (2 * q)) & 3u) == uint32_t(jr & 3)) ? in : 0u;
+            ar[q][h] = __builtin_bit_cast(_Float16, uint16_t(val & hit));
+          }
         }
         const half8 Bx = {bx[0], bx[1], bx[2], bx[3], bx[4], bx[5], bx[6], bx[7]};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          // A: row i = jr of tile q is row 16 (jr >> 2) + 4q + (jr & 3): four-row
-          // group 4 (jr >> 2) + q of the 64-row tile, position jr & 3
-          const int gg = 4 * (jr >> 2) + q;
-          _Float16 ar[8];
-#pragma unroll
-          for (int h = 0; h < 8; ++h) {
-            const int s = s0 + 8 * kb + h;
-            const int sc = min(s, s_hi - 1);
-            const int64_t ti = int64_t(tlc) * pr.nS + sc;
-            const _Float16 rv = __builtin_bit_cast(_Float16, gptr(pr.rval)[ti * 16 + gg]);
-            const uint32_t pos = (gptr(pr.ridx)[ti] >> (2 * gg)) & 3u;
-            ar[h] = (s < s_hi && pos == uint32_t(jr & 3)) ? rv : (_Float16)0;
-          }
-          const half8 Ar = {ar[0], ar[1], ar[2], ar[3], ar[4], ar[5], ar[6], ar[7]};
+          const half8 Ar = {ar[q][0], ar[q][1], ar[q][2], ar[q][3], ar[q][4], ar[q][5], ar[q][6], ar[q][7]};
           C[q][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ar, Bx, C[q][0], 0, 0, 0);
         }
       }
