@@ -34,7 +34,8 @@
 //     half-wave, so a half-wave's reads hit distinct banks), one 8-byte read
 //     gives digits 0-3 as two fp16 pairs (the A operand pairs as they are),
 //     and a 2-byte read from a 32-copy digit-4 table at half that address
-//     gives digit 4 straight into its half of the operand register;
+//     gives digit 4 (one v_perm pairs two bytes' digit 4 into one operand
+//     register);
 //   - ten MFMAs per row tile and column block: eight take digits 0-3 of two
 //     packs each, two take digit 4 of eight packs each; the B operands are
 //     per slice images in LDS in exactly the MFMA lane order, built one unit
@@ -55,23 +56,18 @@ constexpr int kMRP = kMW * 64;            // rows per panel
 constexpr int kMu = 10;                   // MFMAs per group unit and column block
 constexpr int kRowStride = 256;           // bytes per code in the digit 0-3 table (32 copies x 8)
 constexpr int kTab = kCodes * kRowStride; // 62,208 bytes
-// Digit-4 table, either mirrored (code c, copy k at kTab + c * 256 + 8 k: the
-// digit 0-3 entry's address plus a constant) or compact (kTab + c * 128 +
-// 4 k: half that address plus a constant, one shift more per byte, half the
-// space); the mirror leaves no room for two column blocks' images.
-template <int NB>
-struct T4 {
-  static constexpr bool kMirror = NB == 1;
-  static constexpr int kBytes = kMirror ? kCodes * 256 : kCodes * 128;
-  static constexpr int kStride = kMirror ? 8 : 4;  // bytes per copy
-};
+// Digit-4 table: code c, copy k at kTab + c * 128 + 4 k, half the digit 0-3
+// entry's address plus a constant (one shift per byte).  Its reads have a
+// 4-byte stride across a half-wave; a table at the digit 0-3 entry's own
+// address (8-byte stride) takes twice as long per 2-byte read.
+constexpr int kT4Bytes = kCodes * 128;
 constexpr int kImg = kMu * 64 * 16;       // one B-operand image (10 MFMAs x 64 lanes x 16 bytes)
 constexpr float kBigScale = 1.0f / 65536.0f;
 
 template <int NB>
 struct MLds {
   static constexpr int T4OFF = kTab;
-  static constexpr int IMG = kTab + T4<NB>::kBytes;  // [2 buffers][NB] images
+  static constexpr int IMG = kTab + kT4Bytes;  // [2 buffers][NB] images
   static constexpr int FLAG = IMG + 2 * NB * kImg;    // int [3]: slice needs scaling
   static constexpr int BYTES = FLAG + 16;
 };
@@ -160,7 +156,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     const _Float16 t4[2] = {(_Float16)(d4 - 1), (_Float16)0};
     uint32_t m4;
     __builtin_memcpy(&m4, t4, 4);
-    *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * (32 * T4<NB>::kStride) + T4<NB>::kStride * cp) = m4;
+    *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = m4;
   }
   if (tid < 3) bigf[tid] = 0;
   __syncthreads();  // flags cleared before the first images can set one
@@ -316,10 +312,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
         for (int k = 0; k < 8; ++k) d03[k] = *(lds_u32x2*)(size_t(ad[k]));
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          if constexpr (T4<NB>::kMirror)
-            d4[k] = lds_pair(ad[2 * k] + L::T4OFF, ad[2 * k + 1] + L::T4OFF);
-          else
-            d4[k] = lds_pair((ad[2 * k] >> 1) + L::T4OFF, (ad[2 * k + 1] >> 1) + L::T4OFF);
+          d4[k] = lds_pair((ad[2 * k] >> 1) + L::T4OFF, (ad[2 * k + 1] >> 1) + L::T4OFF);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
