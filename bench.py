@@ -54,15 +54,19 @@ def build_stack(wl, B, dev, seed, layers=None):
     for layer, mat, role, N, K in wl.matrices():
         if layers is not None and layer >= layers:
             break
-        L = synth.layer_inputs(seed, layer, mat, N, K, p0=wl.p0, frac=wl.frac)
+        L = synth.layer_inputs(seed, layer, mat, N, K, p0=wl.p0, frac=wl.frac, resid=wl.resid)
         x = synth.activations(seed, layer, mat, B, K)
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-        pm = q.pack_matrix(t(L["trits"]), t(L["alpha"]), t(L["v"]), t(L["S"]), t(L["R"]), t(L["idx"]))
         nS = int(L["S"].size)
+        if wl.resid == "e4m3":
+            pm = q.pack_matrix_e4m3(t(L["trits"]), t(L["alpha"]), t(L["v"]), t(L["bitmap"]), nS, t(L["R8"]),
+                                    t(L["idx"]))
+        else:
+            pm = q.pack_matrix(t(L["trits"]), t(L["alpha"]), t(L["v"]), t(L["S"]), t(L["R"]), t(L["idx"]))
         mats.append({
             "layer": layer, "mat": mat, "role": role, "N": N, "K": K, "nS": nS, "pm": pm, "x": t(x),
             "y": torch.empty((B, N), dtype=torch.float32, device=dev),
-            "bytes": q.algorithmic_bytes(N, K, nS),
+            "bytes": q.algorithmic_bytes(N, K, nS, value_bytes=1 if wl.resid == "e4m3" else 2),
         })
         if layer == 0 or (layer + 1) % 8 == 0 and mat == len(wl.shapes) - 1:
             log(f"packed layer {layer} {role} {N}x{K} ({time.time() - t0:.1f}s)")
@@ -137,17 +141,20 @@ def replay_spread(g, stream, reps):
             "replays": reps}
 
 
-def kernel_name(B, grouped=False, rows_per_panel=1024):
+def kernel_name(B, grouped=False, rows_per_panel=1024, e4m3=False):
+    f8 = "true" if e4m3 else "false"
     if grouped and B > 1:
-        return f"grouped_mma_kernel<{1 if B <= 8 else 2}>"  # hi/lo activation halves in one or two MFMAs
+        # hi/lo activation halves in one or two MFMAs
+        return f"grouped_mma_kernel<{1 if B <= 8 else 2}, {f8}>"
     if grouped:
-        return f"grouped_gemv_kernel<{rows_per_panel // 128}>"  # 8 waves x 16 rows per row block
+        return f"grouped_gemv_kernel<{rows_per_panel // 128}, {f8}>"  # 8 waves x 16 rows per row block
     return f"fk_gemv_kernel<{B}>" if B <= 4 else f"lut_gemv_kernel<{B}, 2>"
 
 
-def traffic_per_launch(kernel, algorithmic_bytes):
+def traffic_per_launch(kernel, algorithmic_bytes, workload="llama3_8b_stack batch 1"):
     """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel source (sha256 recorded in the summary)."""
+    taken on this kernel and workload and on the current kernel source
+    (sha256 recorded in the summary)."""
     import hashlib
 
     name = "grouped_gemv" if kernel.startswith("grouped") else "fk_gemv"
@@ -164,7 +171,7 @@ def traffic_per_launch(kernel, algorithmic_bytes):
     for f in srcs:  # the kernel's source file, then the shared header
         h.update(open(os.path.join(ROOT, "paper_2609_00224_amd", "csrc", f), "rb").read())
     digest = h.hexdigest()
-    if kv.get("kernel") != kernel or kv.get("source_sha256") != digest:
+    if kv.get("kernel") != kernel or kv.get("source_sha256") != digest or kv.get("workload") != workload:
         return None
     try:
         return int(float(kv["hbm_bytes_per_launch"]))
@@ -202,7 +209,10 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
     worst = 0.0
     t_oracle = 0.0
     for m in mats:
-        L = synth.layer_inputs(seed, m["layer"], m["mat"], m["N"], m["K"], p0=wl.p0, frac=wl.frac)
+        L = synth.layer_inputs(seed, m["layer"], m["mat"], m["N"], m["K"], p0=wl.p0, frac=wl.frac,
+                               resid=wl.resid)
+        if wl.resid == "e4m3":
+            L["R"] = oracle.e4m3_as_half(L["R8"])
         x = synth.activations(seed, m["layer"], m["mat"], B, m["K"])
         P = oracle.pack(L.pop("trits"))
         args = (m["N"], m["K"], P, L["alpha"], L["v"], L["S"], L["R"], L["idx"], x)
@@ -319,13 +329,13 @@ def main():
     # so the average launch moves token_bytes / launches.  Durations come
     # from HIP events around the graph replays above.
     n_launch = 1 if grouped else len(mats)
-    kname = kernel_name(B, grouped, gp.info.rows_per_panel if grouped else 1024)
+    kname = kernel_name(B, grouped, gp.info.rows_per_panel if grouped else 1024, wl.resid == "e4m3")
     per_launch_bytes = token_bytes / n_launch
     us_launch = ms * 1e3 / n_launch
     ach = per_launch_bytes / (us_launch * 1e-6) / 1e9
     roof = {"bound": "hbm", "achieved": round(ach, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBS, 4),
-            "traffic": traffic_per_launch(kname, per_launch_bytes),
+            "traffic": traffic_per_launch(kname, per_launch_bytes, f"{wl.name} batch {B}"),
             "kernel": kname, "launches_per_step": n_launch,
             "algorithmic_bytes_per_launch": int(per_launch_bytes), "us_per_launch": round(us_launch, 3)}
     chained = {"us_per_token": round(ms_chain * 1e3, 2), "value": round(gbs_chain, 2), "unit": "GB/s",

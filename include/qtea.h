@@ -41,14 +41,16 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 2
+#define QTEA_ABI_VERSION 3
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
   QTEA_OK = 0,
   QTEA_ERR_INVALID_ARG = -1, /* null pointer, bad size, bad descriptor      */
   QTEA_ERR_BAD_TRIT = -2,    /* a trit outside {-1, 0, +1}                   */
-  QTEA_ERR_BAD_RESIDUAL = -3,/* idx > 3, or S not strictly increasing in [0,K) */
+  QTEA_ERR_BAD_RESIDUAL = -3,/* idx > 3, S not strictly increasing in [0,K),
+                                a salient bitmap that disagrees with n_salient
+                                or marks a column >= K, an E4M3 NaN value  */
   QTEA_ERR_BATCH = -4,       /* batch outside [1, QTEA_MAX_BATCH]            */
   QTEA_ERR_WORKSPACE = -5,   /* workspace or packed buffer too small         */
   QTEA_ERR_HIP = -6,         /* a HIP runtime call or kernel launch failed   */
@@ -62,7 +64,8 @@ enum qtea_status {
  */
 typedef struct qtea_desc {
   uint32_t magic;       /* QTEA_DESC_MAGIC when valid                        */
-  uint32_t layout;      /* device layout version                             */
+  uint32_t layout;      /* device layout version: 2 = fp16 residual values,
+                           3 = FP8 E4M3 residual values (qtea_pack_e4m3)     */
   int64_t N, K;         /* output rows, input columns                        */
   int64_t n_salient;    /* |S|                                               */
   int64_t n_packs;      /* ceil(K / 5) one-byte packs per row                */
@@ -114,6 +117,30 @@ int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_sca
               int64_t packed_bytes, qtea_desc* out_desc, void* stream);
 
 /*
+ * The paper's storage of the salient residual (the "compact
+ * semi-structured format" of its GEMV section, at its evaluation setting of
+ * FP8 E4M3 values in 5% of the columns): a bitmap over the input columns
+ * marks the salient ones, and every four-entry group of a salient column
+ * holds one one-byte E4M3 value with its 2-bit position.  Same operation as
+ * qtea_pack with R[s][g] = the E4M3 value (exact in fp16 and fp32; every
+ * GEMV entry point accepts either layout).
+ *
+ *   salient_bitmap device uint32 [ceil(K/32)]: bit (j % 32) of word j / 32
+ *                  set when column j is salient; bits at or past K clear;
+ *                  exactly n_salient bits set.  S is the set bits ascending.
+ *   resid_val      device uint8 [n_salient][N/4]: E4M3 codes (sign, four
+ *                  exponent bits of bias 7, three mantissa bits; the two
+ *                  NaN codes 0x7f, 0xff are rejected)
+ *   packed         device buffer of packed_bytes >= qtea_packed_bytes_e4m3(...)
+ * Other arguments, errors and synchronization as qtea_pack.
+ */
+int qtea_packed_bytes_e4m3(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes);
+int qtea_pack_e4m3(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
+                   const uint16_t* col_rescale, const uint32_t* salient_bitmap, int64_t n_salient,
+                   const uint8_t* resid_val, const uint8_t* resid_idx, void* packed, int64_t packed_bytes,
+                   qtea_desc* out_desc, void* stream);
+
+/*
  * Workspace bytes that qtea_gemv (batch = 1) / qtea_gemm_lowbatch need for
  * this matrix at this batch size.  The workspace holds per-K-slice partial
  * sums and per-row-block arrival counters.  It must be zero-filled before
@@ -160,9 +187,10 @@ int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_
                       int8_t* trits, int32_t* resid_row, void* stream);
 
 /*
- * Grouped GEMV: y_m = W_m x_m for a list of n_problems independent problems
- * (each W_m packed by qtea_pack; the same operation as qtea_gemv applied to
- * every problem) in one persistent launch.  The problems' packed bytes are
+ * Grouped GEMV: Y_m = X_m W_m^T for a list of n_problems independent problems
+ * at one batch size (each W_m packed by qtea_pack or, all of them,
+ * qtea_pack_e4m3; the same operation as qtea_gemm_lowbatch applied to every
+ * problem) in one persistent launch.  The problems' packed bytes are
  * streamed back to back: a workgroup already loads the next problem's
  * weights while it finishes the current one.  No problem may read another
  * problem's output (all activations must be ready when the launch starts);
@@ -176,12 +204,16 @@ int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_
 typedef struct qtea_grouped_info {
   uint32_t magic;          /* set by qtea_grouped_plan                    */
   int32_t n_problems;
-  int32_t batch;           /* activation rows per problem (only 1 so far) */
-  int32_t grid;            /* workgroups of the launch (two per CU)       */
+  int32_t batch;           /* activation rows per problem (1..16)         */
+  int32_t grid;            /* workgroups of the launch (batch 1: two per
+                              CU, table lookups; batch 2..16: one per CU,
+                              matrix cores)                               */
   int32_t rows_per_panel;  /* output rows of one work unit               */
   int32_t max_parts;       /* chunks sharing one panel, at most          */
   int32_t n_chunks;        /* chunks of work units (scheduling grain)    */
   int32_t n_split_panels;  /* panels whose parts are summed by a second launch */
+  int32_t layout;          /* residual layout of every problem (2 or 3)  */
+  int32_t reserved;
   int64_t n_units;
   int64_t plan_bytes;      /* device plan buffer size                    */
   int64_t workspace_bytes; /* workspace needed by qtea_grouped_gemv      */
@@ -196,11 +228,13 @@ int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes);
  *                        pointers to the packed buffers (qtea_pack)
  *   x[m]                 host array of device pointers, fp16 [batch][K_m]
  *   y[m]                 host array of device pointers, fp32 [batch][N_m]
- *   batch                must be 1 (QTEA_ERR_BATCH otherwise)
+ *   batch                activation rows per problem, 1..QTEA_MAX_BATCH
+ *                        (QTEA_ERR_BATCH otherwise)
  *   plan                 device buffer, >= qtea_grouped_plan_bytes(n_problems)
  *   info                 host, filled on success
  * Errors: QTEA_ERR_INVALID_ARG (also for a matrix whose packed codes or
- * residual values take 2 GiB or more: the kernel uses 32-bit offsets),
+ * residual values take 2 GiB or more: the kernel uses 32-bit offsets; and
+ * for a list that mixes the two residual layouts),
  * QTEA_ERR_BATCH, QTEA_ERR_WORKSPACE (plan buffer too small), QTEA_ERR_HIP.
  */
 int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const uint16_t* const* x,

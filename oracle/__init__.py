@@ -9,8 +9,9 @@ this module only marshals numpy arrays through ctypes.
 Pins (tests/test_oracle.py): exhaustive code round trip, sign-symmetry and
 zero-pattern closed forms, hand-worked example (tests/golden), brute force
 in exact rational arithmetic on tiny inputs, textbook special cases, the
-paper's bits-per-weight figures.  Every function is pinned; none is marked
-"parity unpinned".
+paper's bits-per-weight figures, the FP8 E4M3 decode against a library
+routine and the format's closed forms, the salient bitmap against brute
+force.  Every function is pinned; none is marked "parity unpinned".
 """
 from __future__ import annotations
 
@@ -83,6 +84,12 @@ def _L():
         lib.or_bpw_paper.argtypes = [dbl, dbl]
         lib.or_algorithmic_bytes.restype = i64
         lib.or_algorithmic_bytes.argtypes = [i64, i64, i64]
+        lib.or_e4m3_to_double.restype = dbl
+        lib.or_e4m3_to_double.argtypes = [ctypes.c_uint8]
+        lib.or_bitmap_to_list.restype = i64
+        lib.or_bitmap_to_list.argtypes = [vp, i64, vp, i64]
+        lib.or_algorithmic_bytes_vb.restype = i64
+        lib.or_algorithmic_bytes_vb.argtypes = [i64, i64, i64, i64]
         _lib = lib
     return _lib
 
@@ -233,3 +240,44 @@ def bpw_paper(f, value_bits) -> float:
 
 def algorithmic_bytes(N, K, nS) -> int:
     return int(_L().or_algorithmic_bytes(N, K, nS))
+
+
+def e4m3_to_double(code: int) -> float:
+    return float(_L().or_e4m3_to_double(int(code) & 0xFF))
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    """fp64 values of FP8 E4M3 codes (any shape)."""
+    c = _c(codes, np.uint8)
+    table = np.array([e4m3_to_double(i) for i in range(256)], dtype=np.float64)
+    return table[c]
+
+
+def e4m3_as_half(codes) -> np.ndarray:
+    """The same values as fp16 (every finite E4M3 value is one); raises if a
+    code is NaN."""
+    d = e4m3_decode(codes)
+    if np.isnan(d).any():
+        raise OracleError(ERR_RESID, "e4m3_as_half (NaN code)")
+    h = d.astype(np.float16)
+    assert np.array_equal(h.astype(np.float64), d)
+    return h
+
+
+def bitmap_to_list(words, K: int) -> np.ndarray:
+    """Ascending salient columns marked in a column bitmap."""
+    w = np.ascontiguousarray(words)
+    if w.dtype.itemsize != 4:
+        raise ValueError("bitmap words are 32-bit")
+    w = w.view(np.uint32)
+    if w.size != (K + 31) // 32:
+        raise ValueError("a bitmap of ceil(K/32) words")
+    S = np.empty(K, dtype=np.int32)
+    n = int(_L().or_bitmap_to_list(w.ctypes.data, K, S.ctypes.data, K))
+    if n < 0:
+        raise OracleError(n, "bitmap_to_list")
+    return S[:n].copy()
+
+
+def algorithmic_bytes_vb(N, K, nS, value_bytes) -> int:
+    return int(_L().or_algorithmic_bytes_vb(N, K, nS, value_bytes))

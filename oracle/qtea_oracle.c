@@ -332,3 +332,43 @@ int64_t or_algorithmic_bytes(int64_t N, int64_t K, int64_t nS) {
   const int64_t entries = (N / 4) * nS;
   return N * or_num_packs(K) + 2 * entries + (2 * entries + 7) / 8 + 2 * N + 2 * K + 4 * nS;
 }
+
+/* The paper's storage of the salient residual (its GEMV section, at its
+ * evaluation setting): one FP8 E4M3 value per four entries of a salient
+ * column and a bitmap over the input columns marking the salient ones. */
+
+/* FP8 E4M3 -> binary64, from the format's definition: sign bit, 4 exponent
+ * bits with bias 7, 3 mantissa bits; exponent 0 is subnormal (m/8 * 2^-6);
+ * no infinities; exponent 15 with mantissa 7 is NaN. */
+double or_e4m3_to_double(uint8_t c) {
+  const int sign = c >> 7, e = (c >> 3) & 15, m = c & 7;
+  double mag;
+  if (e == 15 && m == 7)
+    mag = NAN;
+  else if (e == 0)
+    mag = ldexp((double)m, -9); /* (m / 8) * 2^(1 - 7) */
+  else
+    mag = ldexp((double)(8 + m), e - 10); /* (1 + m/8) * 2^(e - 7) */
+  return sign ? -mag : mag;
+}
+
+/* Salient column list from a bitmap (bit j % 32 of word j / 32 marks column
+ * j), ascending.  Returns the count, or OR_ERR_RESID for a bit at or past K
+ * or more than cap columns. */
+int64_t or_bitmap_to_list(const uint32_t* words, int64_t K, int32_t* S, int64_t cap) {
+  int64_t n = 0;
+  const int64_t nw = (K + 31) / 32;
+  for (int64_t j = 0; j < 32 * nw; ++j) {
+    if (!((words[j / 32] >> (j % 32)) & 1u)) continue;
+    if (j >= K || n >= cap) return OR_ERR_RESID;
+    S[n++] = (int32_t)j;
+  }
+  return n;
+}
+
+/* Weight bytes of one GEMV as or_algorithmic_bytes, with value_bytes per
+ * residual value (2 for fp16, 1 for E4M3). */
+int64_t or_algorithmic_bytes_vb(int64_t N, int64_t K, int64_t nS, int64_t value_bytes) {
+  const int64_t entries = (N / 4) * nS;
+  return N * or_num_packs(K) + value_bytes * entries + (2 * entries + 7) / 8 + 2 * N + 2 * K + 4 * nS;
+}

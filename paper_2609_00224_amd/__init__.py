@@ -1,13 +1,13 @@
 """MI355X (gfx950) compressed ternary GEMV: Python binding of libqtea.so.
 
 The binding marshals arguments only: every step of the GEMV runs in the HIP
-kernels of ``csrc/qtea.hip`` and ``csrc/grouped.hip`` behind the C ABI of
-``include/qtea.h``.  Torch
+kernels of ``csrc/qtea.hip``, ``csrc/grouped.hip`` and ``csrc/grouped_mma.hip``
+behind the C ABI of ``include/qtea.h``.  Torch
 is used to allocate device memory and to name the current HIP stream.
 There is no CPU fallback: if the library is not built, loading it raises.
 
 Entry points carry the C names: qtea_packed_bytes, qtea_pack,
-qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
+qtea_packed_bytes_e4m3, qtea_pack_e4m3, qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
 qtea_debug_unpack, qtea_status_string, qtea_abi_version,
 qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv.
 """
@@ -35,7 +35,10 @@ EXPORTS = (
     "qtea_status_string", "qtea_abi_version", "qtea_packed_bytes", "qtea_pack",
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
     "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
+    "qtea_packed_bytes_e4m3", "qtea_pack_e4m3",
 )
+QTEA_LAYOUT_FP16 = 2  # residual values fp16
+QTEA_LAYOUT_E4M3 = 3  # residual values FP8 E4M3
 QTEA_GROUPED_MAGIC = 0x51475250
 
 
@@ -57,7 +60,9 @@ class QteaGroupedInfo(ctypes.Structure):
     _fields_ = [
         ("magic", ctypes.c_uint32), ("n_problems", ctypes.c_int32), ("batch", ctypes.c_int32),
         ("grid", ctypes.c_int32), ("rows_per_panel", ctypes.c_int32), ("max_parts", ctypes.c_int32),
-        ("n_chunks", ctypes.c_int32), ("n_split_panels", ctypes.c_int32), ("n_units", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+        ("n_chunks", ctypes.c_int32), ("n_split_panels", ctypes.c_int32),
+        ("layout", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("n_units", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
     ]
 
 
@@ -89,6 +94,10 @@ def load(path: str = LIB_PATH):
     lib.qtea_packed_bytes.argtypes = [i64, i64, i64, ctypes.POINTER(i64)]
     lib.qtea_pack.restype = i32
     lib.qtea_pack.argtypes = [vp, i64, i64, vp, vp, vp, i64, vp, vp, vp, i64, pdesc, vp]
+    lib.qtea_packed_bytes_e4m3.restype = i32
+    lib.qtea_packed_bytes_e4m3.argtypes = [i64, i64, i64, ctypes.POINTER(i64)]
+    lib.qtea_pack_e4m3.restype = i32
+    lib.qtea_pack_e4m3.argtypes = [vp, i64, i64, vp, vp, vp, i64, vp, vp, vp, i64, pdesc, vp]
     lib.qtea_workspace_bytes.restype = i32
     lib.qtea_workspace_bytes.argtypes = [pdesc, i32, ctypes.POINTER(i64)]
     lib.qtea_workspace_init.restype = i32
@@ -171,6 +180,37 @@ def qtea_pack(trits, row_scale, col_rescale, salient, resid_val, resid_idx, pack
                           _ptr(packed), packed.numel() * packed.element_size(), ctypes.byref(d),
                           _stream(stream))
     _check(st, "qtea_pack")
+    return d
+
+
+def qtea_packed_bytes_e4m3(N: int, K: int, n_salient: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().qtea_packed_bytes_e4m3(N, K, n_salient, ctypes.byref(out)), "qtea_packed_bytes_e4m3")
+    return out.value
+
+
+def qtea_pack_e4m3(trits, row_scale, col_rescale, salient_bitmap, n_salient: int, resid_val,
+                   resid_idx, packed, stream=None) -> QteaDesc:
+    """Pack with the paper's residual storage: int8 [N][K] trits, fp16 [N]
+    and [K] scales, int32 [ceil(K/32)] salient column bitmap (bit j % 32 of
+    word j / 32), uint8 [nS][N/4] E4M3 residual codes, uint8 [nS][N/4]
+    positions, into `packed` (uint8, >= qtea_packed_bytes_e4m3)."""
+    import torch
+
+    _need_cuda(trits, row_scale, col_rescale, salient_bitmap, resid_val, resid_idx, packed)
+    assert trits.dtype == torch.int8 and row_scale.dtype == torch.float16
+    assert col_rescale.dtype == torch.float16 and salient_bitmap.dtype == torch.int32
+    assert resid_val.dtype == torch.uint8 and resid_idx.dtype == torch.uint8
+    N, K = trits.shape
+    if salient_bitmap.numel() != (K + 31) // 32:
+        raise ValueError("the salient bitmap has ceil(K/32) words")
+    nS = int(n_salient)
+    d = QteaDesc()
+    st = load().qtea_pack_e4m3(_ptr(trits), N, K, _ptr(row_scale), _ptr(col_rescale), _ptr(salient_bitmap),
+                               nS, _ptr(resid_val) if nS else None, _ptr(resid_idx) if nS else None,
+                               _ptr(packed), packed.numel() * packed.element_size(), ctypes.byref(d),
+                               _stream(stream))
+    _check(st, "qtea_pack_e4m3")
     return d
 
 
@@ -290,6 +330,18 @@ def pack_matrix(trits, alpha, v, S, R, idx, stream=None) -> PackedMatrix:
     return PackedMatrix(d, packed)
 
 
+def pack_matrix_e4m3(trits, alpha, v, bitmap, n_salient, R8, idx, stream=None) -> PackedMatrix:
+    """Allocate the packed buffer and pack with E4M3 residual values and a
+    salient column bitmap (all arguments device tensors)."""
+    import torch
+
+    N, K = trits.shape
+    nbytes = qtea_packed_bytes_e4m3(N, K, int(n_salient))
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=trits.device)
+    d = qtea_pack_e4m3(trits, alpha, v, bitmap, n_salient, R8, idx, packed, stream=stream)
+    return PackedMatrix(d, packed)
+
+
 def new_workspace(desc: QteaDesc, batch: int, device="cuda"):
     """A zero-filled workspace for this matrix and batch size."""
     import torch
@@ -298,10 +350,11 @@ def new_workspace(desc: QteaDesc, batch: int, device="cuda"):
     return torch.zeros(max(n, 4), dtype=torch.uint8, device=device)
 
 
-def algorithmic_bytes(N: int, K: int, n_salient: int) -> int:
+def algorithmic_bytes(N: int, K: int, n_salient: int, value_bytes: int = 2) -> int:
     """Weight bytes one GEMV must read in the paper's format: packed trits
-    (ceil(K/5) bytes per row), fp16 residual values plus 2-bit positions for
-    one entry per four rows of each salient column, fp16 alpha and v, and
-    the int32 salient list."""
+    (ceil(K/5) bytes per row), residual values (fp16: 2 bytes, E4M3: 1)
+    plus 2-bit positions for one entry per four rows of each salient column,
+    fp16 alpha and v, and the int32 salient list."""
     entries = (N // 4) * n_salient
-    return N * ((K + 4) // 5) + 2 * entries + (2 * entries + 7) // 8 + 2 * N + 2 * K + 4 * n_salient
+    return (N * ((K + 4) // 5) + value_bytes * entries + (2 * entries + 7) // 8 + 2 * N + 2 * K
+            + 4 * n_salient)

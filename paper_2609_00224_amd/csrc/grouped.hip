@@ -83,7 +83,8 @@ __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
   return 0x0C0C0000u | (uint32_t(k) << 8) | uint32_t(4 + k);
 }
 
-template <int RB>
+// F8: residual values are E4M3 bytes (layout 3), else fp16 (layout 2).
+template <int RB, bool F8>
 __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __restrict__ plan,
                                                            float* __restrict__ part,
                                                            uint32_t* __restrict__ counters) {
@@ -164,10 +165,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // salient residual of unit c: this wave's tiles over the slice's first
   // kResCols salient columns, fetched as two loads per lane and staged in
   // the wave's LDS area in the residual phase.  rvq: 16 bytes of a tile's
-  // value run (32 bytes per column; lanes 0..31 the first tile, 32..63 the
-  // second); ris: lanes 0..31 the position words of the tiles (16 per tile),
-  // lanes 32..63 the salient column indices.  Indices are clamped into their
-  // regions (without salient columns both read the row scales).
+  // value run (fp16: 32 bytes per column, lanes 0..31 the first tile, 32..63
+  // the second; E4M3: 16 bytes per column, lanes 0..15 and 16..31, the upper
+  // half-wave repeating them); ris: lanes 0..31 the position words of the
+  // tiles (16 per tile), lanes 32..63 the salient column indices.  Indices
+  // are clamped into their regions (without salient columns both read the
+  // row scales).
   u32x4 rvq;
   uint32_t ris;
   auto load_res = [&](const Cursor c, const int s_lo, const int s_hi) {
@@ -175,11 +178,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const bool any = pr.nS > 0;
     const uint32_t nS = uint32_t(pr.nS), n_tiles = uint32_t(pr.n_pad >> 6);
     const uint32_t tile0 = uint32_t(c.panel * TPP + w * TPW);
-    const uint32_t Tv = min(tile0 + (TPW == 2 ? uint32_t(lane >> 5) : 0u), n_tiles - 1u);
+    constexpr uint32_t VB = F8 ? 16u : 32u;  // value bytes per (tile, salient column)
+    const uint32_t Tv = min(tile0 + (TPW == 2 ? uint32_t(F8 ? (lane >> 4) & 1 : lane >> 5) : 0u), n_tiles - 1u);
     const uint32_t ncs = uint32_t(min(s_hi - s_lo, kResCols));
-    const uint32_t len = ncs * 32u;
-    const uint32_t lofs = min(uint32_t(lane & 31) * 16u, len >= 16u ? len - 16u : 0u);
-    const uint32_t vofs = any ? min((Tv * nS + uint32_t(s_lo)) * 32u + lofs, n_tiles * nS * 32u - 16u) : 0u;
+    const uint32_t len = ncs * VB;
+    const uint32_t lofs = min(uint32_t(lane & (F8 ? 15 : 31)) * 16u, len >= 16u ? len - 16u : 0u);
+    const uint32_t vofs = any ? min((Tv * nS + uint32_t(s_lo)) * VB + lofs, n_tiles * nS * VB - 16u) : 0u;
     rvq = *reinterpret_cast<const gu32x4*>(
         (any ? reinterpret_cast<gu8*>(gptr(pr.rval)) : reinterpret_cast<gu8*>(gptr(pr.alpha))) + vofs);
     const uint32_t Ti = min(tile0 + (TPW == 2 ? uint32_t((lane >> 4) & 1) : 0u), n_tiles - 1u);
@@ -390,10 +394,11 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       asm volatile("" ::: "memory");
       const int nc = grow_ok ? (ncol < kResCols ? ncol : kResCols) : 0;
       for (int c = rq; c < nc; c += QR) {
-        const uint16_t hv = reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16];
+        const float rv = F8 ? e4m3_to_float(reinterpret_cast<const uint8_t*>(rv_w)[256 * rtile + 16 * c + g16])
+                            : h2f(reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16]);
         const uint32_t idx = (ri_w[16 * rtile + c] >> gsh) & 3u;
         const float xv = __uint_as_float(ri_w[32 + c]);
-        const float t = h2f(hv) * xv;
+        const float t = rv * xv;
 #pragma unroll
         for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
       }
@@ -402,7 +407,9 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       const int64_t T = int64_t(grow >> 4);
       for (int s = s_lo + kResCols + rq; s < s_hi; s += QR) {
         if (grow_ok) {
-          const float t = h2f(gptr(pr.rval)[rval_index(grow, s, pr.nS)]) * xr_lds[gptr(pr.S)[s] - col0];
+          const int64_t vi = rval_index(grow, s, pr.nS);
+          const float rv = F8 ? e4m3_to_float(reinterpret_cast<gu8*>(gptr(pr.rval))[vi]) : h2f(gptr(pr.rval)[vi]);
+          const float t = rv * xr_lds[gptr(pr.S)[s] - col0];
           const uint32_t idx = (gptr(pr.ridx)[T * pr.nS + s] >> gsh) & 3u;
 #pragma unroll
           for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
@@ -544,11 +551,11 @@ int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   return *n_slices * *n_panels;
 }
 
-template <int RB>
+template <int RB, bool F8>
 hipError_t set_lds_attr() {
   static bool done = false;
   if (!done) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB, F8>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, GLds<RB>::BYTES);
     if (e != hipSuccess) return e;
     done = true;
@@ -570,19 +577,20 @@ int grid_size() {
   int dev = 0, n = 0, per = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (set_lds_attr<kMaxRB>() != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, reinterpret_cast<const void*>(&grouped_gemv_kernel<kMaxRB>),
+  if (set_lds_attr<kMaxRB, false>() != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, reinterpret_cast<const void*>(&grouped_gemv_kernel<kMaxRB, false>),
                                                    kGT, GLds<kMaxRB>::BYTES) != hipSuccess)
     return 0;
   return n * std::max(1, std::min(per, kWgPerCu));
 }
 
-template <int RB>
+template <int RB, bool F8>
 hipError_t launch_grouped(const uint8_t* plan, int grid, int n_splits, float* part, uint32_t* counters,
                           hipStream_t st) {
-  const hipError_t e = set_lds_attr<RB>();
+  const hipError_t e = set_lds_attr<RB, F8>();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(grouped_gemv_kernel<RB>, dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan, part, counters);
+  hipLaunchKernelGGL((grouped_gemv_kernel<RB, F8>), dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan, part,
+                     counters);
   if (n_splits > 0) {
     constexpr int RP = GLds<RB>::RP;
     hipLaunchKernelGGL(grouped_reduce_kernel<RP>, dim3(n_splits), dim3(RP / 4), 0, st, plan, part);
@@ -620,11 +628,13 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   const bool mma = batch > 1;
   const int G = mma ? cu_count() : grid_size();
   if (G < 1) return QTEA_ERR_HIP;
+  const uint32_t layout = descs[0].layout;
   for (int m = 0; m < n_problems; ++m) {
     if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
+    if (descs[m].layout != layout) return QTEA_ERR_INVALID_ARG;  // one residual format per plan
     // the kernel addresses the packed bytes and the residual with 32-bit offsets
     const int64_t trit_bytes = descs[m].n_pad * descs[m].n_groups * kGroupPacks;
-    const int64_t resid_bytes = (descs[m].n_pad / 4) * descs[m].n_salient * 2;
+    const int64_t resid_bytes = (descs[m].n_pad / 4) * descs[m].n_salient * (layout == kLayoutE4M3 ? 1 : 2);
     if (trit_bytes >= (int64_t(1) << 31) || resid_bytes >= (int64_t(1) << 31)) return QTEA_ERR_INVALID_ARG;
   }
 
@@ -787,6 +797,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   H->n_grabs = n_grabs;
   H->off_splits = off_splits;
   H->n_splits = n_splits;
+  H->f8 = layout == kLayoutE4M3;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(plan, hbuf, size_t(need), hipMemcpyHostToDevice, st);
@@ -802,6 +813,8 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   info->max_parts = max_parts;
   info->n_chunks = int32_t(n_chunks);
   info->n_split_panels = int32_t(n_splits);
+  info->layout = int32_t(layout);
+  info->reserved = 0;
   info->n_units = total_units;
   info->plan_bytes = need;
   info->workspace_bytes = kAlign + 2 * n_chunks * RP * int64_t(batch) * 4;
@@ -817,19 +830,23 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   float* part = reinterpret_cast<float*>(ws + kAlign);
   const uint8_t* pl = static_cast<const uint8_t*>(plan);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (info->layout != kLayout && info->layout != kLayoutE4M3) return QTEA_ERR_INVALID_ARG;
+  const bool f8 = info->layout == kLayoutE4M3;
   hipError_t e;
   if (info->batch > 1) {
     if (info->rows_per_panel != grouped_mma_rows_per_panel()) return QTEA_ERR_INVALID_ARG;
-    e = launch_grouped_mma(pl, info->grid, info->batch, part, st);
+    e = launch_grouped_mma(pl, info->grid, info->batch, f8, part, st);
     if (e == hipSuccess && info->n_split_panels > 0) {
       hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, pl, part);
       e = hipGetLastError();
     }
     return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
   }
-  switch (info->rows_per_panel) {
-    case GLds<4>::RP: e = launch_grouped<4>(pl, info->grid, info->n_split_panels, part, counters, st); break;
-    case GLds<8>::RP: e = launch_grouped<8>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+  switch (info->rows_per_panel * (f8 ? -1 : 1)) {
+    case GLds<4>::RP: e = launch_grouped<4, false>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+    case GLds<8>::RP: e = launch_grouped<8, false>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+    case -GLds<4>::RP: e = launch_grouped<4, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+    case -GLds<8>::RP: e = launch_grouped<8, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
     default: return QTEA_ERR_INVALID_ARG;
   }
   return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;

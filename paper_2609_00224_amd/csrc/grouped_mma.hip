@@ -115,6 +115,20 @@ __device__ __forceinline__ float dpp_ror8(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x128, 0xf, 0xf, false));
 }
 
+// Four E4M3 bytes to four fp16 values (bytes 0, 1 in the first dword, 2, 3
+// in the second).  A code's seven magnitude bits placed at bits 7..13 of a
+// half are the fp16 bits of its value times 2^-8 (a subnormal code gives a
+// subnormal half), so one exact multiply by 256 per pair restores the
+// value; the sign bits move to bit 15 of their halves.
+__device__ __forceinline__ u32x2 e4m3x4_to_half(uint32_t w) {
+  const half2_t k256 = {(_Float16)256.0f, (_Float16)256.0f};
+  const half2_t a = __builtin_bit_cast(half2_t, ((w & 0x7fu) << 7) | ((w & 0x7f00u) << 15)) * k256;
+  const half2_t b = __builtin_bit_cast(half2_t, ((w & 0x7f0000u) >> 9) | ((w & 0x7f000000u) >> 1)) * k256;
+  const uint32_t sa = ((w & 0x80u) << 8) | ((w & 0x8000u) << 16);
+  const uint32_t sb = ((w & 0x800000u) >> 8) | (w & 0x80000000u);
+  return u32x2{__builtin_bit_cast(uint32_t, a) | sa, __builtin_bit_cast(uint32_t, b) | sb};
+}
+
 // fp16 hi / lo split of a (RNE both); hi + lo == a whenever a - hi is
 // representable (|a| >= 1/8), else within 2^-25.
 __device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
@@ -122,7 +136,8 @@ __device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(a - (float)hi);
 }
 
-template <int NB>
+// F8: residual values are E4M3 bytes (layout 3), else fp16 (layout 2).
+template <int NB, bool F8>
 __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
                                                           float* __restrict__ part) {
   using L = MLds<NB>;
@@ -377,7 +392,9 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       // residual words, then x at the salient columns.
       gi32* Sp = gptr(pr.S);
       gu16* xp = gptr(pr.x) + uint32_t(min(jr, B - 1)) * uint32_t(pr.K);
-      gu16* rvp = gptr(pr.rval) + uint32_t(tlc) * uint32_t(pr.nS) * 16u + 4u * uint32_t(jr >> 2);
+      // the lane's four values of a column: 8 bytes (fp16) or 4 (E4M3)
+      gu8* rvp = reinterpret_cast<gu8*>(gptr(pr.rval)) +
+                 (uint32_t(tlc) * uint32_t(pr.nS) * 16u + 4u * uint32_t(jr >> 2)) * (F8 ? 1u : 2u);
       gu32* rip = gptr(pr.ridx) + uint32_t(tlc) * uint32_t(pr.nS);
       const uint32_t psh = 8u * uint32_t(jr >> 2);
       const uint32_t bmask = (jr < B && jr < BP) ? 0xffffu : 0u;
@@ -389,7 +406,10 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
         for (int h = 0; h < 8; ++h) {
           const uint32_t sc = uint32_t(min(s0 + 8 * kb + h, s_hi - 1));
           col[h] = Sp[sc];
-          rv[h] = *reinterpret_cast<gu32x2*>(rvp + 16u * sc);
+          if constexpr (F8)
+            rv[h].x = *reinterpret_cast<gu32*>(rvp + 16u * sc);  // converted where used
+          else
+            rv[h] = *reinterpret_cast<gu32x2*>(rvp + 32u * sc);
           pw[h] = rip[sc];
         }
         uint16_t xb[8];
@@ -403,9 +423,10 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
           const uint32_t in = (s0 + 8 * kb + h < s_hi) ? 0xffffu : 0u;
           bx[h] = __builtin_bit_cast(_Float16, uint16_t(xb[h] & (in & bmask)));
           const uint32_t pwh = pw[h] >> psh;
+          const u32x2 hv = F8 ? e4m3x4_to_half(rv[h].x) : rv[h];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const uint32_t wd = q < 2 ? rv[h].x : rv[h].y;
+            const uint32_t wd = q < 2 ? hv.x : hv.y;
             const uint32_t val = (q & 1) ? wd >> 16 : wd & 0xffffu;
             const uint32_t hit = (((pwh >> (2 * q)) & 3u) == uint32_t(jr & 3)) ? in : 0u;
             ar[q][h] = __builtin_bit_cast(_Float16, uint16_t(val & hit));
@@ -457,16 +478,16 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   }
 }
 
-template <int NB>
+template <int NB, bool F8>
 hipError_t launch(const uint8_t* plan, int grid, float* part, hipStream_t st) {
   static bool done = false;
   if (!done) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_mma_kernel<NB>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_mma_kernel<NB, F8>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, MLds<NB>::BYTES);
     if (e != hipSuccess) return e;
     done = true;
   }
-  hipLaunchKernelGGL(grouped_mma_kernel<NB>, dim3(grid), dim3(kMT), MLds<NB>::BYTES, st, plan, part);
+  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8>), dim3(grid), dim3(kMT), MLds<NB>::BYTES, st, plan, part);
   return hipGetLastError();
 }
 
@@ -474,8 +495,9 @@ hipError_t launch(const uint8_t* plan, int grid, float* part, hipStream_t st) {
 
 int grouped_mma_rows_per_panel() { return kMRP; }
 
-hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, float* part, hipStream_t st) {
-  return batch <= 8 ? launch<1>(plan, grid, part, st) : launch<2>(plan, grid, part, st);
+hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8, float* part, hipStream_t st) {
+  if (f8) return batch <= 8 ? launch<1, true>(plan, grid, part, st) : launch<2, true>(plan, grid, part, st);
+  return batch <= 8 ? launch<1, false>(plan, grid, part, st) : launch<2, false>(plan, grid, part, st);
 }
 
 }  // namespace qtea_grouped

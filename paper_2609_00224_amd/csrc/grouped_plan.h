@@ -23,7 +23,7 @@ struct GProblem {
   const uint16_t* v;
   const int32_t* S;
   const int32_t* spos;
-  const uint16_t* rval;
+  const uint16_t* rval;  // fp16, or E4M3 bytes when the plan's f8 is set
   const uint32_t* ridx;
   const uint16_t* x;
   float* y;
@@ -38,6 +38,7 @@ struct GPlanHeader {
   uint32_t magic, version;
   int32_t n_problems, n_wg, rows_per_panel, max_parts, batch, n_chunks;
   int64_t n_units, off_chunks, n_grabs, off_splits, n_splits;
+  int32_t f8, reserved;  // residual values are E4M3 bytes (layout 3) in every problem
 };
 
 // A chunk: units [ub, ue), the first of them at (problem m, panel, slice).
@@ -95,7 +96,7 @@ constexpr int kAuxNT = 2;
 // Device-side launches of the low-batch kernels (grouped_mma.hip): the
 // persistent matrix-core kernel for 2 <= batch <= 16 over `grid`
 // workgroups, and its static shared-memory size.
-hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, float* part, hipStream_t st);
+hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8, float* part, hipStream_t st);
 int grouped_mma_rows_per_panel();
 
 }  // namespace qtea_grouped

@@ -1,7 +1,7 @@
 // Compressed ternary GEMV for gfx950: packing, the lookup-table GEMV and
 // the C ABI declared in include/qtea.h.
 //
-// Device layout (layout version 2), all regions 256-byte aligned:
+// Device layout (layout versions 2 and 3), all regions 256-byte aligned:
 //   header   256 B: magic, layout, sizes; a validation flag word at +128.
 //   trits    [n_pad/64 tiles][n_groups][64 rows][16 bytes]
 //            One 16-byte unit holds the sixteen packs of one 16-pack group
@@ -14,7 +14,8 @@
 //   v        fp16 [n_groups * 80]      (zero in the column padding)
 //   salient  int32 [n_salient]
 //   spos     int32 [n_groups + 1]      first s with S_s >= 80 * g
-//   rval     fp16 [n_pad/64][n_salient][16]  residual of four-row group g in salient
+//   rval     [n_pad/64][n_salient][16] fp16 (layout 2) or FP8 E4M3 bytes
+//            (layout 3): residual of four-row group g in salient
 //            column s at ((g / 16) * n_salient + s) * 16 + g % 16: the sixteen
 //            groups of a tile are contiguous per column, and a tile's residual
 //            over a run of salient columns is one contiguous run
@@ -87,18 +88,24 @@ __global__ void pack_trits_kernel(const int8_t* __restrict__ trits, int64_t N, i
   }
 }
 
+// Scales, salient list and residual blocks.  VT is the residual value type:
+// uint16_t (fp16 bits, layout 2) or uint8_t (E4M3 bytes, layout 3; a NaN code
+// is flagged).  With S == o_S the salient list is already in place (derived
+// from a bitmap) and only read.
+template <typename VT>
 __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint16_t* __restrict__ v,
-                                 const int32_t* __restrict__ S, const uint16_t* __restrict__ rval,
+                                 const int32_t* S, const VT* __restrict__ rval,
                                  const uint8_t* __restrict__ ridx, int64_t N, int64_t K, int64_t nS,
                                  int64_t n_pad, int64_t n_groups, uint16_t* __restrict__ o_alpha,
-                                 uint16_t* __restrict__ o_v, int32_t* __restrict__ o_S,
-                                 int32_t* __restrict__ o_spos, uint16_t* __restrict__ o_rval,
-                                 uint32_t* __restrict__ o_ridx) {
+                                 uint16_t* __restrict__ o_v, int32_t* o_S,
+                                 int32_t* __restrict__ o_spos, VT* __restrict__ o_rval,
+                                 uint32_t* __restrict__ o_ridx, uint32_t* __restrict__ flags) {
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
   const int64_t t0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   for (int64_t i = t0; i < n_pad; i += stride) o_alpha[i] = i < N ? alpha[i] : 0;
   for (int64_t i = t0; i < n_groups * kGroupCols; i += stride) o_v[i] = i < K ? v[i] : 0;
-  for (int64_t i = t0; i < nS; i += stride) o_S[i] = S[i];
+  if (S != o_S)
+    for (int64_t i = t0; i < nS; i += stride) o_S[i] = S[i];
   for (int64_t g = t0; g <= n_groups; g += stride) {
     // lower bound of 80 g in the sorted salient list
     int64_t lo = 0, hi = nS;
@@ -113,11 +120,15 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
     o_spos[g] = int32_t(lo);
   }
   const int64_t G = N / 4, Gp = n_pad / 4, Wp = n_pad / 64;
+  uint32_t f = 0;
   for (int64_t i = t0; i < nS * Gp; i += stride) {
     const int64_t tile = i / (16 * nS), rem = i - tile * 16 * nS;
     const int64_t s = rem >> 4, g = 16 * tile + (rem & 15);
-    o_rval[i] = g < G ? rval[s * G + g] : 0;
+    const VT val = g < G ? rval[s * G + g] : VT(0);
+    if (sizeof(VT) == 1 && e4m3_is_nan(val)) f |= kFlagBadResid;
+    o_rval[i] = val;
   }
+  if (f) atomicOr(flags, f);
   for (int64_t i = t0; i < nS * Wp; i += stride) {
     const int64_t w = i / nS, s = i % nS;
     uint32_t word = 0;
@@ -129,11 +140,58 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
   }
 }
 
-__global__ void write_header_kernel(uint8_t* packed, int64_t N, int64_t K, int64_t nS) {
+// Salient column list from a column bitmap (bit j % 32 of word j / 32 set
+// when column j is salient), ascending, by one workgroup: each thread counts
+// a contiguous run of words, a scan over the threads gives every run's first
+// list position.  A bit at or past K, or a count other than nS, is flagged
+// (and nothing is written).
+__global__ __launch_bounds__(1024) void bitmap_salient_kernel(const uint32_t* __restrict__ bitmap,
+                                                              int64_t K, int64_t nS,
+                                                              int32_t* __restrict__ o_S,
+                                                              uint32_t* __restrict__ flags) {
+  __shared__ int64_t run[1024];
+  const int t = threadIdx.x;
+  const int64_t nw = (K + 31) / 32, per = (nw + 1023) / 1024;
+  const int64_t w0 = min(nw, int64_t(t) * per), w1 = min(nw, w0 + per);
+  const uint32_t tail = (K & 31) ? (1u << (K & 31)) - 1u : 0xffffffffu;
+  uint32_t f = 0;
+  int64_t cnt = 0;
+  for (int64_t w = w0; w < w1; ++w) {
+    uint32_t b = bitmap[w];
+    if (w == nw - 1) {
+      if (b & ~tail) f |= kFlagBadResid;
+      b &= tail;
+    }
+    cnt += __popc(b);
+  }
+  run[t] = cnt;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {  // inclusive scan
+    const int64_t add = t >= off ? run[t - off] : 0;
+    __syncthreads();
+    run[t] += add;
+    __syncthreads();
+  }
+  if (run[1023] != nS) {
+    f |= kFlagBadResid;
+  } else {
+    int64_t pos = run[t] - cnt;
+    for (int64_t w = w0; w < w1; ++w) {
+      uint32_t b = bitmap[w] & (w == nw - 1 ? tail : 0xffffffffu);
+      while (b) {
+        o_S[pos++] = int32_t(32 * w + (__ffs(b) - 1));
+        b &= b - 1u;
+      }
+    }
+  }
+  if (f) atomicOr(flags, f);
+}
+
+__global__ void write_header_kernel(uint8_t* packed, int64_t N, int64_t K, int64_t nS, int layout) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     uint32_t* h = reinterpret_cast<uint32_t*>(packed);
     h[0] = QTEA_DESC_MAGIC;
-    h[1] = kLayout;
+    h[1] = uint32_t(layout);
     int64_t* h64 = reinterpret_cast<int64_t*>(packed + 8);
     h64[0] = N;
     h64[1] = K;
@@ -195,7 +253,7 @@ struct GemvArgs {
   const uint16_t* v;
   const int32_t* S;
   const int32_t* spos;
-  const uint16_t* rval;
+  const uint16_t* rval;  // fp16, or E4M3 bytes when f8
   const uint32_t* ridx;
   const uint16_t* x;
   float* y;
@@ -203,6 +261,7 @@ struct GemvArgs {
   uint32_t* counters;
   int64_t N, K, n_pad;
   int n_groups, n_tiles, nS;
+  int f8;  // residual values are E4M3 bytes (layout 3)
   int nrb, nslices, ks_groups;
 };
 
@@ -362,7 +421,9 @@ __global__ __launch_bounds__(kThreads) void lut_gemv_kernel(const GemvArgs p) {
         for (int j = 0; j < TPW; ++j) {
           const int64_t r = int64_t(tile[j]) * kTileRows + lane;
           r_word[j][u] = ok && valid[j] ? p.ridx[int64_t(tile[j]) * p.nS + s] : 0u;
-          r_val[j][u] = ok && valid[j] ? p.rval[rval_index(r >> 2, s, p.nS)] : uint16_t(0);
+          const int64_t vi = rval_index(r >> 2, s, p.nS);
+          r_val[j][u] = !(ok && valid[j]) ? uint16_t(0)
+                        : p.f8 ? e4m3_to_half_bits(reinterpret_cast<const uint8_t*>(p.rval)[vi]) : p.rval[vi];
         }
       }
     };
@@ -537,12 +598,13 @@ struct FkArgs {
   const uint16_t* v;
   const int32_t* S;
   const int32_t* spos;
-  const uint16_t* rval;
+  const uint16_t* rval;  // fp16, or E4M3 bytes when f8
   const uint32_t* ridx;
   const uint16_t* x;
   float* y;
   int64_t N, K, n_pad;
   int n_groups, nS;
+  int f8;  // residual values are E4M3 bytes (layout 3)
   int R;   // rows per workgroup (multiple of 16)
   int KS;  // waves per 16-row block (K parts)
   int CG;  // 16-pack groups per table chunk (multiple of 4)
@@ -684,7 +746,9 @@ __global__ __launch_bounds__(kFkMaxThreads) void fk_gemv_kernel(const FkArgs p) 
         const bool ok = row_ok && s < se;
         rs_col[u] = ok ? p.S[s] : -1;
         rs_word[u] = ok ? p.ridx[tile * p.nS + s] : 0u;
-        rs_val[u] = ok ? p.rval[rval_index(row >> 2, s, p.nS)] : uint16_t(0);
+        const int64_t vi = rval_index(row >> 2, s, p.nS);
+        rs_val[u] = !ok ? uint16_t(0)
+                    : p.f8 ? e4m3_to_half_bits(reinterpret_cast<const uint8_t*>(p.rval)[vi]) : p.rval[vi];
       }
     };
     load_res(0);
@@ -945,35 +1009,65 @@ int qtea_packed_bytes(int64_t N, int64_t K, int64_t n_salient, int64_t* out_byte
   return QTEA_OK;
 }
 
-int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
-              const uint16_t* col_rescale, const int32_t* salient, int64_t n_salient,
-              const uint16_t* resid_val, const uint8_t* resid_idx, void* packed,
-              int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
+int qtea_packed_bytes_e4m3(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes) {
+  Layout L;
+  if (!out_bytes || !make_layout(N, K, n_salient, &L, kLayoutE4M3)) return QTEA_ERR_INVALID_ARG;
+  *out_bytes = L.total;
+  return QTEA_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// The two pack entry points: layout 2 takes a salient list and fp16
+// residual values, layout 3 a salient bitmap and E4M3 residual bytes.
+int pack_any(int layout, const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
+             const uint16_t* col_rescale, const int32_t* salient, const uint32_t* bitmap,
+             int64_t n_salient, const void* resid_val, const uint8_t* resid_idx, void* packed,
+             int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
   Layout L;
   if (!out_desc) return QTEA_ERR_INVALID_ARG;
   out_desc->magic = 0;
-  if (!make_layout(N, K, n_salient, &L)) return QTEA_ERR_INVALID_ARG;
+  if (!make_layout(N, K, n_salient, &L, layout)) return QTEA_ERR_INVALID_ARG;
   if (!trits || !row_scale || !col_rescale || !packed) return QTEA_ERR_INVALID_ARG;
-  if (n_salient > 0 && (!salient || !resid_val || !resid_idx)) return QTEA_ERR_INVALID_ARG;
+  if (n_salient > 0 && (!resid_val || !resid_idx)) return QTEA_ERR_INVALID_ARG;
+  if (layout == kLayout ? (n_salient > 0 && !salient) : !bitmap) return QTEA_ERR_INVALID_ARG;
   if (packed_bytes < L.total) return QTEA_ERR_WORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* pk = static_cast<uint8_t*>(packed);
   uint32_t* flags = reinterpret_cast<uint32_t*>(pk + kFlagOffset);
+  int32_t* o_S = reinterpret_cast<int32_t*>(pk + L.off_salient);
 
-  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, st, pk, N, K, n_salient);
+  hipLaunchKernelGGL(write_header_kernel, dim3(1), dim3(64), 0, st, pk, N, K, n_salient, layout);
   const int64_t ni = n_salient * (N / 4);
+  // the salient list given is checked here; one derived from a bitmap is
+  // checked as it is derived
   hipLaunchKernelGGL(validate_kernel, dim3(grid_for(N * K, 256 * 16)), dim3(256), 0, st, trits, N * K,
-                     resid_idx, ni, salient, n_salient, K, flags);
+                     resid_idx, ni, layout == kLayout ? salient : nullptr,
+                     layout == kLayout ? n_salient : int64_t(0), K, flags);
+  if (layout == kLayoutE4M3) {
+    hipLaunchKernelGGL(bitmap_salient_kernel, dim3(1), dim3(1024), 0, st, bitmap, K, n_salient, o_S, flags);
+    salient = o_S;
+  }
   const int64_t n_units = L.n_tiles * L.n_groups * kTileRows;
   hipLaunchKernelGGL(pack_trits_kernel, dim3(grid_for(n_units)), dim3(256), 0, st, trits, N, K,
                      L.n_groups, n_units, pk + L.off_trits);
   const int64_t meta_n = L.n_pad + L.n_groups * kGroupCols + n_salient * (L.n_pad / 4);
-  hipLaunchKernelGGL(pack_meta_kernel, dim3(grid_for(meta_n)), dim3(256), 0, st, row_scale,
-                     col_rescale, salient, resid_val, resid_idx, N, K, n_salient, L.n_pad, L.n_groups,
-                     reinterpret_cast<uint16_t*>(pk + L.off_alpha),
-                     reinterpret_cast<uint16_t*>(pk + L.off_v), reinterpret_cast<int32_t*>(pk + L.off_salient),
-                     reinterpret_cast<int32_t*>(pk + L.off_spos), reinterpret_cast<uint16_t*>(pk + L.off_rval),
-                     reinterpret_cast<uint32_t*>(pk + L.off_ridx));
+  uint16_t* o_alpha = reinterpret_cast<uint16_t*>(pk + L.off_alpha);
+  uint16_t* o_v = reinterpret_cast<uint16_t*>(pk + L.off_v);
+  int32_t* o_spos = reinterpret_cast<int32_t*>(pk + L.off_spos);
+  uint32_t* o_ridx = reinterpret_cast<uint32_t*>(pk + L.off_ridx);
+  if (layout == kLayout)
+    hipLaunchKernelGGL(pack_meta_kernel<uint16_t>, dim3(grid_for(meta_n)), dim3(256), 0, st, row_scale,
+                       col_rescale, salient, static_cast<const uint16_t*>(resid_val), resid_idx, N, K,
+                       n_salient, L.n_pad, L.n_groups, o_alpha, o_v, o_S, o_spos,
+                       reinterpret_cast<uint16_t*>(pk + L.off_rval), o_ridx, flags);
+  else
+    hipLaunchKernelGGL(pack_meta_kernel<uint8_t>, dim3(grid_for(meta_n)), dim3(256), 0, st, row_scale,
+                       col_rescale, salient, static_cast<const uint8_t*>(resid_val), resid_idx, N, K,
+                       n_salient, L.n_pad, L.n_groups, o_alpha, o_v, o_S, o_spos, pk + L.off_rval, o_ridx,
+                       flags);
   if (hipGetLastError() != hipSuccess) return QTEA_ERR_HIP;
   uint32_t hflags = 0;
   if (hipMemcpyAsync(&hflags, flags, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return QTEA_ERR_HIP;
@@ -983,7 +1077,7 @@ int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_sca
 
   qtea_desc d;
   d.magic = QTEA_DESC_MAGIC;
-  d.layout = kLayout;
+  d.layout = uint32_t(layout);
   d.N = N;
   d.K = K;
   d.n_salient = n_salient;
@@ -1000,6 +1094,26 @@ int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_sca
   d.off_ridx = L.off_ridx;
   *out_desc = d;
   return QTEA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
+              const uint16_t* col_rescale, const int32_t* salient, int64_t n_salient,
+              const uint16_t* resid_val, const uint8_t* resid_idx, void* packed,
+              int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
+  return pack_any(kLayout, trits, N, K, row_scale, col_rescale, salient, nullptr, n_salient, resid_val,
+                  resid_idx, packed, packed_bytes, out_desc, stream);
+}
+
+int qtea_pack_e4m3(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
+                   const uint16_t* col_rescale, const uint32_t* salient_bitmap, int64_t n_salient,
+                   const uint8_t* resid_val, const uint8_t* resid_idx, void* packed, int64_t packed_bytes,
+                   qtea_desc* out_desc, void* stream) {
+  return pack_any(kLayoutE4M3, trits, N, K, row_scale, col_rescale, nullptr, salient_bitmap, n_salient,
+                  resid_val, resid_idx, packed, packed_bytes, out_desc, stream);
 }
 
 int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes) {
@@ -1047,6 +1161,7 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
   a.n_groups = int(d.n_groups);
   a.n_tiles = int(d.n_pad / kTileRows);
   a.nS = int(d.n_salient);
+  a.f8 = d.layout == kLayoutE4M3;
   a.nrb = pl.nrb;
   a.nslices = pl.nslices;
   a.ks_groups = pl.ks_groups;
@@ -1067,6 +1182,7 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
     k.n_pad = a.n_pad;
     k.n_groups = a.n_groups;
     k.nS = a.nS;
+    k.f8 = a.f8;
     k.R = f.R;
     k.KS = f.KS;
     k.CG = f.CG;

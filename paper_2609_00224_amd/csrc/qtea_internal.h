@@ -1,6 +1,6 @@
 // Internal definitions shared by the library's translation units: layout
-// constants, the device layout arithmetic (layout version 2) and small
-// device helpers.  Not part of the public ABI.
+// constants, the device layout arithmetic (layout versions 2 and 3) and
+// small device helpers.  Not part of the public ABI.
 #ifndef QTEA_INTERNAL_H_
 #define QTEA_INTERNAL_H_
 
@@ -19,13 +19,36 @@ constexpr int kCodes = 243;      // 3^5
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr uint32_t kZeroCode4 = 0x79797979u;  // four copies of code 121 (all-zero trits)
-constexpr int kLayout = 2;
+constexpr int kLayout = 2;      // residual values fp16
+constexpr int kLayoutE4M3 = 3;  // residual values FP8 E4M3 (one byte each)
 constexpr int64_t kAlign = 256;
 constexpr int64_t kHeaderBytes = 256;
 constexpr int kFlagOffset = 128;
 
 constexpr uint32_t kFlagBadTrit = 1u;
 constexpr uint32_t kFlagBadResid = 2u;
+
+// FP8 E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa bits, no
+// infinities; exponent and mantissa all ones is NaN) to the fp16 bits of the
+// same value.  Every finite E4M3 value is an fp16 value: normal values keep
+// their mantissa and move the exponent bias from 7 to 15; a subnormal m 2^-9
+// (m = 1..7) is normal in fp16.
+__host__ __device__ __forceinline__ uint16_t e4m3_to_half_bits(uint32_t b) {
+  const uint32_t s = (b & 0x80u) << 8, e = (b >> 3) & 15u, m = b & 7u;
+  if (e) return uint16_t(s | ((e + 8u) << 10) | (m << 7));
+  if (!m) return uint16_t(s);
+  const uint32_t p = m >= 4u ? 2u : (m >= 2u ? 1u : 0u);  // floor(log2 m)
+  return uint16_t(s | ((p + 6u) << 10) | ((m << (10u - p)) & 0x3ffu));
+}
+__host__ __device__ __forceinline__ bool e4m3_is_nan(uint32_t b) { return (b & 0x7fu) == 0x7fu; }
+// The same value as fp32: a normal code moves its exponent bias from 7 to
+// 127; a subnormal one is m 2^-9 (exact).
+__device__ __forceinline__ float e4m3_to_float(uint32_t b) {
+  const uint32_t sgn = (b & 0x80u) << 24, e = (b >> 3) & 15u, m = b & 7u;
+  const float nrm = __uint_as_float(sgn | ((e + 120u) << 23) | (m << 20));
+  const float sub = __uint_as_float(sgn | __float_as_uint(float(m) * 0x1p-9f));
+  return e ? nrm : sub;
+}
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -53,12 +76,15 @@ __device__ __forceinline__ float h2f(uint16_t h) {
 // Layout arithmetic shared by the host entry points.
 // ---------------------------------------------------------------------------
 struct Layout {
+  int64_t value_bytes;  // bytes per residual value: 2 (fp16, layout 2) or 1 (E4M3, layout 3)
   int64_t n_packs, n_groups, n_pad, n_tiles;
   int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx, total;
 };
 
-inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L) {
+inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L, int layout = kLayout) {
   if (N < 4 || N % 4 != 0 || K < 1 || nS < 0 || nS > K) return false;
+  if (layout != kLayout && layout != kLayoutE4M3) return false;
+  L->value_bytes = layout == kLayoutE4M3 ? 1 : 2;
   if (N > (int64_t(1) << 31) - 64 || K > (int64_t(1) << 31) - 80) return false;
   L->n_packs = cdiv(K, 5);
   L->n_groups = cdiv(L->n_packs, kGroupPacks);
@@ -76,7 +102,7 @@ inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L) {
   L->off_spos = o;
   o = align_up(o + 4 * (L->n_groups + 1), kAlign);
   L->off_rval = o;
-  o = align_up(o + 2 * nS * (L->n_pad / 4), kAlign);
+  o = align_up(o + L->value_bytes * nS * (L->n_pad / 4), kAlign);
   L->off_ridx = o;
   o = align_up(o + 4 * nS * (L->n_pad / 64), kAlign);
   L->total = o;
@@ -84,9 +110,9 @@ inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L) {
 }
 
 inline bool desc_ok(const qtea_desc* d) {
-  if (!d || d->magic != QTEA_DESC_MAGIC || d->layout != kLayout) return false;
+  if (!d || d->magic != QTEA_DESC_MAGIC) return false;
   Layout L;
-  if (!make_layout(d->N, d->K, d->n_salient, &L)) return false;
+  if (!make_layout(d->N, d->K, d->n_salient, &L, int(d->layout))) return false;
   return L.total == d->bytes_total && L.off_trits == d->off_trits && L.off_alpha == d->off_alpha &&
          L.off_v == d->off_v && L.off_salient == d->off_salient && L.off_spos == d->off_spos &&
          L.off_rval == d->off_rval && L.off_ridx == d->off_ridx && L.n_pad == d->n_pad &&

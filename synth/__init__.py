@@ -17,7 +17,10 @@ available; shapes follow Llama-3-8B, Qwen3-14B and Llama-3-70B linears):
   * |S| = floor(f * K + 1/2) columns chosen uniformly without replacement,
     sorted ascending;
   * one residual per (salient column, group of 4 consecutive output rows), at
-    a uniformly drawn position 0..3 in the group.
+    a uniformly drawn position 0..3 in the group;
+  * for the paper's residual storage (resid="e4m3"): the same R draw rounded
+    to FP8 E4M3 (RNE, by torch's float8_e4m3fn conversion) and given as
+    codes, and the salient set given as a column bitmap.
 """
 from __future__ import annotations
 
@@ -141,13 +144,31 @@ def normal_f16(k: int, n: int, mu: float, sigma: float) -> np.ndarray:
     return d.astype(np.float16)
 
 
+def normal_e4m3(k: int, n: int, mu: float, sigma: float) -> np.ndarray:
+    """FP8 E4M3 codes (uint8) of float64 normal draws, rounded to nearest even."""
+    import torch
+
+    d = np.empty(n, dtype=np.float64)
+    _L().synth_normal(k, n, mu, sigma, d.ctypes.data)
+    return torch.from_numpy(d).to(torch.float8_e4m3fn).view(torch.uint8).numpy().copy()
+
+
+def column_bitmap(S, K: int) -> np.ndarray:
+    """int32 [ceil(K/32)] words, bit j % 32 of word j / 32 set for j in S."""
+    w = np.zeros((K + 31) // 32, dtype=np.uint32)
+    S = np.asarray(S, dtype=np.int64)
+    np.bitwise_or.at(w, S // 32, (np.uint32(1) << (S % 32).astype(np.uint32)))
+    return w.view(np.int32)
+
+
 def layer_inputs(seed, layer, mat, N, K, p0=Fraction(2, 5), frac=Fraction(2, 100),
-                 with_trits=True, rows=None) -> dict:
+                 with_trits=True, rows=None, resid="fp16") -> dict:
     """All non-activation inputs of one compressed N x K matrix.
 
     Returns numpy arrays: trits int8 [N][K] (omitted if with_trits is False),
     alpha fp16 [N], v fp16 [K], S int32 [nS] (sorted), R fp16 [nS][N/4],
-    idx uint8 [nS][N/4].
+    idx uint8 [nS][N/4]; with resid="e4m3" R is replaced by R8, uint8 E4M3
+    codes [nS][N/4], and bitmap, int32 [ceil(K/32)], is added.
     """
     if N % 4:
         raise ValueError("N must be a multiple of 4 (1:4 residual groups)")
@@ -166,9 +187,15 @@ def layer_inputs(seed, layer, mat, N, K, p0=Fraction(2, 5), frac=Fraction(2, 100
         "alpha": uniform_f16(key(seed, layer, mat, FIELD_ALPHA), N, 0.01, 0.03),
         "v": uniform_f16(key(seed, layer, mat, FIELD_V), K, 0.8, 1.2),
         "S": S,
-        "R": normal_f16(key(seed, layer, mat, FIELD_RVAL), nS * G, 0.0, 0.01).reshape(nS, G),
         "idx": idx.reshape(nS, G),
     }
+    if resid == "e4m3":
+        out["R8"] = normal_e4m3(key(seed, layer, mat, FIELD_RVAL), nS * G, 0.0, 0.01).reshape(nS, G)
+        out["bitmap"] = column_bitmap(S, K)
+    elif resid == "fp16":
+        out["R"] = normal_f16(key(seed, layer, mat, FIELD_RVAL), nS * G, 0.0, 0.01).reshape(nS, G)
+    else:
+        raise ValueError(f"unknown residual storage {resid!r}")
     if with_trits:
         out["trits"] = trits(seed, layer, mat, N, K, p0, rows=rows)
     return out

@@ -19,6 +19,7 @@ class Workload:
     p0: Fraction = Fraction(2, 5)
     frac: Fraction = Fraction(2, 100)
     note: str = ""
+    resid: str = "fp16"  # residual value storage: "fp16" or "e4m3"
 
     def matrices(self):
         """Yield (layer, mat, role, N, K) in per-token execution order."""
@@ -44,6 +45,11 @@ WORKLOADS = {
     "llama3_70b_stack": Workload("llama3_70b_stack", LLAMA3_70B, 80, (1, 16),
                                  p0=Fraction(1, 2),
                                  note="80-layer Llama-3-70B-shaped linear stack, P(0)=0.5"),
+    # the paper's evaluation storage: 5% salient columns, FP8 E4M3 residual
+    # values, a column bitmap (1.7 bits per weight in its accounting)
+    "llama3_8b_stack_e4m3": Workload("llama3_8b_stack_e4m3", LLAMA3_8B, 32, (1, 4),
+                                     frac=Fraction(5, 100), resid="e4m3",
+                                     note="32-layer Llama-3-8B-shaped stack, 5% salient, E4M3 residual"),
 }
 
 ORDER = ["gemv_4096x4096", "llama3_8b_layer", "llama3_8b_stack", "qwen3_14b_stack", "llama3_70b_stack"]

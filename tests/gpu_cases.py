@@ -164,3 +164,37 @@ def assert_close(y_gpu, y_ref, x, wmax, what=""):
         bad = np.nonzero(d > bound)[0]
         assert bad.size == 0, (f"{what}: batch {b} row bound exceeded at {bad[:5]} "
                                f"err {d[bad[:5]]} bound {bound[bad[:5]]}")
+
+
+# ---------------------------------------------------------------------------
+# The paper's residual storage: FP8 E4M3 values, salient column bitmap.
+# ---------------------------------------------------------------------------
+def e4m3_dyadic_case(seed, N, K, B, nS):
+    """dyadic_case with E4M3 residual codes of exponent field 4..9: values
+    (1 + m/8) 2^(e-7) are multiples of 2^-6 below 8, so every product with x
+    and every partial sum stays exact in fp32 and the GPU result equals the
+    oracle's bit for bit."""
+    c = dyadic_case(seed, N, K, B, nS)
+    rng = np.random.default_rng(seed + 7)
+    shape = (nS, N // 4)
+    sgn, e, m = rng.integers(0, 2, shape), rng.integers(4, 10, shape), rng.integers(0, 8, shape)
+    c["R8"] = ((sgn << 7) | (e << 3) | m).astype(np.uint8)
+    c["R"] = oracle.e4m3_as_half(c["R8"])
+    return c
+
+
+def e4m3_synth_case(seed, N, K, B, frac=Fraction(5, 100), layer=0, mat=0):
+    """Synthetic inputs with E4M3 residual codes (the N(0, 0.01) draw rounded:
+    mostly subnormal codes) on a fraction frac of the columns."""
+    L = synth.layer_inputs(seed, layer, mat, N, K, frac=frac, resid="e4m3")
+    L["R"] = oracle.e4m3_as_half(L["R8"])
+    L["x"] = synth.activations(seed, layer, mat, B, K)
+    return L
+
+
+def gpu_pack_e4m3(case, dev="cuda"):
+    import paper_2609_00224_amd as q
+
+    return q.pack_matrix_e4m3(to_dev(case["trits"], dev), to_dev(case["alpha"], dev), to_dev(case["v"], dev),
+                              to_dev(synth.column_bitmap(case["S"], case["K"]), dev), int(case["S"].size),
+                              to_dev(case["R8"], dev), to_dev(case["idx"], dev))

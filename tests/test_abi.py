@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert q.qtea_abi_version() == 2
+    assert q.qtea_abi_version() == 3
     assert q.qtea_status_string(0) == "ok"
     for s in range(-6, 0):
         assert q.qtea_status_string(s) != "unknown status"
@@ -75,3 +75,27 @@ def test_invalid_descriptor_rejected_on_host(lib):
 def test_algorithmic_bytes_matches_oracle():
     for N, K, nS in [(4096, 4096, 82), (8192, 28672, 573), (4, 1, 0), (12, 37, 5)]:
         assert q.algorithmic_bytes(N, K, nS) == oracle.algorithmic_bytes(N, K, nS)
+
+
+def test_e4m3_packed_bytes_and_host_checks(lib):
+    for N, K, nS in [(4096, 4096, 205), (64, 5, 1), (12, 37, 0)]:
+        n8, n16 = q.qtea_packed_bytes_e4m3(N, K, nS), q.qtea_packed_bytes(N, K, nS)
+        assert n8 % 256 == 0 and n8 <= n16
+    with pytest.raises(q.QteaError) as e:
+        q.qtea_packed_bytes_e4m3(6, 10, 0)
+    assert e.value.status == q.QTEA_ERR_INVALID_ARG
+    dd = q.QteaDesc()
+    assert lib.qtea_pack_e4m3(None, 4, 4, None, None, None, 0, None, None, None, 0, ctypes.byref(dd),
+                              None) == q.QTEA_ERR_INVALID_ARG
+    assert dd.magic == 0
+
+
+def test_grouped_info_mirror_size():
+    # 8 + 2 int32 fields, then three int64 fields
+    assert ctypes.sizeof(q.QteaGroupedInfo) == 64
+    assert q.QteaGroupedInfo.n_units.offset == 40
+
+
+def test_algorithmic_bytes_e4m3_matches_oracle():
+    for N, K, nS in [(4096, 4096, 205), (8192, 28672, 1434), (4, 1, 0)]:
+        assert q.algorithmic_bytes(N, K, nS, value_bytes=1) == oracle.algorithmic_bytes_vb(N, K, nS, 1)

@@ -334,3 +334,72 @@ def test_bits_per_weight_full_accounting():
 ])
 def test_algorithmic_bytes_per_shape(N, K, nS, expect):
     assert oracle.algorithmic_bytes(N, K, nS) == expect
+
+
+# ---------------------------------------------------------------------------
+# The paper's residual storage: FP8 E4M3 values and a salient column bitmap.
+# ---------------------------------------------------------------------------
+def test_e4m3_matches_library_routine_all_codes():
+    """All 256 codes against torch's float8_e4m3fn (an independent
+    implementation of the same OCP format)."""
+    import torch
+
+    codes = np.arange(256, dtype=np.uint8)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = oracle.e4m3_decode(codes)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert set(np.flatnonzero(nan)) == {0x7F, 0xFF}
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def test_e4m3_closed_forms():
+    f = oracle.e4m3_to_double
+    assert f(0x00) == 0.0 and math.copysign(1.0, f(0x80)) == -1.0
+    assert f(0x38) == 1.0          # exponent field 7 = bias: 2^0
+    assert f(0x3C) == 1.5          # mantissa 4/8
+    assert f(0x7E) == 448.0        # largest finite: 1.75 * 2^8
+    assert f(0x08) == 2.0 ** -6    # smallest normal
+    assert f(0x01) == 2.0 ** -9    # smallest subnormal: 1/8 * 2^-6
+    assert f(0x07) == 7 * 2.0 ** -9
+    assert f(0xB8) == -1.0
+
+
+def test_e4m3_order_sign_and_fp16_exactness():
+    pos = oracle.e4m3_decode(np.arange(0x7F, dtype=np.uint8))  # 0x00..0x7e, finite
+    assert np.all(np.diff(pos) > 0)  # strictly increasing with the code
+    neg = oracle.e4m3_decode(np.arange(0x80, 0xFF, dtype=np.uint8))
+    assert np.array_equal(neg, -pos)
+    # every finite value is an fp16 value
+    h = oracle.e4m3_as_half(np.arange(0x7F, dtype=np.uint8))
+    assert np.array_equal(h.astype(np.float64), pos)
+    with pytest.raises(oracle.OracleError):
+        oracle.e4m3_as_half(np.array([0x7F], dtype=np.uint8))
+
+
+@pytest.mark.parametrize("K", [1, 31, 32, 33, 100, 4096, 14337])
+def test_bitmap_to_list_brute_force(K):
+    rng = np.random.default_rng(K)
+    S = np.sort(rng.choice(K, size=max(1, K // 20), replace=False)).astype(np.int32)
+    words = np.zeros((K + 31) // 32, dtype=np.uint32)
+    for j in S:  # brute force, one bit at a time
+        words[j // 32] |= np.uint32(1) << np.uint32(j % 32)
+    assert np.array_equal(oracle.bitmap_to_list(words, K), S)
+    assert np.array_equal(oracle.bitmap_to_list(np.zeros_like(words), K), np.zeros(0, np.int32))
+
+
+def test_bitmap_bit_past_K_rejected():
+    with pytest.raises(oracle.OracleError):
+        oracle.bitmap_to_list(np.array([1 << 5], dtype=np.uint32), 5)
+    assert np.array_equal(oracle.bitmap_to_list(np.array([1 << 4], dtype=np.uint32), 5), [4])
+
+
+def test_e4m3_storage_bytes():
+    # one byte per value instead of two: the residual value bytes halve
+    for N, K, nS in [(4096, 4096, 205), (28672, 4096, 205), (4096, 14336, 717)]:
+        b16, b8 = oracle.algorithmic_bytes_vb(N, K, nS, 2), oracle.algorithmic_bytes_vb(N, K, nS, 1)
+        assert b16 == oracle.algorithmic_bytes(N, K, nS)
+        assert b16 - b8 == (N // 4) * nS
+    # the paper's setting: 5% of columns, 8-bit values, one per four entries
+    assert oracle.bpw_paper(0.05, 8) == pytest.approx(1.7, abs=1e-12)

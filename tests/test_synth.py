@@ -68,10 +68,35 @@ def test_layer_inputs_shapes_and_ranges():
     assert abs(x.mean()) < 0.05 and abs(x.std() - 1.0) < 0.05
 
 
+def st_shapes():
+    return WORKLOADS["llama3_8b_stack"].shapes
+
+
 def test_workload_table():
     assert [w for w in WORKLOADS] == ["gemv_4096x4096", "llama3_8b_layer", "llama3_8b_stack",
-                                      "qwen3_14b_stack", "llama3_70b_stack"]
+                                      "qwen3_14b_stack", "llama3_70b_stack", "llama3_8b_stack_e4m3"]
+    e8 = WORKLOADS["llama3_8b_stack_e4m3"]
+    assert e8.resid == "e4m3" and e8.frac == Fraction(5, 100) and e8.shapes == st_shapes()
+    assert all(WORKLOADS[n].resid == "fp16" for n in list(WORKLOADS)[:5])
     st = WORKLOADS["llama3_8b_stack"]
     assert st.layers == 32 and len(list(st.matrices())) == 128
     assert WORKLOADS["llama3_70b_stack"].p0 == Fraction(1, 2)
     assert WORKLOADS["qwen3_14b_stack"].frac == Fraction(3, 100)
+
+
+def test_e4m3_residual_inputs():
+    import oracle
+
+    L = synth.layer_inputs(3, 1, 2, 256, 4096, frac=Fraction(5, 100), resid="e4m3")
+    nS = synth.n_salient(4096, Fraction(5, 100))
+    assert nS == 205 and L["S"].size == nS and "R" not in L
+    assert L["R8"].dtype == np.uint8 and L["R8"].shape == (nS, 64)
+    assert not np.any((L["R8"] & 0x7F) == 0x7F)  # no NaN codes
+    assert L["bitmap"].dtype == np.int32 and L["bitmap"].size == 128
+    assert np.array_equal(oracle.bitmap_to_list(L["bitmap"], 4096), L["S"])
+    # the codes are the fp64 draw rounded to E4M3: within half an E4M3 step
+    # of the fp16 rounding of the same draw
+    R16 = synth.layer_inputs(3, 1, 2, 256, 4096, frac=Fraction(5, 100))["R"].astype(np.float64)
+    R8 = oracle.e4m3_decode(L["R8"])
+    step = np.maximum(2.0 ** (np.floor(np.log2(np.maximum(np.abs(R16), 2.0 ** -6))) - 3), 2.0 ** -9)
+    assert np.all(np.abs(R8 - R16) <= 0.5 * step + 2.0 ** -12)
