@@ -50,7 +50,10 @@ constexpr int kGT = 512;                                  // threads per workgro
 constexpr int kGW = kGT / 64;                             // waves per workgroup
 constexpr int kWgPerCu = 2;                               // workgroups sharing a CU
 constexpr int kTabBytes = kCodes * 256;                   // 62,208: code row = 64 packs x 4 bytes
-constexpr int kResCols = 16;  // salient columns of a slice staged per wave (more: direct loads)
+// salient columns of a slice staged per wave (more: direct loads): fp16
+// values fill the wave's 1 KiB value area at 16 columns, E4M3 values at 32
+constexpr int kResCols = 16;
+constexpr int kResCols8 = 32;
 static_assert(kSlicePacks * 4 == 256, "one table row of 256 bytes per code");
 
 static_assert(kSliceCols % 64 == 0, "staging by whole waves");
@@ -67,13 +70,14 @@ struct GLds {
   static constexpr int ST = kTabBytes;                    // two buffers: a_j fp32 [320], x_j fp32 [320]
   static constexpr int STB = 8 * kSliceCols;              // bytes of one buffer
   static constexpr int RR = ST + 2 * STB;                 // residual row sums, fp32 [RP]
-  static constexpr int RV = RR + 4 * RP;                  // per wave: fp16 values [TPW][kResCols][16]
+  static constexpr int RV = RR + 4 * RP;                  // per wave: values [TPW][16 fp16 or 32 E4M3 columns][16]
   static constexpr int RI = RV + kGW * 1024;              // per wave: u32 positions [2][16], fp32 x [32]
   static constexpr int FLAG = RI + kGW * 256;             // one int
   static constexpr int BYTES = FLAG + 16;
 };
 static_assert(GLds<4>::TPW == 1 && GLds<8>::TPW == 2, "one or two tiles per wave");
-static_assert(2 * kResCols * 32 == 1024, "one 16-byte load per lane stages two tiles' values");
+static_assert(2 * kResCols * 32 == 1024 && 2 * kResCols8 * 16 == 1024,
+              "one 16-byte load per lane stages two tiles' values");
 static_assert(kWgPerCu * GLds<8>::BYTES <= 160 * 1024, "two workgroups per CU");
 
 
@@ -162,27 +166,28 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       al[i] = gptr(pr.alpha)[rowq < np ? rowq : np - 1];
     }
   };
-  // salient residual of unit c: this wave's tiles over the slice's first
-  // kResCols salient columns, fetched as two loads per lane and staged in
-  // the wave's LDS area in the residual phase.  rvq: 16 bytes of a tile's
-  // value run (fp16: 32 bytes per column, lanes 0..31 the first tile, 32..63
-  // the second; E4M3: 16 bytes per column, lanes 0..15 and 16..31, the upper
-  // half-wave repeating them); ris: lanes 0..31 the position words of the
-  // tiles (16 per tile), lanes 32..63 the salient column indices.  Indices
-  // are clamped into their regions (without salient columns both read the
-  // row scales).
+  // salient residual of unit c: this wave's tiles over the slice's first RC
+  // salient columns, fetched as two loads per lane (three for E4M3) and
+  // staged in the wave's LDS area in the residual phase.  rvq: 16 bytes of a
+  // tile's value run (lanes 0..31 the first tile, 32..63 the second; fp16:
+  // 32 bytes per column, 16 columns; E4M3: 16 bytes per column, 32 columns);
+  // ris: lanes 0..31 the position words of the tiles (16 columns per tile),
+  // lanes 32..63 the salient column indices; ris2 (E4M3): the same for
+  // columns 16..31.  Indices are clamped into their regions (without salient
+  // columns all read the row scales).
+  constexpr int RC = F8 ? kResCols8 : kResCols;
   u32x4 rvq;
-  uint32_t ris;
+  uint32_t ris, ris2 = 0;
   auto load_res = [&](const Cursor c, const int s_lo, const int s_hi) {
     const GProblem& pr = P[c.m];
     const bool any = pr.nS > 0;
     const uint32_t nS = uint32_t(pr.nS), n_tiles = uint32_t(pr.n_pad >> 6);
     const uint32_t tile0 = uint32_t(c.panel * TPP + w * TPW);
     constexpr uint32_t VB = F8 ? 16u : 32u;  // value bytes per (tile, salient column)
-    const uint32_t Tv = min(tile0 + (TPW == 2 ? uint32_t(F8 ? (lane >> 4) & 1 : lane >> 5) : 0u), n_tiles - 1u);
-    const uint32_t ncs = uint32_t(min(s_hi - s_lo, kResCols));
+    const uint32_t Tv = min(tile0 + (TPW == 2 ? uint32_t(lane >> 5) : 0u), n_tiles - 1u);
+    const uint32_t ncs = uint32_t(min(s_hi - s_lo, RC));
     const uint32_t len = ncs * VB;
-    const uint32_t lofs = min(uint32_t(lane & (F8 ? 15 : 31)) * 16u, len >= 16u ? len - 16u : 0u);
+    const uint32_t lofs = min(uint32_t(lane & 31) * 16u, len >= 16u ? len - 16u : 0u);
     const uint32_t vofs = any ? min((Tv * nS + uint32_t(s_lo)) * VB + lofs, n_tiles * nS * VB - 16u) : 0u;
     rvq = *reinterpret_cast<const gu32x4*>(
         (any ? reinterpret_cast<gu8*>(gptr(pr.rval)) : reinterpret_cast<gu8*>(gptr(pr.alpha))) + vofs);
@@ -191,6 +196,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     gu32* ib = !any ? reinterpret_cast<gu32*>(gptr(pr.alpha))
                     : (lane < 32 ? gptr(pr.ridx) + Ti * nS : reinterpret_cast<gu32*>(gptr(pr.S)));
     ris = ib[sc];
+    if constexpr (F8) ris2 = ib[any ? min(uint32_t(s_lo) + 16u + uint32_t(lane & 15), nS - 1u) : 0u];
   };
   // salient range [spos[g0], spos[g1]) of unit c's groups, as a vector load
   // (lane 0 reads the first bound, the other lanes the second): a scalar load
@@ -392,20 +398,33 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       const uint32_t xw = __float_as_uint(xr_lds[xc >= 0 && xc < kSliceCols ? xc : 0]);
       ri_w[lane] = lane < 32 ? ris : xw;
       asm volatile("" ::: "memory");
-      const int nc = grow_ok ? (ncol < kResCols ? ncol : kResCols) : 0;
-      for (int c = rq; c < nc; c += QR) {
-        const float rv = F8 ? e4m3_to_float(reinterpret_cast<const uint8_t*>(rv_w)[256 * rtile + 16 * c + g16])
-                            : h2f(reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16]);
-        const uint32_t idx = (ri_w[16 * rtile + c] >> gsh) & 3u;
-        const float xv = __uint_as_float(ri_w[32 + c]);
-        const float t = rv * xv;
+      const int nc = grow_ok ? (ncol < RC ? ncol : RC) : 0;
+      // columns [c0, c1) with their position words and activations at ri_w
+      // (value rows of 512 bytes per tile: 32 bytes per fp16 column, 16 per E4M3 one)
+      auto columns = [&](int c0, int c1) {
+        for (int c = c0 + rq; c < c1; c += QR) {
+          const float rv = F8 ? e4m3_to_float(reinterpret_cast<const uint8_t*>(rv_w)[512 * rtile + 16 * c + g16])
+                              : h2f(reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16]);
+          const uint32_t idx = (ri_w[16 * rtile + c - c0] >> gsh) & 3u;
+          const float xv = __uint_as_float(ri_w[32 + c - c0]);
+          const float t = rv * xv;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+          for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+        }
+      };
+      columns(0, nc < 16 ? nc : 16);
+      if (F8 && ncol > 16) {  // uniform: columns 16..31 through the same words area
+        asm volatile("" ::: "memory");  // after the reads above (same wave: in order)
+        const int xc2 = int(ris2) - col0;
+        const uint32_t xw2 = __float_as_uint(xr_lds[xc2 >= 0 && xc2 < kSliceCols ? xc2 : 0]);
+        ri_w[lane] = lane < 32 ? ris2 : xw2;
+        asm volatile("" ::: "memory");
+        columns(16, nc);
       }
     }
-    if (ncol > kResCols) {  // a slice with many salient columns (uniform branch)
+    if (ncol > RC) {  // a slice with many salient columns (uniform branch)
       const int64_t T = int64_t(grow >> 4);
-      for (int s = s_lo + kResCols + rq; s < s_hi; s += QR) {
+      for (int s = s_lo + RC + rq; s < s_hi; s += QR) {
         if (grow_ok) {
           const int64_t vi = rval_index(grow, s, pr.nS);
           const float rv = F8 ? e4m3_to_float(reinterpret_cast<gu8*>(gptr(pr.rval))[vi]) : h2f(gptr(pr.rval)[vi]);

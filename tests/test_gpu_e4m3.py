@@ -8,6 +8,8 @@ codes); the same values stored as fp16 give bit-identical outputs; invalid
 inputs are rejected."""
 from __future__ import annotations
 
+from fractions import Fraction
+
 import numpy as np
 import pytest
 
@@ -160,3 +162,18 @@ def test_e4m3_pack_errors():
     with pytest.raises(q.QteaError) as e:
         q.plan_grouped([a, b], [x, x], [y1, y2], batch=1)
     assert e.value.status == q.QTEA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("frac", [Fraction(12, 100), Fraction(25, 100)])
+def test_e4m3_dense_salient_grouped(frac):
+    """Slices with more than 16 and more than 32 salient columns (the staged
+    and the direct-load residual paths of the batch-1 kernel)."""
+    for B in (1, 4):
+        shapes = [(4096, 4096), (1024, 3000)]
+        cases = [e4m3_synth_case(21, N, K, B, frac=frac, mat=i) for i, (N, K) in enumerate(shapes)]
+        _report(f"grouped dense salient frac={frac} B={B}")
+        ys, _ = _grouped([gpu_pack_e4m3(c) for c in cases], cases, B)
+        for c, y in zip(cases, ys):
+            ref, wmax = oracle_rows(c)
+            assert_close(y, ref, c["x"], wmax, f"e4m3 frac={frac} B={B}")
+            assert_precise(y, ref, f"e4m3 frac={frac} B={B}")
