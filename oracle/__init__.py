@@ -90,6 +90,16 @@ def _L():
         lib.or_bitmap_to_list.argtypes = [vp, i64, vp, i64]
         lib.or_algorithmic_bytes_vb.restype = i64
         lib.or_algorithmic_bytes_vb.argtypes = [i64, i64, i64, i64]
+        lib.or_num_groups128.restype = i64
+        lib.or_num_groups128.argtypes = [i64]
+        lib.or_pack128.restype = i32
+        lib.or_pack128.argtypes = [vp, i64, i64, vp]
+        lib.or_unpack128.restype = i32
+        lib.or_unpack128.argtypes = [vp, i64, i64, vp]
+        lib.or_gemv128_rows.restype = i32
+        lib.or_gemv128_rows.argtypes = [i64, i64, vp, vp, i64, vp, vp, vp, vp, i64, vp, vp, vp, i64, vp, i32]
+        lib.or_algorithmic_bytes128.restype = i64
+        lib.or_algorithmic_bytes128.argtypes = [i64, i64, i64, i64]
         _lib = lib
     return _lib
 
@@ -281,3 +291,56 @@ def bitmap_to_list(words, K: int) -> np.ndarray:
 
 def algorithmic_bytes_vb(N, K, nS, value_bytes) -> int:
     return int(_L().or_algorithmic_bytes_vb(N, K, nS, value_bytes))
+
+
+# The paper's 128-column quantization groups (Eq. 10 with alpha and beta per
+# row and group; 26 bytes per row and group).
+def num_groups128(K: int) -> int:
+    return int(_L().or_num_groups128(K))
+
+
+def pack128(trits) -> np.ndarray:
+    t = _c(trits, np.int8)
+    n, K = t.shape
+    out = np.empty((n, 26 * num_groups128(K)), dtype=np.uint8)
+    rc = _L().or_pack128(t.ctypes.data, n, K, out.ctypes.data)
+    if rc:
+        raise OracleError(rc, "pack128")
+    return out
+
+
+def unpack128(codes, K: int) -> np.ndarray:
+    c = _c(codes, np.uint8)
+    n = c.shape[0]
+    if c.shape[1] != 26 * num_groups128(K):
+        raise ValueError("code row length must be 26 * ceil(K/128)")
+    out = np.empty((n, K), dtype=np.int8)
+    rc = _L().or_unpack128(c.ctypes.data, n, K, out.ctypes.data)
+    if rc:
+        raise OracleError(rc, "unpack128")
+    return out
+
+
+def gemv128(N, K, codes_rows, alpha, beta, v, S, R, idx, x, rows=None, nthreads=None) -> np.ndarray:
+    """fp64 y[b][i] with per-row, per-128-column-group alpha and beta
+    ([N][ceil(K/128)] fp16) for output rows `rows` (default all)."""
+    rows = np.arange(N, dtype=np.int64) if rows is None else _c(rows, np.int64)
+    ng = num_groups128(K)
+    P = _c(codes_rows, np.uint8)
+    if P.shape != (rows.size, 26 * ng):
+        raise ValueError(f"codes_rows must be [{rows.size}][{26 * ng}]")
+    alpha, beta = _bits16(alpha).reshape(N, ng), _bits16(beta).reshape(N, ng)
+    keep, la = _layer_args(N, K, np.zeros(N, np.uint16), v, S, R, idx)
+    x = _bits16(x).reshape(-1, K)
+    B = x.shape[0]
+    y = np.empty((B, rows.size), dtype=np.float64)
+    rc = _L().or_gemv128_rows(N, K, P.ctypes.data, rows.ctypes.data, rows.size, alpha.ctypes.data,
+                              beta.ctypes.data, *la[1:], x.ctypes.data, B, y.ctypes.data,
+                              int(nthreads or threads()))
+    if rc:
+        raise OracleError(rc, "gemv128")
+    return y
+
+
+def algorithmic_bytes128(N, K, nS, value_bytes) -> int:
+    return int(_L().or_algorithmic_bytes128(N, K, nS, value_bytes))

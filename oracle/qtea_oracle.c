@@ -372,3 +372,128 @@ int64_t or_algorithmic_bytes_vb(int64_t N, int64_t K, int64_t nS, int64_t value_
   const int64_t entries = (N / 4) * nS;
   return N * or_num_packs(K) + value_bytes * entries + (2 * entries + 7) / 8 + 2 * N + 2 * K + 4 * nS;
 }
+
+/* ------------------------------------------------------------------------
+ * The paper's quantization groups (Eq. 10 in full; its setting: group size
+ * 128).  Row r and 128-column group g have a scale alpha_{r,g} and a bias
+ * beta_{r,g}:
+ *
+ *   y[b][r] = sum_g ( alpha_{r,g} sum_{j in g} T[r][j] v_j x[b][j]
+ *                   + beta_{r,g}  sum_{j in g} x[b][j] )
+ *           + the Eq. 11 residual, as above.
+ *
+ * The 128 trits of a row's group are packed into 26 bytes (the paper's
+ * appendix: 1.625 bits per weight): bytes 0..24 hold columns 5p..5p+4 of
+ * the group, byte 25 its last three columns and two zero trits; columns
+ * past K (in the last group) are zero trits too.
+ * ------------------------------------------------------------------------ */
+int64_t or_num_groups128(int64_t K) { return (K + 127) / 128; }
+
+/* out[r][26 g + p]: code of pack p of group g of row r. */
+int or_pack128(const int8_t* trits, int64_t nrows, int64_t K, uint8_t* out) {
+  if (nrows < 0 || K < 1) return OR_ERR_ARG;
+  const int64_t ng = or_num_groups128(K);
+  for (int64_t r = 0; r < nrows; ++r)
+    for (int64_t g = 0; g < ng; ++g)
+      for (int p = 0; p < 26; ++p) {
+        int8_t t[5];
+        for (int i = 0; i < 5; ++i) {
+          const int64_t c = 5 * p + i;  /* column within the group */
+          const int64_t j = 128 * g + c;
+          t[i] = (c < 128 && j < K) ? trits[r * K + j] : 0;
+        }
+        const int code = or_encode5(t);
+        if (code < 0) return code;
+        out[(r * ng + g) * 26 + p] = (uint8_t)code;
+      }
+  return OR_OK;
+}
+
+/* Inverse of or_pack128; rejects invalid bytes and nonzero padding trits. */
+int or_unpack128(const uint8_t* bytes, int64_t nrows, int64_t K, int8_t* trits) {
+  if (nrows < 0 || K < 1) return OR_ERR_ARG;
+  const int64_t ng = or_num_groups128(K);
+  for (int64_t r = 0; r < nrows; ++r)
+    for (int64_t g = 0; g < ng; ++g)
+      for (int p = 0; p < 26; ++p) {
+        int8_t t[5];
+        const int rc = or_decode_code(bytes[(r * ng + g) * 26 + p], t);
+        if (rc) return rc;
+        for (int i = 0; i < 5; ++i) {
+          const int64_t c = 5 * p + i;
+          const int64_t j = 128 * g + c;
+          if (c < 128 && j < K)
+            trits[r * K + j] = t[i];
+          else if (t[i] != 0)
+            return OR_ERR_CODE;
+        }
+      }
+  return OR_OK;
+}
+
+/* y[b][i] for output rows rows[i], from the packed groups P_rows[i] (row
+ * rows[i], 26 bytes per group), the group scales and biases alpha, beta
+ * ([N][ng] fp16), v [K], the residual as above, x [B][K]; fp64, each group's
+ * two sums in ascending column order, groups in ascending order. */
+int or_gemv128_rows(int64_t N, int64_t K, const uint8_t* P_rows, const int64_t* rows, int64_t nrows,
+                    const uint16_t* alpha, const uint16_t* beta, const uint16_t* v, const int32_t* S,
+                    int64_t nS, const uint16_t* R, const uint8_t* idx, const uint16_t* x, int64_t B,
+                    double* y, int nthreads) {
+  const or_layer L = make_layer(N, K, nS, alpha, v, S, R, idx);
+  int rc = check_layer(&L);
+  if (rc) return rc;
+  if (B < 1) return OR_ERR_ARG;
+  for (int64_t i = 0; i < nrows; ++i)
+    if (rows[i] < 0 || rows[i] >= N) return OR_ERR_ARG;
+  const int64_t ng = or_num_groups128(K), G = N / 4;
+  double* xd = (double*)malloc((size_t)(B * K) * sizeof(double));
+  if (!xd) return OR_ERR_NOMEM;
+  for (int64_t e = 0; e < B * K; ++e) xd[e] = or_half_to_double(x[e]);
+  int err = OR_OK;
+#pragma omp parallel num_threads(nthreads > 0 ? nthreads : 1)
+  {
+    int8_t* T = (int8_t*)malloc((size_t)K);
+    if (!T) {
+#pragma omp atomic write
+      err = OR_ERR_NOMEM;
+    }
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t i = 0; i < nrows; ++i) {
+      if (!T) continue;
+      const int64_t r = rows[i];
+      const int rr = or_unpack128(P_rows + i * ng * 26, 1, K, T);
+      if (rr) {
+#pragma omp atomic write
+        err = rr;
+        continue;
+      }
+      for (int64_t b = 0; b < B; ++b) {
+        const double* xb = xd + b * K;
+        double total = 0.0;
+        for (int64_t g = 0; g < ng; ++g) {
+          double tv = 0.0, xs = 0.0;
+          for (int64_t j = 128 * g; j < 128 * g + 128 && j < K; ++j) {
+            tv += (double)T[j] * or_half_to_double(v[j]) * xb[j];
+            xs += xb[j];
+          }
+          total += or_half_to_double(alpha[r * ng + g]) * tv + or_half_to_double(beta[r * ng + g]) * xs;
+        }
+        double res = 0.0;
+        for (int64_t s = 0; s < nS; ++s)
+          if (idx[s * G + r / 4] == (uint8_t)(r % 4)) res += or_half_to_double(R[s * G + r / 4]) * xb[S[s]];
+        y[b * nrows + i] = total + res;
+      }
+    }
+    free(T);
+  }
+  free(xd);
+  return err;
+}
+
+/* Weight bytes of one GEMV in the grouped format: 26 bytes per row and
+ * group, fp16 alpha and beta per row and group, the residual with value_bytes
+ * per value and 2-bit positions, fp16 v, int32 salient list. */
+int64_t or_algorithmic_bytes128(int64_t N, int64_t K, int64_t nS, int64_t value_bytes) {
+  const int64_t ng = or_num_groups128(K), entries = (N / 4) * nS;
+  return N * ng * 26 + 4 * N * ng + value_bytes * entries + (2 * entries + 7) / 8 + 2 * K + 4 * nS;
+}

@@ -403,3 +403,124 @@ def test_e4m3_storage_bytes():
         assert b16 - b8 == (N // 4) * nS
     # the paper's setting: 5% of columns, 8-bit values, one per four entries
     assert oracle.bpw_paper(0.05, 8) == pytest.approx(1.7, abs=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# The paper's 128-column quantization groups: per-group alpha and beta,
+# 26 bytes per row and group.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("K", [1, 5, 127, 128, 129, 300, 1000])
+def test_pack128_round_trip_and_padding(K):
+    rng = np.random.default_rng(K)
+    T = rng.integers(-1, 2, size=(3, K)).astype(np.int8)
+    P = oracle.pack128(T)
+    ng = (K + 127) // 128
+    assert P.shape == (3, 26 * ng) and P.max() < 243
+    assert np.array_equal(oracle.unpack128(P, K), T)
+    # byte 25 of a group holds its columns 125..127 and two zero trits: digits 3, 4 are 1
+    assert np.all(P[:, 25::26] // 27 == 4)
+    # columns past K are zero trits: a group with none of its columns left
+    # never occurs, and a fully padded byte is the all-zero code 121
+    for g in range(ng):
+        for p in range(26):
+            if 128 * g + 5 * p >= K:
+                assert np.all(P[:, 26 * g + p] == 121)
+    # first byte of every group: its columns 0..4 in base 3, least significant first
+    for g in range(ng):
+        cols = [128 * g + i for i in range(5)]
+        want = sum((int(T[0, j]) + 1 if j < K else 1) * 3 ** i for i, j in enumerate(cols))
+        assert P[0, 26 * g] == want
+
+
+def test_pack128_bits_per_weight():
+    # 26 one-byte packs per 128 columns: 1.625 bits per weight, 9.85x below fp16
+    assert oracle.pack128(np.zeros((1, 128), np.int8)).shape[1] == 26
+    assert 8 * 26 / 128 == 1.625 and round(16 / 1.625, 2) == 9.85
+
+
+def _g128_dyadic(seed, N, K, B, nS):
+    rng = np.random.default_rng(seed)
+    ng = (K + 127) // 128
+    S = np.sort(rng.choice(K, size=nS, replace=False)).astype(np.int32) if nS else np.zeros(0, np.int32)
+    return {
+        "T": rng.integers(-1, 2, size=(N, K)).astype(np.int8),
+        "alpha": (2.0 ** -rng.integers(0, 6, size=(N, ng))).astype(np.float16),
+        "beta": (rng.integers(-8, 9, size=(N, ng)) / 64.0).astype(np.float16),
+        "v": rng.choice([0.5, 1.0, 1.5, 2.0], size=K).astype(np.float16),
+        "S": S,
+        "R": (rng.integers(-64, 65, size=(nS, N // 4)) / 64.0).astype(np.float16),
+        "idx": rng.integers(0, 4, size=(nS, N // 4)).astype(np.uint8),
+        "x": (rng.integers(-8, 9, size=(B, K)) / 4.0).astype(np.float16),
+    }
+
+
+def _g128(c, N, K, **kw):
+    return oracle.gemv128(N, K, oracle.pack128(c["T"]), c["alpha"], c["beta"], c["v"], c["S"], c["R"],
+                          c["idx"], c["x"], **kw)
+
+
+@pytest.mark.parametrize("N,K,B,nS", [(8, 130, 2, 3), (4, 128, 1, 0), (12, 300, 3, 5), (4, 7, 2, 1)])
+def test_gemv128_brute_force_exact(N, K, B, nS):
+    """Exact rational arithmetic, term by term from Eq. 10 and Eq. 11."""
+    c = _g128_dyadic(N * K + B, N, K, B, nS)
+    Fr = lambda h: Fraction(float(h))
+    want = np.zeros((B, N), dtype=object)
+    for b in range(B):
+        for r in range(N):
+            tot = Fraction(0)
+            for g in range((K + 127) // 128):
+                cols = range(128 * g, min(128 * g + 128, K))
+                tv = sum(int(c["T"][r, j]) * Fr(c["v"][j]) * Fr(c["x"][b, j]) for j in cols)
+                xs = sum(Fr(c["x"][b, j]) for j in cols)
+                tot += Fr(c["alpha"][r, g]) * tv + Fr(c["beta"][r, g]) * xs
+            for s in range(nS):
+                if c["idx"][s, r // 4] == r % 4:
+                    tot += Fr(c["R"][s, r // 4]) * Fr(c["x"][b, c["S"][s]])
+            want[b, r] = tot
+    got = _g128(c, N, K)
+    assert all(Fraction(got[b, r]) == want[b, r] for b in range(B) for r in range(N))
+
+
+def test_gemv128_one_scale_per_row_is_the_single_group_product():
+    """alpha_{r,g} = alpha_r for every g and beta = 0 reduces to Eq. 10 with
+    one group: the single-group oracle (other packing, other sum order) gives
+    the same values exactly on dyadic inputs."""
+    N, K, B, nS = 16, 1000, 2, 9
+    c = _g128_dyadic(5, N, K, B, nS)
+    c["alpha"] = np.repeat(c["alpha"][:, :1], c["alpha"].shape[1], axis=1)
+    c["beta"] = np.zeros_like(c["beta"])
+    y128 = _g128(c, N, K)
+    y1 = oracle.gemv(N, K, oracle.pack(c["T"]), c["alpha"][:, 0], c["v"], c["S"], c["R"], c["idx"], c["x"])
+    assert np.array_equal(y128, y1)
+
+
+def test_gemv128_bias_alone_is_the_group_sums():
+    N, K, B = 8, 300, 2
+    c = _g128_dyadic(6, N, K, B, 0)
+    c["T"][:] = 0
+    y = _g128(c, N, K)
+    xg = np.zeros((B, 3))
+    xpad = np.zeros((B, 384))
+    xpad[:, :K] = c["x"].astype(np.float64)
+    xg = xpad.reshape(B, 3, 128).sum(axis=2)  # per-group activation sums
+    want = xg @ c["beta"].astype(np.float64).T
+    assert np.array_equal(y, want)
+
+
+def test_gemv128_rows_subset_and_sign():
+    N, K, B, nS = 12, 260, 2, 4
+    c = _g128_dyadic(8, N, K, B, nS)
+    full = _g128(c, N, K)
+    rows = np.array([11, 0, 5], dtype=np.int64)
+    part = oracle.gemv128(N, K, oracle.pack128(c["T"][rows]), c["alpha"], c["beta"], c["v"], c["S"], c["R"],
+                          c["idx"], c["x"], rows=rows)
+    assert np.array_equal(part, full[:, rows])
+    neg = dict(c, alpha=-c["alpha"], beta=-c["beta"], R=-c["R"])
+    assert np.array_equal(_g128(neg, N, K), -full)
+
+
+def test_algorithmic_bytes128():
+    # 8B-shaped gate_up, 5% E4M3 residual: 26 bytes per row and group plus 4 bytes of scales
+    N, K, nS = 28672, 4096, 205
+    b = oracle.algorithmic_bytes128(N, K, nS, 1)
+    assert b == N * 32 * 26 + 4 * N * 32 + (N // 4) * nS + ((N // 4) * nS * 2 + 7) // 8 + 2 * K + 4 * nS
