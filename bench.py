@@ -54,11 +54,15 @@ def build_stack(wl, B, dev, seed, layers=None):
     for layer, mat, role, N, K in wl.matrices():
         if layers is not None and layer >= layers:
             break
-        L = synth.layer_inputs(seed, layer, mat, N, K, p0=wl.p0, frac=wl.frac, resid=wl.resid)
+        L = synth.layer_inputs(seed, layer, mat, N, K, p0=wl.p0, frac=wl.frac, resid=wl.resid,
+                               groups=wl.groups)
         x = synth.activations(seed, layer, mat, B, K)
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         nS = int(L["S"].size)
-        if wl.resid == "e4m3":
+        if wl.groups:
+            pm = q.pack_matrix_g128(t(L["trits"]), t(L["alpha_g"]), t(L["beta_g"]), t(L["v"]), t(L["bitmap"]), nS,
+                                    t(L["R8"]), t(L["idx"]))
+        elif wl.resid == "e4m3":
             pm = q.pack_matrix_e4m3(t(L["trits"]), t(L["alpha"]), t(L["v"]), t(L["bitmap"]), nS, t(L["R8"]),
                                     t(L["idx"]))
         else:
@@ -66,7 +70,8 @@ def build_stack(wl, B, dev, seed, layers=None):
         mats.append({
             "layer": layer, "mat": mat, "role": role, "N": N, "K": K, "nS": nS, "pm": pm, "x": t(x),
             "y": torch.empty((B, N), dtype=torch.float32, device=dev),
-            "bytes": q.algorithmic_bytes(N, K, nS, value_bytes=1 if wl.resid == "e4m3" else 2),
+            "bytes": (q.algorithmic_bytes_g128(N, K, nS) if wl.groups else
+                      q.algorithmic_bytes(N, K, nS, value_bytes=1 if wl.resid == "e4m3" else 2)),
         })
         if layer == 0 or (layer + 1) % 8 == 0 and mat == len(wl.shapes) - 1:
             log(f"packed layer {layer} {role} {N}x{K} ({time.time() - t0:.1f}s)")
@@ -141,8 +146,10 @@ def replay_spread(g, stream, reps):
             "replays": reps}
 
 
-def kernel_name(B, grouped=False, rows_per_panel=1024, e4m3=False):
+def kernel_name(B, grouped=False, rows_per_panel=1024, e4m3=False, g128=False):
     f8 = "true" if e4m3 else "false"
+    if grouped and g128:
+        return f"grouped_gemv_kernel<{rows_per_panel // 128}, true, true>"
     if grouped and B > 1:
         # hi/lo activation halves in one or two MFMAs
         return f"grouped_mma_kernel<{1 if B <= 8 else 2}, {f8}>"
@@ -210,14 +217,19 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
     t_oracle = 0.0
     for m in mats:
         L = synth.layer_inputs(seed, m["layer"], m["mat"], m["N"], m["K"], p0=wl.p0, frac=wl.frac,
-                               resid=wl.resid)
+                               resid=wl.resid, groups=wl.groups)
         if wl.resid == "e4m3":
             L["R"] = oracle.e4m3_as_half(L["R8"])
         x = synth.activations(seed, m["layer"], m["mat"], B, m["K"])
-        P = oracle.pack(L.pop("trits"))
-        args = (m["N"], m["K"], P, L["alpha"], L["v"], L["S"], L["R"], L["idx"], x)
+        if wl.groups:
+            gemv = oracle.gemv128
+            args = (m["N"], m["K"], oracle.pack128(L.pop("trits")), L["alpha_g"], L["beta_g"], L["v"], L["S"],
+                    L["R"], L["idx"], x)
+        else:
+            gemv = oracle.gemv
+            args = (m["N"], m["K"], oracle.pack(L.pop("trits")), L["alpha"], L["v"], L["S"], L["R"], L["idx"], x)
         t0 = time.perf_counter()
-        y = oracle.gemv(*args, nthreads=nthreads)
+        y = gemv(*args, nthreads=nthreads)
         t_oracle += time.perf_counter() - t0
         yg = m["y"].cpu().numpy().astype(np.float64)
         rel = np.linalg.norm(yg - y, axis=1) / np.linalg.norm(y, axis=1)
@@ -227,7 +239,7 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
     while t_oracle < min_s:
         for args in inputs:
             t0 = time.perf_counter()
-            oracle.gemv(*args, nthreads=nthreads)
+            gemv(*args, nthreads=nthreads)
             t_oracle += time.perf_counter() - t0
         passes += 1
     us_token = t_oracle / passes * 1e6
@@ -283,12 +295,15 @@ def main():
     seed = synth.DEFAULT_SEED if args.seed is None else args.seed
     mats = build_stack(wl, B, dev, seed, args.layers)
     n_layers = len({m["layer"] for m in mats})
-    ws_bytes = max(q.qtea_workspace_bytes(m["pm"].desc, B) for m in mats)
+    ws_bytes = 4 if wl.groups else max(q.qtea_workspace_bytes(m["pm"].desc, B) for m in mats)
     ws = torch.zeros(max(ws_bytes, 4), dtype=torch.uint8, device=dev)
     stream = torch.cuda.Stream(device=dev)
 
     token_bytes = sum(m["bytes"] for m in mats)
     ms_chain = float("nan")
+    if wl.groups and not args.grouped_only:
+        log("the grouped format runs through the grouped entry points only: timing the grouped execution")
+        args.grouped_only = True
     if not args.grouped_only:
         g = capture(mats, B, ws, stream)
         ms_chain = time_graph(g, stream, args.steps, args.warmup)
@@ -329,7 +344,8 @@ def main():
     # so the average launch moves token_bytes / launches.  Durations come
     # from HIP events around the graph replays above.
     n_launch = 1 if grouped else len(mats)
-    kname = kernel_name(B, grouped, gp.info.rows_per_panel if grouped else 1024, wl.resid == "e4m3")
+    kname = kernel_name(B, grouped, gp.info.rows_per_panel if grouped else 1024, wl.resid == "e4m3",
+                        bool(wl.groups))
     per_launch_bytes = token_bytes / n_launch
     us_launch = ms * 1e3 / n_launch
     ach = per_launch_bytes / (us_launch * 1e-6) / 1e9

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 3
+#define QTEA_ABI_VERSION 4
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -65,10 +65,12 @@ enum qtea_status {
 typedef struct qtea_desc {
   uint32_t magic;       /* QTEA_DESC_MAGIC when valid                        */
   uint32_t layout;      /* device layout version: 2 = fp16 residual values,
-                           3 = FP8 E4M3 residual values (qtea_pack_e4m3)     */
+                           3 = FP8 E4M3 residual values (qtea_pack_e4m3),
+                           4 = 128-column groups (qtea_pack_g128)          */
   int64_t N, K;         /* output rows, input columns                        */
   int64_t n_salient;    /* |S|                                               */
-  int64_t n_packs;      /* ceil(K / 5) one-byte packs per row                */
+  int64_t n_packs;      /* one-byte packs per row: ceil(K / 5), or 26 per
+                           128-column group in layout 4                      */
   int64_t n_groups;     /* ceil(n_packs / 16) sixteen-pack groups            */
   int64_t n_pad;        /* N rounded up to a multiple of 64                  */
   int64_t bytes_total;  /* size of the packed buffer in bytes                */
@@ -141,6 +143,33 @@ int qtea_pack_e4m3(const int8_t* trits, int64_t N, int64_t K, const uint16_t* ro
                    qtea_desc* out_desc, void* stream);
 
 /*
+ * The paper's full format (Eq. 10 with its group size of 128, and its
+ * storage): for row r and the g-th group of 128 input columns a scale
+ * alpha[r][g] and a bias beta[r][g],
+ *
+ *   y[b][r] = sum_g ( alpha[r][g] * sum_{j in g} T[r][j] * v_j * x[b][j]
+ *                   + beta[r][g]  * sum_{j in g} x[b][j] )  + the residual;
+ *
+ * each group's 128 trits packed into 26 bytes (25 of five columns, the last
+ * of three columns and two zero trits; 1.625 bits per weight), the residual
+ * stored as in qtea_pack_e4m3.
+ *
+ *   group_scale, group_bias  device fp16 [N][ceil(K/128)]
+ *   other arguments          as qtea_pack_e4m3
+ *   packed                   >= qtea_packed_bytes_g128(...)
+ *
+ * A matrix in this layout runs through the grouped entry points at batch 1
+ * (qtea_grouped_plan / qtea_grouped_gemv); qtea_gemv, qtea_gemm_lowbatch and
+ * qtea_workspace_bytes answer QTEA_ERR_INVALID_ARG for it.  qtea_debug_unpack
+ * returns its codes as [N][26 ceil(K/128)], group after group.
+ */
+int qtea_packed_bytes_g128(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes);
+int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* group_scale,
+                   const uint16_t* group_bias, const uint16_t* col_rescale, const uint32_t* salient_bitmap,
+                   int64_t n_salient, const uint8_t* resid_val, const uint8_t* resid_idx, void* packed,
+                   int64_t packed_bytes, qtea_desc* out_desc, void* stream);
+
+/*
  * Workspace bytes that qtea_gemv (batch = 1) / qtea_gemm_lowbatch need for
  * this matrix at this batch size.  The workspace holds per-K-slice partial
  * sums and per-row-block arrival counters.  It must be zero-filled before
@@ -190,7 +219,8 @@ int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_
  * Grouped GEMV: Y_m = X_m W_m^T for a list of n_problems independent problems
  * at one batch size (each W_m packed by qtea_pack or, all of them,
  * qtea_pack_e4m3; the same operation as qtea_gemm_lowbatch applied to every
- * problem) in one persistent launch.  The problems' packed bytes are
+ * problem) in one persistent launch.  Matrices packed by qtea_pack_g128 run
+ * here at batch 1 (QTEA_ERR_BATCH for a larger batch).  The problems' packed bytes are
  * streamed back to back: a workgroup already loads the next problem's
  * weights while it finishes the current one.  No problem may read another
  * problem's output (all activations must be ready when the launch starts);
@@ -212,7 +242,7 @@ typedef struct qtea_grouped_info {
   int32_t max_parts;       /* chunks sharing one panel, at most          */
   int32_t n_chunks;        /* chunks of work units (scheduling grain)    */
   int32_t n_split_panels;  /* panels whose parts are summed by a second launch */
-  int32_t layout;          /* residual layout of every problem (2 or 3)  */
+  int32_t layout;          /* layout of every problem (2, 3 or 4)       */
   int32_t reserved;
   int64_t n_units;
   int64_t plan_bytes;      /* device plan buffer size                    */

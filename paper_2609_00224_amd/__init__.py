@@ -7,7 +7,8 @@ is used to allocate device memory and to name the current HIP stream.
 There is no CPU fallback: if the library is not built, loading it raises.
 
 Entry points carry the C names: qtea_packed_bytes, qtea_pack,
-qtea_packed_bytes_e4m3, qtea_pack_e4m3, qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
+qtea_packed_bytes_e4m3, qtea_pack_e4m3, qtea_packed_bytes_g128, qtea_pack_g128,
+qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
 qtea_debug_unpack, qtea_status_string, qtea_abi_version,
 qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv.
 """
@@ -35,10 +36,11 @@ EXPORTS = (
     "qtea_status_string", "qtea_abi_version", "qtea_packed_bytes", "qtea_pack",
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
     "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
-    "qtea_packed_bytes_e4m3", "qtea_pack_e4m3",
+    "qtea_packed_bytes_e4m3", "qtea_pack_e4m3", "qtea_packed_bytes_g128", "qtea_pack_g128",
 )
 QTEA_LAYOUT_FP16 = 2  # residual values fp16
 QTEA_LAYOUT_E4M3 = 3  # residual values FP8 E4M3
+QTEA_LAYOUT_G128 = 4  # 128-column groups with scale and bias, E4M3 residual
 QTEA_GROUPED_MAGIC = 0x51475250
 
 
@@ -98,6 +100,10 @@ def load(path: str = LIB_PATH):
     lib.qtea_packed_bytes_e4m3.argtypes = [i64, i64, i64, ctypes.POINTER(i64)]
     lib.qtea_pack_e4m3.restype = i32
     lib.qtea_pack_e4m3.argtypes = [vp, i64, i64, vp, vp, vp, i64, vp, vp, vp, i64, pdesc, vp]
+    lib.qtea_packed_bytes_g128.restype = i32
+    lib.qtea_packed_bytes_g128.argtypes = [i64, i64, i64, ctypes.POINTER(i64)]
+    lib.qtea_pack_g128.restype = i32
+    lib.qtea_pack_g128.argtypes = [vp, i64, i64, vp, vp, vp, vp, i64, vp, vp, vp, i64, pdesc, vp]
     lib.qtea_workspace_bytes.restype = i32
     lib.qtea_workspace_bytes.argtypes = [pdesc, i32, ctypes.POINTER(i64)]
     lib.qtea_workspace_init.restype = i32
@@ -211,6 +217,40 @@ def qtea_pack_e4m3(trits, row_scale, col_rescale, salient_bitmap, n_salient: int
                                _ptr(packed), packed.numel() * packed.element_size(), ctypes.byref(d),
                                _stream(stream))
     _check(st, "qtea_pack_e4m3")
+    return d
+
+
+def qtea_packed_bytes_g128(N: int, K: int, n_salient: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().qtea_packed_bytes_g128(N, K, n_salient, ctypes.byref(out)), "qtea_packed_bytes_g128")
+    return out.value
+
+
+def qtea_pack_g128(trits, group_scale, group_bias, col_rescale, salient_bitmap, n_salient: int, resid_val,
+                   resid_idx, packed, stream=None) -> QteaDesc:
+    """Pack in the paper's grouped format: int8 [N][K] trits, fp16 [N][ceil(K/128)]
+    group scales and biases, fp16 [K] rescales, int32 [ceil(K/32)] salient
+    bitmap, uint8 [nS][N/4] E4M3 residual codes and positions."""
+    import torch
+
+    _need_cuda(trits, group_scale, group_bias, col_rescale, salient_bitmap, resid_val, resid_idx, packed)
+    assert trits.dtype == torch.int8 and group_scale.dtype == torch.float16
+    assert group_bias.dtype == torch.float16 and col_rescale.dtype == torch.float16
+    assert salient_bitmap.dtype == torch.int32
+    assert resid_val.dtype == torch.uint8 and resid_idx.dtype == torch.uint8
+    N, K = trits.shape
+    ng = (K + 127) // 128
+    if tuple(group_scale.shape) != (N, ng) or tuple(group_bias.shape) != (N, ng):
+        raise ValueError("group scales and biases are [N][ceil(K/128)]")
+    if salient_bitmap.numel() != (K + 31) // 32:
+        raise ValueError("the salient bitmap has ceil(K/32) words")
+    nS = int(n_salient)
+    d = QteaDesc()
+    st = load().qtea_pack_g128(_ptr(trits), N, K, _ptr(group_scale), _ptr(group_bias), _ptr(col_rescale),
+                               _ptr(salient_bitmap), nS, _ptr(resid_val) if nS else None,
+                               _ptr(resid_idx) if nS else None, _ptr(packed),
+                               packed.numel() * packed.element_size(), ctypes.byref(d), _stream(stream))
+    _check(st, "qtea_pack_g128")
     return d
 
 
@@ -340,6 +380,27 @@ def pack_matrix_e4m3(trits, alpha, v, bitmap, n_salient, R8, idx, stream=None) -
     packed = torch.empty(nbytes, dtype=torch.uint8, device=trits.device)
     d = qtea_pack_e4m3(trits, alpha, v, bitmap, n_salient, R8, idx, packed, stream=stream)
     return PackedMatrix(d, packed)
+
+
+def pack_matrix_g128(trits, alpha, beta, v, bitmap, n_salient, R8, idx, stream=None) -> PackedMatrix:
+    """Allocate the packed buffer and pack in the paper's grouped format."""
+    import torch
+
+    N, K = trits.shape
+    nbytes = qtea_packed_bytes_g128(N, K, int(n_salient))
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=trits.device)
+    d = qtea_pack_g128(trits, alpha, beta, v, bitmap, n_salient, R8, idx, packed, stream=stream)
+    return PackedMatrix(d, packed)
+
+
+def algorithmic_bytes_g128(N: int, K: int, n_salient: int) -> int:
+    """Weight bytes of one GEMV in the paper's grouped format: 26 bytes per
+    row and 128-column group, fp16 scale and bias per row and group, one
+    E4M3 byte and a 2-bit position per residual value, fp16 v, the int32
+    salient list."""
+    ng = (K + 127) // 128
+    entries = (N // 4) * n_salient
+    return N * ng * 26 + 4 * N * ng + entries + (2 * entries + 7) // 8 + 2 * K + 4 * n_salient
 
 
 def new_workspace(desc: QteaDesc, batch: int, device="cuda"):

@@ -73,7 +73,8 @@ struct GLds {
   static constexpr int RV = RR + 4 * RP;                  // per wave: values [TPW][16 fp16 or 32 E4M3 columns][16]
   static constexpr int RI = RV + kGW * 1024;              // per wave: u32 positions [2][16], fp32 x [32]
   static constexpr int FLAG = RI + kGW * 256;             // one int
-  static constexpr int BYTES = FLAG + 16;
+  static constexpr int XS = FLAG + 16;                    // layout 4: [2 buffers][5 waves][2] fp32 group sums of x
+  static constexpr int BYTES = XS + 128;
 };
 static_assert(GLds<4>::TPW == 1 && GLds<8>::TPW == 2, "one or two tiles per wave");
 static_assert(2 * kResCols * 32 == 1024 && 2 * kResCols8 * 16 == 1024,
@@ -87,8 +88,13 @@ __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
   return 0x0C0C0000u | (uint32_t(k) << 8) | uint32_t(4 + k);
 }
 
-// F8: residual values are E4M3 bytes (layout 3), else fp16 (layout 2).
-template <int RB, bool F8>
+// F8: residual values are E4M3 bytes (layouts 3, 4), else fp16 (layout 2).
+// G128: the paper's 128-column groups (layout 4): a slice is two groups, its
+// device columns 160 g + c (c < 128) the group's columns; each 16-byte unit's
+// sum is scaled by its row's alpha[r][g] as it is added, and the quarter
+// holding the first half of a group adds beta[r][g] times the group's sum
+// of x.
+template <int RB, bool F8, bool G128 = false>
 __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __restrict__ plan,
                                                            float* __restrict__ part,
                                                            uint32_t* __restrict__ counters) {
@@ -147,12 +153,18 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // waits for the next unit's weights, which are the youngest loads.
 
   // activations: this thread stages slice column tid (kept as loaded, checked when staged)
+  // real column of device column tid of slice s (layout 4: 160 device
+  // columns per 128-column group, the last 32 padding)
+  auto real_col = [&](int s) -> uint32_t {
+    return G128 ? uint32_t(s * 2 * kScaleCols + kScaleCols * (tid / 160) + tid % 160)
+                : uint32_t(s * kSliceCols + tid);
+  };
   auto load_xv = [&](const Cursor c, uint16_t& xr, uint16_t& vr) {
     const GProblem& pr = P[c.m];
     const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
-    const uint32_t col = uint32_t(c.slice * kSliceCols + tid);
+    const uint32_t col = real_col(c.slice), dcol = uint32_t(c.slice * kSliceCols + tid);
     xr = gptr(pr.x)[col < kx ? col : kx - 1];
-    vr = gptr(pr.v)[col < kv ? col : kv - 1];
+    vr = gptr(pr.v)[dcol < kv ? dcol : kv - 1];  // v is in device column order
   };
   // row scales of the row blocks this lane finalizes: t = q + 4 i
   constexpr int RF = RB / 4;
@@ -237,18 +249,47 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   }
   load_res(cur, s_lo_c, s_hi_c);
   uint16_t al[RF];
-  load_alpha(cur, al);
+  if (!G128) load_alpha(cur, al);
+  // layout 4: (alpha | beta << 16) of row block t's row in the quarter's group, one unit ahead
+  uint32_t AB[G128 ? RB : 1];
+  auto ab_at = [&](const Cursor c, int t) -> uint32_t {
+    const GProblem& pr = P[c.m];
+    const int n_sg = pr.n_groups >> 1, n_tiles = int(pr.n_pad >> 6);
+    const int sg = min(2 * c.slice + (q >> 1), n_sg - 1);
+    const int tl = min(c.panel * TPP + wt + (kGW / 4) * t, n_tiles - 1);
+    return reinterpret_cast<gu32*>(gptr(pr.alpha))[(uint32_t(tl * n_sg + sg) << 6) + uint32_t(wr * 16 + l16)];
+  };
+  if constexpr (G128) {
+#pragma unroll
+    for (int t = 0; t < RB; ++t) AB[t] = ab_at(cur, t);
+  }
 
   // stage a slice's activations in buffer b: a_j = v_j x_j (exact in fp32) and x_j
   auto stage = [&](const Cursor c, int b) {
     if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
       const GProblem& pr = P[c.m];
-      const int gcol = c.slice * kSliceCols + tid;
-      const float xf = gcol < pr.K ? h2f(xr) : 0.0f;
-      const float vf = gcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
+      const int gcol = int(real_col(c.slice)), dcol = c.slice * kSliceCols + tid;
+      const bool xin = gcol < pr.K && (!G128 || tid % 160 < kScaleCols);
+      const float xf = xin ? h2f(xr) : 0.0f;
+      const float vf = dcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
       float* st = reinterpret_cast<float*>(lds + L::ST + b * L::STB);
       st[tid] = vf * xf;
       st[kSliceCols + tid] = xf;
+      if constexpr (G128) {
+        // the slice's two groups' sums of x: per wave (butterfly, fixed
+        // order), the five waves' parts summed by their readers
+        float s0 = tid < 160 ? xf : 0.0f, s1 = tid < 160 ? 0.0f : xf;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+          s0 += __shfl_xor(s0, off);
+          s1 += __shfl_xor(s1, off);
+        }
+        if (lane == 0) {
+          float* xs = reinterpret_cast<float*>(lds + L::XS + 64 * b) + 2 * w;
+          xs[0] = s0;
+          xs[1] = s1;
+        }
+      }
     }
   };
   stage(cur, 0);
@@ -281,6 +322,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     uint32_t taken = 0;
     if (take && tid == 0) taken = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int col0 = cur.slice * kSliceCols;
+    // device column of real column j of this slice, if it is one
+    const int rcol0 = G128 ? cur.slice * 2 * kScaleCols : col0;
+    auto xcol = [&](int j) -> int {
+      const int jl = j - rcol0;
+      return G128 ? (jl >= 0 && jl < 2 * kScaleCols ? 160 * (jl >> 7) + (jl & (kScaleCols - 1)) : -1) : jl;
+    };
     const int sb = it & 1;  // staging buffer of this unit
     const float* a_lds = reinterpret_cast<const float*>(lds + L::ST + sb * L::STB);
     const float* xr_lds = a_lds + kSliceCols;
@@ -351,6 +398,14 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const uint32_t lane_off = ((uint32_t(n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & smask;
 #pragma unroll
     for (int t = 0; t < RB; ++t) acc[t] = pstart ? 0.0f : acc[t];
+    // layout 4: the sum of x over this quarter's group, for the first
+    // quarter of each group (the other adds no bias)
+    float xq = 0.0f;
+    if constexpr (G128) {
+      const float* xs = reinterpret_cast<const float*>(lds + L::XS + 64 * sb) + (q >> 1);
+      const float xg = (((xs[0] + xs[2]) + xs[4]) + xs[6]) + xs[8];
+      xq = (q & 1) ? 0.0f : xg;
+    }
 #pragma unroll
     for (int t = 0; t < RB; ++t) {
       const u32x4 wv = W[t];
@@ -364,8 +419,17 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: addresses
       __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // DS reads
       __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: sums
+      if constexpr (G128) {
+        float su = e[0];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[t] += e[i];
+        for (int i = 1; i < 16; ++i) su += e[i];
+        const float al4 = h2f(uint16_t(AB[t] & 0xffffu)), be4 = h2f(uint16_t(AB[t] >> 16));
+        acc[t] = __builtin_fmaf(be4, xq, __builtin_fmaf(al4, su, acc[t]));
+        AB[t] = ab_at(nxt, t);  // the next unit's, after the last use
+      } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[t] += e[i];
+      }
       // keep the sums here: without a use in this block the compiler sinks
       // a unit's adds below the residual and holds every entry in registers
       asm volatile("" : "+v"(acc[t]));
@@ -394,7 +458,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       char* rv_w = lds + L::RV + w * 1024;
       uint32_t* ri_w = reinterpret_cast<uint32_t*>(lds + L::RI + w * 256);
       *reinterpret_cast<u32x4*>(rv_w + 16 * lane) = rvq;
-      const int xc = int(ris) - col0;
+      const int xc = xcol(int(ris));
       const uint32_t xw = __float_as_uint(xr_lds[xc >= 0 && xc < kSliceCols ? xc : 0]);
       ri_w[lane] = lane < 32 ? ris : xw;
       asm volatile("" ::: "memory");
@@ -415,7 +479,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       columns(0, nc < 16 ? nc : 16);
       if (F8 && ncol > 16) {  // uniform: columns 16..31 through the same words area
         asm volatile("" ::: "memory");  // after the reads above (same wave: in order)
-        const int xc2 = int(ris2) - col0;
+        const int xc2 = xcol(int(ris2));
         const uint32_t xw2 = __float_as_uint(xr_lds[xc2 >= 0 && xc2 < kSliceCols ? xc2 : 0]);
         ri_w[lane] = lane < 32 ? ris2 : xw2;
         asm volatile("" ::: "memory");
@@ -428,7 +492,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         if (grow_ok) {
           const int64_t vi = rval_index(grow, s, pr.nS);
           const float rv = F8 ? e4m3_to_float(reinterpret_cast<gu8*>(gptr(pr.rval))[vi]) : h2f(gptr(pr.rval)[vi]);
-          const float t = rv * xr_lds[gptr(pr.S)[s] - col0];
+          const float t = rv * xr_lds[xcol(gptr(pr.S)[s])];
           const uint32_t idx = (gptr(pr.ridx)[T * pr.nS + s] >> gsh) & 3u;
 #pragma unroll
           for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
@@ -477,7 +541,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
         for (int t = 1; t < RB; ++t)
           if (tq == t) mine = tot[t];
         prow[i] = (w + kGW * tq) * 16 + l16;
-        val[i] = h2f(al[i]) * mine + rres[prow[i]];
+        val[i] = (G128 ? mine : h2f(al[i]) * mine) + rres[prow[i]];  // layout 4: scaled per unit
       }
       gf32* y = (gf32*)pr.y;
       const int64_t row0 = int64_t(cur.panel) * RP;
@@ -511,7 +575,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     s_lo_c = __builtin_amdgcn_readlane(spv, 0);
     s_hi_c = __builtin_amdgcn_readlane(spv, 1);
     load_res(nxt, s_lo_c, s_hi_c);  // after the last use of this unit's residual values
-    load_alpha(nxt, al);            // and of its row scales
+    if (!G128) load_alpha(nxt, al);  // and of its row scales
     cur = nxt;
   }
 }
@@ -570,11 +634,11 @@ int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   return *n_slices * *n_panels;
 }
 
-template <int RB, bool F8>
+template <int RB, bool F8, bool G128 = false>
 hipError_t set_lds_attr() {
   static bool done = false;
   if (!done) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB, F8>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB, F8, G128>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, GLds<RB>::BYTES);
     if (e != hipSuccess) return e;
     done = true;
@@ -603,13 +667,13 @@ int grid_size() {
   return n * std::max(1, std::min(per, kWgPerCu));
 }
 
-template <int RB, bool F8>
+template <int RB, bool F8, bool G128 = false>
 hipError_t launch_grouped(const uint8_t* plan, int grid, int n_splits, float* part, uint32_t* counters,
                           hipStream_t st) {
-  const hipError_t e = set_lds_attr<RB, F8>();
+  const hipError_t e = set_lds_attr<RB, F8, G128>();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((grouped_gemv_kernel<RB, F8>), dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan, part,
-                     counters);
+  hipLaunchKernelGGL((grouped_gemv_kernel<RB, F8, G128>), dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan,
+                     part, counters);
   if (n_splits > 0) {
     constexpr int RP = GLds<RB>::RP;
     hipLaunchKernelGGL(grouped_reduce_kernel<RP>, dim3(n_splits), dim3(RP / 4), 0, st, plan, part);
@@ -648,12 +712,13 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   const int G = mma ? cu_count() : grid_size();
   if (G < 1) return QTEA_ERR_HIP;
   const uint32_t layout = descs[0].layout;
+  if (layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;  // the grouped format runs at batch 1
   for (int m = 0; m < n_problems; ++m) {
     if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
     if (descs[m].layout != layout) return QTEA_ERR_INVALID_ARG;  // one residual format per plan
     // the kernel addresses the packed bytes and the residual with 32-bit offsets
     const int64_t trit_bytes = descs[m].n_pad * descs[m].n_groups * kGroupPacks;
-    const int64_t resid_bytes = (descs[m].n_pad / 4) * descs[m].n_salient * (layout == kLayoutE4M3 ? 1 : 2);
+    const int64_t resid_bytes = (descs[m].n_pad / 4) * descs[m].n_salient * (layout == kLayout ? 2 : 1);
     if (trit_bytes >= (int64_t(1) << 31) || resid_bytes >= (int64_t(1) << 31)) return QTEA_ERR_INVALID_ARG;
   }
 
@@ -816,7 +881,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   H->n_grabs = n_grabs;
   H->off_splits = off_splits;
   H->n_splits = n_splits;
-  H->f8 = layout == kLayoutE4M3;
+  H->f8 = layout != kLayout;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(plan, hbuf, size_t(need), hipMemcpyHostToDevice, st);
@@ -849,8 +914,10 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   float* part = reinterpret_cast<float*>(ws + kAlign);
   const uint8_t* pl = static_cast<const uint8_t*>(plan);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (info->layout != kLayout && info->layout != kLayoutE4M3) return QTEA_ERR_INVALID_ARG;
-  const bool f8 = info->layout == kLayoutE4M3;
+  if (info->layout != kLayout && info->layout != kLayoutE4M3 && info->layout != kLayoutG128)
+    return QTEA_ERR_INVALID_ARG;
+  const bool f8 = info->layout != kLayout, g128 = info->layout == kLayoutG128;
+  if (g128 && info->batch != 1) return QTEA_ERR_INVALID_ARG;
   hipError_t e;
   if (info->batch > 1) {
     if (info->rows_per_panel != grouped_mma_rows_per_panel()) return QTEA_ERR_INVALID_ARG;
@@ -858,6 +925,14 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
     if (e == hipSuccess && info->n_split_panels > 0) {
       hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, pl, part);
       e = hipGetLastError();
+    }
+    return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+  }
+  if (g128) {
+    switch (info->rows_per_panel) {
+      case GLds<4>::RP: e = launch_grouped<4, true, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+      case GLds<8>::RP: e = launch_grouped<8, true, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+      default: return QTEA_ERR_INVALID_ARG;
     }
     return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
   }

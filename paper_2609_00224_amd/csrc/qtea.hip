@@ -99,17 +99,20 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
                                  int64_t n_pad, int64_t n_groups, uint16_t* __restrict__ o_alpha,
                                  uint16_t* __restrict__ o_v, int32_t* o_S,
                                  int32_t* __restrict__ o_spos, VT* __restrict__ o_rval,
-                                 uint32_t* __restrict__ o_ridx, uint32_t* __restrict__ flags) {
+                                 uint32_t* __restrict__ o_ridx, uint32_t* __restrict__ flags, int g128) {
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
   const int64_t t0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  for (int64_t i = t0; i < n_pad; i += stride) o_alpha[i] = i < N ? alpha[i] : 0;
-  for (int64_t i = t0; i < n_groups * kGroupCols; i += stride) o_v[i] = i < K ? v[i] : 0;
+  if (o_alpha)  // layout 4: scales and v by pack_scales128_kernel
+    for (int64_t i = t0; i < n_pad; i += stride) o_alpha[i] = i < N ? alpha[i] : 0;
+  if (o_v)
+    for (int64_t i = t0; i < n_groups * kGroupCols; i += stride) o_v[i] = i < K ? v[i] : 0;
   if (S != o_S)
     for (int64_t i = t0; i < nS; i += stride) o_S[i] = S[i];
   for (int64_t g = t0; g <= n_groups; g += stride) {
-    // lower bound of 80 g in the sorted salient list
+    // lower bound of the first column of 16-pack group g in the sorted
+    // salient list (layout 4: group g holds columns from 128 (g / 2) + 80 (g % 2))
     int64_t lo = 0, hi = nS;
-    const int64_t key = g * kGroupCols;
+    const int64_t key = g128 ? kScaleCols * (g >> 1) + kGroupCols * (g & 1) : g * kGroupCols;
     while (lo < hi) {
       const int64_t mid = (lo + hi) / 2;
       if (S[mid] < key)
@@ -200,6 +203,64 @@ __global__ void write_header_kernel(uint8_t* packed, int64_t N, int64_t K, int64
   }
 }
 
+// Layout 4 trits: one thread per 16-byte unit (tile, 16-pack group dg, row).
+// Byte i of row l's unit holds pack slot 16 (dg % 2) + ((i + l) mod 16) of
+// quantization group dg / 2: slot p < 26 codes the group's columns
+// 5p..5p+4 (zero trits past its column 127 and past K), slots 26..31 the
+// all-zero code.
+__global__ void pack_trits128_kernel(const int8_t* __restrict__ trits, int64_t N, int64_t K,
+                                     int64_t n_groups, int64_t n_units, uint8_t* __restrict__ out) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < n_units; u += stride) {
+    const int64_t l = u % kTileRows;
+    const int64_t dg = (u / kTileRows) % n_groups;
+    const int64_t tile = u / (kTileRows * n_groups);
+    const int64_t r = tile * kTileRows + l, g = dg >> 1;
+    uint32_t w[4] = {kZeroCode4, kZeroCode4, kZeroCode4, kZeroCode4};
+    if (r < N) {
+      const int8_t* row = trits + r * K;
+      for (int i = 0; i < kGroupPacks; ++i) {
+        const int64_t p = kGroupPacks * (dg & 1) + ((i + l) & (kGroupPacks - 1));
+        if (p >= kScalePacks) continue;  // the all-zero code stays
+        uint32_t code = 0, pw = 1;
+        for (int e = 0; e < 5; ++e) {
+          const int64_t c = 5 * p + e, j = kScaleCols * g + c;
+          int t = (c < kScaleCols && j < K) ? row[j] : 0;
+          t = t < -1 ? -1 : (t > 1 ? 1 : t);  // invalid input is reported by validate_kernel
+          code += uint32_t(t + 1) * pw;
+          pw *= 3;
+        }
+        const int sh = 8 * (i & 3);
+        w[i >> 2] = (w[i >> 2] & ~(0xffu << sh)) | (code << sh);
+      }
+    }
+    const u32x4 v = {w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<u32x4*>(out + u * 16) = v;
+  }
+}
+
+// Layout 4 scales and rescales: (alpha | beta << 16) per row and group as
+// [n_pad/64][n_sg][64] (zero in padded rows), v in device column order
+// (column c of 16-pack group dg is slot 16 (dg % 2) + c / 5, column c % 5 of
+// that slot; zero in the padding).
+__global__ void pack_scales128_kernel(const uint16_t* __restrict__ alpha, const uint16_t* __restrict__ beta,
+                                      const uint16_t* __restrict__ v, int64_t N, int64_t K, int64_t n_pad,
+                                      int64_t n_sg, uint32_t* __restrict__ o_ab, uint16_t* __restrict__ o_v) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  const int64_t t0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (int64_t i = t0; i < n_pad * n_sg; i += stride) {
+    const int64_t tile = i / (n_sg * kTileRows), rem = i - tile * n_sg * kTileRows;
+    const int64_t g = rem / kTileRows, r = tile * kTileRows + rem % kTileRows;
+    o_ab[i] = r < N ? uint32_t(alpha[r * n_sg + g]) | (uint32_t(beta[r * n_sg + g]) << 16) : 0u;
+  }
+  for (int64_t i = t0; i < 2 * n_sg * kGroupCols; i += stride) {
+    const int64_t dg = i / kGroupCols, col = i % kGroupCols;
+    const int64_t p = kGroupPacks * (dg & 1) + col / 5, c = 5 * p + col % 5;
+    const int64_t j = kScaleCols * (dg >> 1) + c;
+    o_v[i] = (p < kScalePacks && c < kScaleCols && j < K) ? v[j] : uint16_t(0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Debug unpack (bit-exact read-back of the layout).
 // ---------------------------------------------------------------------------
@@ -219,6 +280,29 @@ __global__ void unpack_codes_kernel(const uint8_t* __restrict__ tr, int64_t N, i
       for (int d = 0; d < 5; ++d) {
         const int64_t j = 5 * p + d;
         if (j < K) trits[r * K + j] = int8_t(int(rest % 3) - 1);
+        rest /= 3;
+      }
+    }
+  }
+}
+
+// Layout 4: the paper's codes [N][26 n_sg] (26 per row and group) and trits.
+__global__ void unpack_codes128_kernel(const uint8_t* __restrict__ tr, int64_t N, int64_t K,
+                                       int64_t n_packs, int64_t n_groups, uint8_t* __restrict__ canon,
+                                       int8_t* __restrict__ trits) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < N * n_packs; e += stride) {
+    const int64_t r = e / n_packs, pp = e % n_packs;
+    const int64_t g = pp / kScalePacks, p = pp % kScalePacks;
+    const int64_t tile = r / kTileRows, l = r % kTileRows, dg = 2 * g + p / kGroupPacks;
+    const int64_t i = ((p % kGroupPacks) - l) & (kGroupPacks - 1);
+    const uint8_t c = tr[((tile * n_groups + dg) * kTileRows + l) * 16 + i];
+    if (canon) canon[e] = c;
+    if (trits) {
+      uint32_t rest = c;
+      for (int d = 0; d < 5; ++d) {
+        const int64_t col = 5 * p + d, j = kScaleCols * g + col;
+        if (col < kScaleCols && j < K) trits[r * K + j] = int8_t(int(rest % 3) - 1);
         rest /= 3;
       }
     }
@@ -1020,17 +1104,20 @@ int qtea_packed_bytes_e4m3(int64_t N, int64_t K, int64_t n_salient, int64_t* out
 
 namespace {
 
-// The two pack entry points: layout 2 takes a salient list and fp16
-// residual values, layout 3 a salient bitmap and E4M3 residual bytes.
+// The pack entry points: layout 2 takes a salient list and fp16 residual
+// values, layout 3 a salient bitmap and E4M3 residual bytes, layout 4 that
+// and per-row, per-128-column-group scales and biases (row_scale and
+// row_bias [N][ceil(K/128)]).
 int pack_any(int layout, const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_scale,
-             const uint16_t* col_rescale, const int32_t* salient, const uint32_t* bitmap,
-             int64_t n_salient, const void* resid_val, const uint8_t* resid_idx, void* packed,
-             int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
+             const uint16_t* row_bias, const uint16_t* col_rescale, const int32_t* salient,
+             const uint32_t* bitmap, int64_t n_salient, const void* resid_val, const uint8_t* resid_idx,
+             void* packed, int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
   Layout L;
   if (!out_desc) return QTEA_ERR_INVALID_ARG;
   out_desc->magic = 0;
   if (!make_layout(N, K, n_salient, &L, layout)) return QTEA_ERR_INVALID_ARG;
   if (!trits || !row_scale || !col_rescale || !packed) return QTEA_ERR_INVALID_ARG;
+  if (layout == kLayoutG128 && !row_bias) return QTEA_ERR_INVALID_ARG;
   if (n_salient > 0 && (!resid_val || !resid_idx)) return QTEA_ERR_INVALID_ARG;
   if (layout == kLayout ? (n_salient > 0 && !salient) : !bitmap) return QTEA_ERR_INVALID_ARG;
   if (packed_bytes < L.total) return QTEA_ERR_WORKSPACE;
@@ -1046,28 +1133,37 @@ int pack_any(int layout, const int8_t* trits, int64_t N, int64_t K, const uint16
   hipLaunchKernelGGL(validate_kernel, dim3(grid_for(N * K, 256 * 16)), dim3(256), 0, st, trits, N * K,
                      resid_idx, ni, layout == kLayout ? salient : nullptr,
                      layout == kLayout ? n_salient : int64_t(0), K, flags);
-  if (layout == kLayoutE4M3) {
+  if (layout != kLayout) {
     hipLaunchKernelGGL(bitmap_salient_kernel, dim3(1), dim3(1024), 0, st, bitmap, K, n_salient, o_S, flags);
     salient = o_S;
   }
   const int64_t n_units = L.n_tiles * L.n_groups * kTileRows;
-  hipLaunchKernelGGL(pack_trits_kernel, dim3(grid_for(n_units)), dim3(256), 0, st, trits, N, K,
-                     L.n_groups, n_units, pk + L.off_trits);
+  if (layout == kLayoutG128) {
+    const int64_t n_sg = L.n_groups / 2;
+    hipLaunchKernelGGL(pack_trits128_kernel, dim3(grid_for(n_units)), dim3(256), 0, st, trits, N, K,
+                       L.n_groups, n_units, pk + L.off_trits);
+    hipLaunchKernelGGL(pack_scales128_kernel, dim3(grid_for(L.n_pad * n_sg)), dim3(256), 0, st, row_scale,
+                       row_bias, col_rescale, N, K, L.n_pad, n_sg, reinterpret_cast<uint32_t*>(pk + L.off_alpha),
+                       reinterpret_cast<uint16_t*>(pk + L.off_v));
+  } else {
+    hipLaunchKernelGGL(pack_trits_kernel, dim3(grid_for(n_units)), dim3(256), 0, st, trits, N, K,
+                       L.n_groups, n_units, pk + L.off_trits);
+  }
   const int64_t meta_n = L.n_pad + L.n_groups * kGroupCols + n_salient * (L.n_pad / 4);
-  uint16_t* o_alpha = reinterpret_cast<uint16_t*>(pk + L.off_alpha);
-  uint16_t* o_v = reinterpret_cast<uint16_t*>(pk + L.off_v);
+  uint16_t* o_alpha = layout == kLayoutG128 ? nullptr : reinterpret_cast<uint16_t*>(pk + L.off_alpha);
+  uint16_t* o_v = layout == kLayoutG128 ? nullptr : reinterpret_cast<uint16_t*>(pk + L.off_v);
   int32_t* o_spos = reinterpret_cast<int32_t*>(pk + L.off_spos);
   uint32_t* o_ridx = reinterpret_cast<uint32_t*>(pk + L.off_ridx);
   if (layout == kLayout)
     hipLaunchKernelGGL(pack_meta_kernel<uint16_t>, dim3(grid_for(meta_n)), dim3(256), 0, st, row_scale,
                        col_rescale, salient, static_cast<const uint16_t*>(resid_val), resid_idx, N, K,
                        n_salient, L.n_pad, L.n_groups, o_alpha, o_v, o_S, o_spos,
-                       reinterpret_cast<uint16_t*>(pk + L.off_rval), o_ridx, flags);
+                       reinterpret_cast<uint16_t*>(pk + L.off_rval), o_ridx, flags, 0);
   else
     hipLaunchKernelGGL(pack_meta_kernel<uint8_t>, dim3(grid_for(meta_n)), dim3(256), 0, st, row_scale,
                        col_rescale, salient, static_cast<const uint8_t*>(resid_val), resid_idx, N, K,
                        n_salient, L.n_pad, L.n_groups, o_alpha, o_v, o_S, o_spos, pk + L.off_rval, o_ridx,
-                       flags);
+                       flags, int(layout == kLayoutG128));
   if (hipGetLastError() != hipSuccess) return QTEA_ERR_HIP;
   uint32_t hflags = 0;
   if (hipMemcpyAsync(&hflags, flags, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return QTEA_ERR_HIP;
@@ -1104,7 +1200,7 @@ int qtea_pack(const int8_t* trits, int64_t N, int64_t K, const uint16_t* row_sca
               const uint16_t* col_rescale, const int32_t* salient, int64_t n_salient,
               const uint16_t* resid_val, const uint8_t* resid_idx, void* packed,
               int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
-  return pack_any(kLayout, trits, N, K, row_scale, col_rescale, salient, nullptr, n_salient, resid_val,
+  return pack_any(kLayout, trits, N, K, row_scale, nullptr, col_rescale, salient, nullptr, n_salient, resid_val,
                   resid_idx, packed, packed_bytes, out_desc, stream);
 }
 
@@ -1112,12 +1208,27 @@ int qtea_pack_e4m3(const int8_t* trits, int64_t N, int64_t K, const uint16_t* ro
                    const uint16_t* col_rescale, const uint32_t* salient_bitmap, int64_t n_salient,
                    const uint8_t* resid_val, const uint8_t* resid_idx, void* packed, int64_t packed_bytes,
                    qtea_desc* out_desc, void* stream) {
-  return pack_any(kLayoutE4M3, trits, N, K, row_scale, col_rescale, nullptr, salient_bitmap, n_salient,
+  return pack_any(kLayoutE4M3, trits, N, K, row_scale, nullptr, col_rescale, nullptr, salient_bitmap, n_salient,
                   resid_val, resid_idx, packed, packed_bytes, out_desc, stream);
 }
 
+int qtea_packed_bytes_g128(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes) {
+  Layout L;
+  if (!out_bytes || !make_layout(N, K, n_salient, &L, kLayoutG128)) return QTEA_ERR_INVALID_ARG;
+  *out_bytes = L.total;
+  return QTEA_OK;
+}
+
+int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* group_scale,
+                   const uint16_t* group_bias, const uint16_t* col_rescale, const uint32_t* salient_bitmap,
+                   int64_t n_salient, const uint8_t* resid_val, const uint8_t* resid_idx, void* packed,
+                   int64_t packed_bytes, qtea_desc* out_desc, void* stream) {
+  return pack_any(kLayoutG128, trits, N, K, group_scale, group_bias, col_rescale, nullptr, salient_bitmap,
+                  n_salient, resid_val, resid_idx, packed, packed_bytes, out_desc, stream);
+}
+
 int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes) {
-  if (!out_bytes || !desc_ok(desc)) return QTEA_ERR_INVALID_ARG;
+  if (!out_bytes || !desc_ok(desc) || desc->layout == kLayoutG128) return QTEA_ERR_INVALID_ARG;
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
   *out_bytes = workspace_need(*desc, batch);
   return QTEA_OK;
@@ -1136,6 +1247,7 @@ int qtea_workspace_init(void* workspace, int64_t bytes, void* stream) {
 int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
                        float* Y, void* workspace, int64_t workspace_bytes, void* stream) {
   if (!desc_ok(desc) || !packed || !X || !Y) return QTEA_ERR_INVALID_ARG;
+  if (desc->layout == kLayoutG128) return QTEA_ERR_INVALID_ARG;  // grouped entry points only
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
   const qtea_desc& d = *desc;
   const Plan pl = make_plan(d, batch);
@@ -1206,7 +1318,10 @@ int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_
   const qtea_desc& d = *desc;
   const uint8_t* pk = static_cast<const uint8_t*>(packed);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (canon_codes || trits)
+  if ((canon_codes || trits) && d.layout == kLayoutG128)
+    hipLaunchKernelGGL(unpack_codes128_kernel, dim3(grid_for(d.N * d.n_packs)), dim3(256), 0, st,
+                       pk + d.off_trits, d.N, d.K, d.n_packs, d.n_groups, canon_codes, trits);
+  else if (canon_codes || trits)
     hipLaunchKernelGGL(unpack_codes_kernel, dim3(grid_for(d.N * d.n_packs)), dim3(256), 0, st,
                        pk + d.off_trits, d.N, d.K, d.n_packs, d.n_groups, canon_codes, trits);
   if (resid_row && d.n_salient > 0)

@@ -21,6 +21,13 @@ constexpr int kThreads = kWaves * 64;
 constexpr uint32_t kZeroCode4 = 0x79797979u;  // four copies of code 121 (all-zero trits)
 constexpr int kLayout = 2;      // residual values fp16
 constexpr int kLayoutE4M3 = 3;  // residual values FP8 E4M3 (one byte each)
+// The paper's format: per row and 128-column group a scale alpha and a bias
+// beta, the group's 128 trits in 26 one-byte packs, E4M3 residual values.
+// On the device a group takes 32 pack slots (two 16-pack groups), slots
+// 26..31 holding the all-zero code.
+constexpr int kLayoutG128 = 4;
+constexpr int kScaleCols = 128;  // columns per quantization group
+constexpr int kScalePacks = 26;  // packs per quantization group (25 of five columns, one of three)
 constexpr int64_t kAlign = 256;
 constexpr int64_t kHeaderBytes = 256;
 constexpr int kFlagOffset = 128;
@@ -76,25 +83,31 @@ __device__ __forceinline__ float h2f(uint16_t h) {
 // Layout arithmetic shared by the host entry points.
 // ---------------------------------------------------------------------------
 struct Layout {
-  int64_t value_bytes;  // bytes per residual value: 2 (fp16, layout 2) or 1 (E4M3, layout 3)
+  int64_t value_bytes;  // bytes per residual value: 2 (fp16, layout 2) or 1 (E4M3, layouts 3 and 4)
   int64_t n_packs, n_groups, n_pad, n_tiles;
   int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx, total;
 };
 
+// Layout 4 differs in three regions: trits hold two 16-pack groups per
+// 128-column group; "alpha" holds u32 (alpha | beta << 16) per row and group
+// as [n_pad/64][n_groups/2][64]; v is in device column order (80 per
+// 16-pack group, zero in the padding slots).  n_packs is the paper's count
+// (26 per group).
 inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L, int layout = kLayout) {
   if (N < 4 || N % 4 != 0 || K < 1 || nS < 0 || nS > K) return false;
-  if (layout != kLayout && layout != kLayoutE4M3) return false;
-  L->value_bytes = layout == kLayoutE4M3 ? 1 : 2;
-  if (N > (int64_t(1) << 31) - 64 || K > (int64_t(1) << 31) - 80) return false;
-  L->n_packs = cdiv(K, 5);
-  L->n_groups = cdiv(L->n_packs, kGroupPacks);
+  if (layout != kLayout && layout != kLayoutE4M3 && layout != kLayoutG128) return false;
+  L->value_bytes = layout == kLayout ? 2 : 1;
+  const bool g128 = layout == kLayoutG128;
+  if (N > (int64_t(1) << 31) - 64 || K > (int64_t(1) << 31) - 160) return false;
+  L->n_packs = g128 ? kScalePacks * cdiv(K, kScaleCols) : cdiv(K, 5);
+  L->n_groups = g128 ? 2 * cdiv(K, kScaleCols) : cdiv(L->n_packs, kGroupPacks);
   L->n_pad = align_up(N, kTileRows);
   L->n_tiles = L->n_pad / kTileRows;
   int64_t o = kHeaderBytes;
   L->off_trits = o;
   o = align_up(o + L->n_pad * L->n_groups * kGroupPacks, kAlign);
   L->off_alpha = o;
-  o = align_up(o + 2 * L->n_pad, kAlign);
+  o = align_up(o + (g128 ? 2 * L->n_pad * L->n_groups : 2 * L->n_pad), kAlign);
   L->off_v = o;
   o = align_up(o + 2 * L->n_groups * kGroupCols, kAlign);
   L->off_salient = o;

@@ -20,7 +20,10 @@ available; shapes follow Llama-3-8B, Qwen3-14B and Llama-3-70B linears):
     a uniformly drawn position 0..3 in the group;
   * for the paper's residual storage (resid="e4m3"): the same R draw rounded
     to FP8 E4M3 (RNE, by torch's float8_e4m3fn conversion) and given as
-    codes, and the salient set given as a column bitmap.
+    codes, and the salient set given as a column bitmap;
+  * for the paper's 128-column quantization groups (groups=128): a scale
+    alpha[r][g] ~ U(0.01, 0.03) and a bias beta[r][g] ~ U(-0.005, 0.005)
+    per row and group, rounded to fp16.
 """
 from __future__ import annotations
 
@@ -36,7 +39,7 @@ _SRC = os.path.join(_HERE, "synth_gen.c")
 _LIB = os.path.join(_HERE, "libsynth.so")
 
 # Field tags of the per-(seed, layer, matrix) streams.
-FIELD_TRITS, FIELD_SALIENT, FIELD_RIDX, FIELD_RVAL, FIELD_ALPHA, FIELD_V, FIELD_X = range(1, 8)
+FIELD_TRITS, FIELD_SALIENT, FIELD_RIDX, FIELD_RVAL, FIELD_ALPHA, FIELD_V, FIELD_X, FIELD_BETA = range(1, 9)
 
 DEFAULT_SEED = 20260224
 
@@ -162,13 +165,14 @@ def column_bitmap(S, K: int) -> np.ndarray:
 
 
 def layer_inputs(seed, layer, mat, N, K, p0=Fraction(2, 5), frac=Fraction(2, 100),
-                 with_trits=True, rows=None, resid="fp16") -> dict:
+                 with_trits=True, rows=None, resid="fp16", groups=0) -> dict:
     """All non-activation inputs of one compressed N x K matrix.
 
     Returns numpy arrays: trits int8 [N][K] (omitted if with_trits is False),
     alpha fp16 [N], v fp16 [K], S int32 [nS] (sorted), R fp16 [nS][N/4],
     idx uint8 [nS][N/4]; with resid="e4m3" R is replaced by R8, uint8 E4M3
-    codes [nS][N/4], and bitmap, int32 [ceil(K/32)], is added.
+    codes [nS][N/4], and bitmap, int32 [ceil(K/32)], is added; with
+    groups=128, alpha_g and beta_g fp16 [N][ceil(K/128)] are added.
     """
     if N % 4:
         raise ValueError("N must be a multiple of 4 (1:4 residual groups)")
@@ -189,6 +193,12 @@ def layer_inputs(seed, layer, mat, N, K, p0=Fraction(2, 5), frac=Fraction(2, 100
         "S": S,
         "idx": idx.reshape(nS, G),
     }
+    if groups:
+        if groups != 128:
+            raise ValueError("quantization groups of 128 columns only")
+        ng = (K + 127) // 128
+        out["alpha_g"] = uniform_f16(key(seed, layer, mat, FIELD_ALPHA), N * ng, 0.01, 0.03).reshape(N, ng)
+        out["beta_g"] = uniform_f16(key(seed, layer, mat, FIELD_BETA), N * ng, -0.005, 0.005).reshape(N, ng)
     if resid == "e4m3":
         out["R8"] = normal_e4m3(key(seed, layer, mat, FIELD_RVAL), nS * G, 0.0, 0.01).reshape(nS, G)
         out["bitmap"] = column_bitmap(S, K)

@@ -20,6 +20,7 @@ class Workload:
     frac: Fraction = Fraction(2, 100)
     note: str = ""
     resid: str = "fp16"  # residual value storage: "fp16" or "e4m3"
+    groups: int = 0  # columns per quantization group (0: one group per row)
 
     def matrices(self):
         """Yield (layer, mat, role, N, K) in per-token execution order."""
@@ -50,6 +51,11 @@ WORKLOADS = {
     "llama3_8b_stack_e4m3": Workload("llama3_8b_stack_e4m3", LLAMA3_8B, 32, (1, 4),
                                      frac=Fraction(5, 100), resid="e4m3",
                                      note="32-layer Llama-3-8B-shaped stack, 5% salient, E4M3 residual"),
+    # the paper's full format: 128-column groups with scale and bias, 26-byte
+    # packs, 5% salient columns with E4M3 residual values and a bitmap
+    "llama3_8b_stack_g128": Workload("llama3_8b_stack_g128", LLAMA3_8B, 32, (1,),
+                                     frac=Fraction(5, 100), resid="e4m3", groups=128,
+                                     note="32-layer Llama-3-8B-shaped stack in the paper's grouped format"),
 }
 
 ORDER = ["gemv_4096x4096", "llama3_8b_layer", "llama3_8b_stack", "qwen3_14b_stack", "llama3_70b_stack"]

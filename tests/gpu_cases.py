@@ -198,3 +198,61 @@ def gpu_pack_e4m3(case, dev="cuda"):
     return q.pack_matrix_e4m3(to_dev(case["trits"], dev), to_dev(case["alpha"], dev), to_dev(case["v"], dev),
                               to_dev(synth.column_bitmap(case["S"], case["K"]), dev), int(case["S"].size),
                               to_dev(case["R8"], dev), to_dev(case["idx"], dev))
+
+
+# ---------------------------------------------------------------------------
+# The paper's grouped format: 128-column groups with a scale and a bias.
+# ---------------------------------------------------------------------------
+def g128_dyadic_case(seed, N, K, B, nS):
+    """e4m3_dyadic_case plus dyadic group scales 2^-e and biases k/64: every
+    product and partial sum, the groups' sums of x included, stays exact in
+    fp32."""
+    c = e4m3_dyadic_case(seed, N, K, B, nS)
+    rng = np.random.default_rng(seed + 11)
+    ng = (K + 127) // 128
+    c["alpha_g"] = (2.0 ** -rng.integers(0, 6, size=(N, ng))).astype(np.float16)
+    c["beta_g"] = (rng.integers(-8, 9, size=(N, ng)) / 64.0).astype(np.float16)
+    return c
+
+
+def g128_synth_case(seed, N, K, B, frac=Fraction(5, 100), layer=0, mat=0):
+    L = synth.layer_inputs(seed, layer, mat, N, K, frac=frac, resid="e4m3", groups=128)
+    L["R"] = oracle.e4m3_as_half(L["R8"])
+    L["x"] = synth.activations(seed, layer, mat, B, K)
+    return L
+
+
+def gpu_pack_g128(case, dev="cuda"):
+    import paper_2609_00224_amd as q
+
+    return q.pack_matrix_g128(to_dev(case["trits"], dev), to_dev(case["alpha_g"], dev), to_dev(case["beta_g"], dev),
+                              to_dev(case["v"], dev), to_dev(synth.column_bitmap(case["S"], case["K"]), dev),
+                              int(case["S"].size), to_dev(case["R8"], dev), to_dev(case["idx"], dev))
+
+
+def oracle_rows_g128(case, rows=None, need_wmax=True, block=512):
+    """fp64 oracle outputs of the grouped format and, per row, max |W_eff|
+    (alpha[r][g] v_j T[r][j] plus the residual) for the tolerance."""
+    N, K = case["N"], case["K"]
+    if rows is None:
+        rows = np.arange(N, dtype=np.int64)
+    codes = oracle.pack128(case["trits"][rows])
+    y = oracle.gemv128(N, K, codes, case["alpha_g"], case["beta_g"], case["v"], case["S"], case["R"],
+                       case["idx"], case["x"], rows=rows)
+    if not need_wmax:
+        return y, None
+    wmax = np.empty(rows.size)
+    ng = (K + 127) // 128
+    v = case["v"].astype(np.float64)
+    for i in range(0, rows.size, block):
+        sl = rows[i:i + block]
+        a = np.repeat(case["alpha_g"][sl].astype(np.float64), 128, axis=1)[:, :K]
+        W = a * v[None, :] * case["trits"][sl].astype(np.float64)
+        G = N // 4
+        for s, col in enumerate(case["S"]):
+            hit = case["idx"][s, sl // 4] == (sl % 4)
+            W[hit, col] += case["R"][s, sl[hit] // 4].astype(np.float64)
+        # the bias acts like a weight beta[r][g] on every column of the group
+        W = np.maximum(np.abs(W), np.repeat(np.abs(case["beta_g"][sl].astype(np.float64)), 128, axis=1)[:, :K])
+        wmax[i:i + block] = W.max(axis=1)
+    return y, wmax

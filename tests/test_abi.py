@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert q.qtea_abi_version() == 3
+    assert q.qtea_abi_version() == 4
     assert q.qtea_status_string(0) == "ok"
     for s in range(-6, 0):
         assert q.qtea_status_string(s) != "unknown status"
@@ -99,3 +99,21 @@ def test_grouped_info_mirror_size():
 def test_algorithmic_bytes_e4m3_matches_oracle():
     for N, K, nS in [(4096, 4096, 205), (8192, 28672, 1434), (4, 1, 0)]:
         assert q.algorithmic_bytes(N, K, nS, value_bytes=1) == oracle.algorithmic_bytes_vb(N, K, nS, 1)
+
+
+def test_g128_packed_bytes_and_host_checks(lib):
+    # 26 packs per 128 columns take 32 device slots; scales and biases 4 bytes per row and group
+    n = q.qtea_packed_bytes_g128(4096, 4096, 205)
+    assert n % 256 == 0 and n >= 4096 * 32 * 32 + 4 * 4096 * 32
+    with pytest.raises(q.QteaError) as e:
+        q.qtea_packed_bytes_g128(6, 10, 0)
+    assert e.value.status == q.QTEA_ERR_INVALID_ARG
+    dd = q.QteaDesc()
+    assert lib.qtea_pack_g128(None, 4, 4, None, None, None, None, 0, None, None, None, 0, ctypes.byref(dd),
+                              None) == q.QTEA_ERR_INVALID_ARG
+    assert dd.magic == 0
+
+
+def test_algorithmic_bytes_g128_matches_oracle():
+    for N, K, nS in [(4096, 4096, 205), (8192, 28672, 1434), (4, 1, 0), (12, 300, 15)]:
+        assert q.algorithmic_bytes_g128(N, K, nS) == oracle.algorithmic_bytes128(N, K, nS, 1)

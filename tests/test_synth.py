@@ -74,7 +74,10 @@ def st_shapes():
 
 def test_workload_table():
     assert [w for w in WORKLOADS] == ["gemv_4096x4096", "llama3_8b_layer", "llama3_8b_stack",
-                                      "qwen3_14b_stack", "llama3_70b_stack", "llama3_8b_stack_e4m3"]
+                                      "qwen3_14b_stack", "llama3_70b_stack", "llama3_8b_stack_e4m3",
+                                      "llama3_8b_stack_g128"]
+    g = WORKLOADS["llama3_8b_stack_g128"]
+    assert g.groups == 128 and g.resid == "e4m3" and g.frac == Fraction(5, 100)
     e8 = WORKLOADS["llama3_8b_stack_e4m3"]
     assert e8.resid == "e4m3" and e8.frac == Fraction(5, 100) and e8.shapes == st_shapes()
     assert all(WORKLOADS[n].resid == "fp16" for n in list(WORKLOADS)[:5])
@@ -100,3 +103,12 @@ def test_e4m3_residual_inputs():
     R8 = oracle.e4m3_decode(L["R8"])
     step = np.maximum(2.0 ** (np.floor(np.log2(np.maximum(np.abs(R16), 2.0 ** -6))) - 3), 2.0 ** -9)
     assert np.all(np.abs(R8 - R16) <= 0.5 * step + 2.0 ** -12)
+
+
+def test_group128_inputs():
+    L = synth.layer_inputs(4, 0, 1, 64, 300, groups=128)
+    assert L["alpha_g"].shape == (64, 3) and L["beta_g"].shape == (64, 3)
+    a, b = L["alpha_g"].astype(np.float64), L["beta_g"].astype(np.float64)
+    assert a.min() >= 0.0099 and a.max() <= 0.0301
+    assert b.min() >= -0.00501 and b.max() <= 0.00501 and (b < 0).any() and (b > 0).any()
+    assert np.array_equal(L["trits"], synth.layer_inputs(4, 0, 1, 64, 300)["trits"])
