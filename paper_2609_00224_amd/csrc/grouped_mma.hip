@@ -38,8 +38,8 @@
 //     register);
 //   - ten MFMAs per row tile and column block: eight take digits 0-3 of two
 //     packs each, two take digit 4 of eight packs each; the B operands are
-//     per slice images in LDS in exactly the MFMA lane order, built one unit
-//     ahead from x and v;
+//     per slice images in LDS, one 16-byte slot per MFMA lane (slots swizzled
+//     per MFMA), built one unit ahead from x and v;
 //   - at the end of a panel part: scale by alpha, add the residual of the
 //     part's salient columns with one more MFMA per 32 of them (A = the 1:4
 //     residual expanded per row, B = x at the salient columns), add hi and
@@ -109,6 +109,14 @@ __device__ __forceinline__ void slot_of_col(int c, int& kb, int& mu, int& h) {
     h = pp & 7;
   }
 }
+
+// Slot of MFMA lane L's 16-byte B operand in MFMA mu's 1 KiB image block:
+// the low four bits of L are xored with mu.  The builders write 2-byte
+// halves, consecutive threads taking consecutive columns, which fall in
+// different MFMAs at one lane: unswizzled, those all sit 1 KiB apart, in
+// the same four banks; with the xor their dwords spread over the banks.
+// The MFMA lanes read the whole block either way.
+__device__ __forceinline__ constexpr int img_lane(int L, int mu) { return L ^ (mu & 15); }
 
 // The value of lane (l + 8) mod 16 of the lane's row of 16 (row_ror:8).
 __device__ __forceinline__ float dpp_ror8(float x) {
@@ -196,8 +204,9 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     int qb, mu, h;
     slot_of_col(pc[i], qb, mu, h);
     const int bb = pb[i] < BP ? pb[i] : 0;  // pairs past the image are not built
-    img_hi[i] = uint32_t(((mu * 64 + bb + 16 * qb) * 8 + h) * 2);
-    img_lo[i] = NB == 1 ? uint32_t(((mu * 64 + bb + 8 + 16 * qb) * 8 + h) * 2) : img_hi[i] + uint32_t(kImg);
+    img_hi[i] = uint32_t(((mu * 64 + img_lane(bb + 16 * qb, mu)) * 8 + h) * 2);
+    img_lo[i] = NB == 1 ? uint32_t(((mu * 64 + img_lane(bb + 8 + 16 * qb, mu)) * 8 + h) * 2)
+                        : img_hi[i] + uint32_t(kImg);
   }
   // loads through buffer resources over x [B][K] and v [n_groups * 80]:
   // reads past either return zero, which is the padding the images need
@@ -307,7 +316,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
         const int mu = i < 4 ? 4 * half + i : 8 + half;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
-          Bv[i][nb] = __builtin_bit_cast(half8, *(lds_u32x4*)(size_t(img + nb * kImg + (mu * 64 + lane) * 16)));
+          Bv[i][nb] = __builtin_bit_cast(half8, *(lds_u32x4*)(size_t(img + nb * kImg + (mu * 64 + img_lane(lane, mu)) * 16)));
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
