@@ -770,6 +770,11 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
     pr.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
     pr.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
     pr.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
+    {
+      Layout lm;  // regions the descriptor does not list
+      make_layout(d.N, d.K, d.n_salient, &lm, int(d.layout));  // succeeds: desc_ok checked it
+      pr.vs = reinterpret_cast<const uint32_t*>(pk + lm.off_vs);
+    }
     pr.x = x[src];
     pr.y = y[src];
     pr.N = d.N;

@@ -69,7 +69,11 @@ struct MLds {
   static constexpr int T4OFF = kTab;
   static constexpr int IMG = kTab + kT4Bytes;  // [2 buffers][NB] images
   static constexpr int FLAG = IMG + 2 * NB * kImg;    // int [3]: slice needs scaling
-  static constexpr int BYTES = FLAG + 16;
+  // the rest: the open panel part's activations at its salient columns,
+  // fp16 [part rank][8 NB batch rows], gathered as the slices are staged
+  static constexpr int XSAL = FLAG + 16;
+  static constexpr int XCAP = (160 * 1024 - XSAL) / (2 * 8 * NB);  // salient columns held
+  static constexpr int BYTES = XSAL + XCAP * 2 * 8 * NB;
 };
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
@@ -208,15 +212,18 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     img_lo[i] = NB == 1 ? uint32_t(((mu * 64 + img_lane(bb + 8 + 16 * qb, mu)) * 8 + h) * 2)
                         : img_hi[i] + uint32_t(kImg);
   }
-  // loads through buffer resources over x [B][K] and v [n_groups * 80]:
-  // reads past either return zero, which is the padding the images need
-  uint16_t xr[NPAIR], vr[NPAIR];
+  // loads through buffer resources over x [B][K] and vs [n_groups * 80] (v in
+  // the low half, 1 + the column's rank among its slice's salient columns in
+  // the high half, 0 if it is not salient): reads past either return zero,
+  // which is the padding the images need
+  uint16_t xr[NPAIR];
+  uint32_t vr[NPAIR];
   auto load_xv = [&](const Cursor cc) {
     const GProblem& pr = P[cc.m];
     const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(pr.x), 0, int(2 * uint32_t(B) * uint32_t(pr.K)), kBufferWord3);
     const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(pr.v), 0, int(2 * uint32_t(pr.n_groups) * kGroupCols), kBufferWord3);
+        const_cast<uint32_t*>(pr.vs), 0, int(4 * uint32_t(pr.n_groups) * kGroupCols), kBufferWord3);
     const int col0 = cc.slice * kSliceCols;
 #pragma unroll
     for (int i = 0; i < NPAIR; ++i) {
@@ -224,19 +231,24 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       // a column past K would read the next batch row: send it past the buffer instead
       const uint32_t xo = (pb[i] < B && col < pr.K) ? uint32_t(2 * (pb[i] * pr.K + col)) : 0x7ffffff0u;
       xr[i] = __builtin_amdgcn_raw_buffer_load_b16(xres, int(xo), 0, 0);
-      vr[i] = __builtin_amdgcn_raw_buffer_load_b16(vres, 2 * col, 0, 0);
+      vr[i] = __builtin_amdgcn_raw_buffer_load_b32(vres, 4 * col, 0, 0);
     }
   };
-  // build the B-operand images of slice cc into buffer bb (scale: 1 or 2^-16);
-  // returns whether any |a| of the slice is beyond the fp16 range at scale 1
-  auto build = [&](const Cursor cc, int bb, float scale) -> bool {
-    (void)cc;
+  // build the B-operand images of slice cc into buffer bb (scale: 1 or 2^-16),
+  // and put x at the slice's salient columns into the part's gather array
+  // from part rank xbase on; returns whether any |a| of the slice is beyond
+  // the fp16 range at scale 1
+  uint16_t* xsal = reinterpret_cast<uint16_t*>(lds + L::XSAL);
+  auto build = [&](int bb, float scale, int xbase) -> bool {
     char* img = lds + L::IMG + bb * NB * kImg;
     bool big = false;
 #pragma unroll
     for (int i = 0; i < NPAIR; ++i) {
       if (tid + kMT * i < kSliceCols * BP) {
-        const float a = float(__builtin_bit_cast(_Float16, vr[i])) * float(__builtin_bit_cast(_Float16, xr[i]));
+        const float a = float(__builtin_bit_cast(_Float16, uint16_t(vr[i] & 0xffffu))) *
+                        float(__builtin_bit_cast(_Float16, xr[i]));
+        const int rank = xbase + int(vr[i] >> 16) - 1;
+        if ((vr[i] >> 16) != 0u && rank < L::XCAP) xsal[rank * BP + pb[i]] = xr[i];
         big |= !(__builtin_fabsf(a) < 65504.0f);
         _Float16 hi, lo;
         split_hl(a * scale, hi, lo);
@@ -263,7 +275,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   for (int q = 0; q < 4; ++q)
     W[q] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, q)));
   load_xv(cur);
-  const bool big0 = build(cur, 0, 1.0f);
+  const bool big0 = build(0, 1.0f, 0);  // the run's first unit starts a part
   if (big0) bigf[0] = 1;
   __syncthreads();
 
@@ -292,7 +304,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       // rare: this slice's |a| reaches the fp16 range; rebuild its images
       // at 2^-16 and scale the running sums around its products
       load_xv(cur);
-      build(cur, sb, kBigScale);
+      build(sb, kBigScale, cptr(pr.spos)[cur.slice * kSliceGroups] - cptr(pr.spos)[pstart_slice * kSliceGroups]);
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -363,9 +375,6 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     }
 
     // the next unit's images into the other buffer
-    if (has_next) {
-      if (build(nxt, sb ^ 1, 1.0f)) bigf[(it + 1) % 3] = 1;
-    }
 
     if (pend) {
       // 1. alpha of the lane's rows: slot v of tile q is row 16 kb + 4q + v
@@ -397,8 +406,9 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       const int s_lo = cptr(pr.spos)[g0], s_hi = cptr(pr.spos)[g1];
       // Every load of an iteration is issued before any of its values is
       // used (indices clamped into the part's range, unused slots masked
-      // afterwards), so an iteration waits on memory twice: S and the
-      // residual words, then x at the salient columns.
+      // afterwards).  The activations at the salient columns come from the
+      // gather array when the part's salient columns fit in it (one wait on
+      // memory per iteration), else from x through the salient list (two).
       gi32* Sp = gptr(pr.S);
       gu16* xp = gptr(pr.x) + uint32_t(min(jr, B - 1)) * uint32_t(pr.K);
       // the lane's four values of a column: 8 bytes (fp16) or 4 (E4M3)
@@ -407,23 +417,38 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       gu32* rip = gptr(pr.ridx) + uint32_t(tlc) * uint32_t(pr.nS);
       const uint32_t psh = 8u * uint32_t(jr >> 2);
       const uint32_t bmask = (jr < B && jr < BP) ? 0xffffu : 0u;
+      const bool gathered = s_hi - s_lo <= L::XCAP;  // uniform
+      const uint16_t* xg = xsal + min(jr, BP - 1);
       for (int s0 = s_lo; s0 < s_hi; s0 += 32) {
-        int col[8];
         u32x2 rv[8];
         uint32_t pw[8];
-#pragma unroll
-        for (int h = 0; h < 8; ++h) {
-          const uint32_t sc = uint32_t(min(s0 + 8 * kb + h, s_hi - 1));
-          col[h] = Sp[sc];
-          if constexpr (F8)
-            rv[h].x = *reinterpret_cast<gu32*>(rvp + 16u * sc);  // converted where used
-          else
-            rv[h] = *reinterpret_cast<gu32x2*>(rvp + 32u * sc);
-          pw[h] = rip[sc];
-        }
         uint16_t xb[8];
+        if (gathered) {
 #pragma unroll
-        for (int h = 0; h < 8; ++h) xb[h] = xp[uint32_t(col[h])];
+          for (int h = 0; h < 8; ++h) {
+            const uint32_t sc = uint32_t(min(s0 + 8 * kb + h, s_hi - 1));
+            if constexpr (F8)
+              rv[h].x = *reinterpret_cast<gu32*>(rvp + 16u * sc);  // converted where used
+            else
+              rv[h] = *reinterpret_cast<gu32x2*>(rvp + 32u * sc);
+            pw[h] = rip[sc];
+            xb[h] = xg[(sc - uint32_t(s_lo)) * BP];
+          }
+        } else {
+          int col[8];
+#pragma unroll
+          for (int h = 0; h < 8; ++h) {
+            const uint32_t sc = uint32_t(min(s0 + 8 * kb + h, s_hi - 1));
+            col[h] = Sp[sc];
+            if constexpr (F8)
+              rv[h].x = *reinterpret_cast<gu32*>(rvp + 16u * sc);
+            else
+              rv[h] = *reinterpret_cast<gu32x2*>(rvp + 32u * sc);
+            pw[h] = rip[sc];
+          }
+#pragma unroll
+          for (int h = 0; h < 8; ++h) xb[h] = xp[uint32_t(col[h])];
+        }
         // B: x[j][S_s] in the hi columns (j < min(B, BP)), zero elsewhere;
         // A: the value of four-row group 4 (jr >> 2) + q in row jr & 3 only
         _Float16 bx[8], ar[4][8];
@@ -481,6 +506,16 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) C[q][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       }
+    }
+    // the next unit's images into the other buffer, after the part end's
+    // reads of the gather array (a next unit after a part end starts a new
+    // part and refills it from rank 0)
+    if (pend && has_next) __syncthreads();
+    if (has_next) {
+      const int xb_n = nxt.slice == 0 ? 0
+                                      : cptr(pr.spos)[nxt.slice * kSliceGroups] -
+                                            cptr(pr.spos)[pstart_slice * kSliceGroups];
+      if (build(sb ^ 1, 1.0f, xb_n)) bigf[(it + 1) % 3] = 1;
     }
     __syncthreads();  // the next unit's images are complete; this unit's are free
     cur = nxt;

@@ -30,7 +30,7 @@ struct GProblem {
   int64_t N, K, n_pad;
   int32_t n_groups, nS, n_slices, n_panels;
   int64_t unit_base;
-  int64_t reserved;
+  const uint32_t* vs;  // v | (1 + rank in the slice's salient run) << 16, per device column
 };
 static_assert(sizeof(GProblem) == 128, "plan record size");
 

@@ -261,6 +261,31 @@ __global__ void pack_scales128_kernel(const uint16_t* __restrict__ alpha, const 
   }
 }
 
+// The vs region (u32 per device column): pass 1 copies the v bits, pass 2
+// marks every salient column with 1 + its rank among the salient columns of
+// its 320-column slice (device columns; layout 4 maps column j to device
+// column 160 (j / 128) + j % 128).
+__global__ void pack_vs_kernel(const uint16_t* __restrict__ o_v, int64_t n_cols, uint32_t* __restrict__ o_vs) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_cols; i += stride) o_vs[i] = o_v[i];
+}
+// A salient list that failed validation (reported by the pack's flags) may
+// hold any value: every index is checked before it is used.
+__global__ void mark_salient_kernel(const int32_t* __restrict__ S, const int32_t* __restrict__ spos, int64_t nS,
+                                    int64_t K, int64_t n_groups, int g128, uint32_t* __restrict__ o_vs) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; s < nS; s += stride) {
+    const int64_t j = S[s];
+    if (j < 0 || j >= K) continue;
+    const int64_t dc = g128 ? 160 * (j / kScaleCols) + j % kScaleCols : j;
+    const int64_t g0 = 4 * (dc / (4 * kGroupCols));
+    if (dc >= n_groups * kGroupCols || g0 > n_groups) continue;
+    const int64_t rank = s - spos[g0];
+    if (rank < 0 || rank >= 4 * kGroupCols) continue;
+    o_vs[dc] |= uint32_t(rank + 1) << 16;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Debug unpack (bit-exact read-back of the layout).
 // ---------------------------------------------------------------------------
@@ -1164,6 +1189,15 @@ int pack_any(int layout, const int8_t* trits, int64_t N, int64_t K, const uint16
                        col_rescale, salient, static_cast<const uint8_t*>(resid_val), resid_idx, N, K,
                        n_salient, L.n_pad, L.n_groups, o_alpha, o_v, o_S, o_spos, pk + L.off_rval, o_ridx,
                        flags, int(layout == kLayoutG128));
+  {
+    uint32_t* o_vs = reinterpret_cast<uint32_t*>(pk + L.off_vs);
+    const uint16_t* v_dev = reinterpret_cast<const uint16_t*>(pk + L.off_v);
+    const int64_t n_cols = L.n_groups * kGroupCols;
+    hipLaunchKernelGGL(pack_vs_kernel, dim3(grid_for(n_cols)), dim3(256), 0, st, v_dev, n_cols, o_vs);
+    if (n_salient > 0)
+      hipLaunchKernelGGL(mark_salient_kernel, dim3(grid_for(n_salient)), dim3(256), 0, st, o_S, o_spos, n_salient,
+                         K, L.n_groups, int(layout == kLayoutG128), o_vs);
+  }
   if (hipGetLastError() != hipSuccess) return QTEA_ERR_HIP;
   uint32_t hflags = 0;
   if (hipMemcpyAsync(&hflags, flags, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return QTEA_ERR_HIP;

@@ -85,7 +85,9 @@ __device__ __forceinline__ float h2f(uint16_t h) {
 struct Layout {
   int64_t value_bytes;  // bytes per residual value: 2 (fp16, layout 2) or 1 (E4M3, layouts 3 and 4)
   int64_t n_packs, n_groups, n_pad, n_tiles;
-  int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx, total;
+  int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx;
+  int64_t off_vs;  // u32 per device column: v | (1 + rank in its slice's salient run) << 16
+  int64_t total;
 };
 
 // Layout 4 differs in three regions: trits hold two 16-pack groups per
@@ -118,6 +120,11 @@ inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L, int layout 
   o = align_up(o + L->value_bytes * nS * (L->n_pad / 4), kAlign);
   L->off_ridx = o;
   o = align_up(o + 4 * nS * (L->n_pad / 64), kAlign);
+  // The v bits again, with each salient column's rank among the salient
+  // columns of its 320-column slice (0: not salient): the matrix-core kernel
+  // gathers the activations of salient columns as it stages a slice.
+  L->off_vs = o;
+  o = align_up(o + 4 * L->n_groups * kGroupCols, kAlign);
   L->total = o;
   return true;
 }
