@@ -186,6 +186,44 @@ def traffic_per_launch(kernel, algorithmic_bytes, workload="llama3_8b_stack batc
         return None
 
 
+def read_ceiling(dev, stream, nbytes=2 << 30, reps=10):
+    """GB/s of the library's plain streaming-read kernel over a buffer far
+    beyond the last-level cache (16-byte non-temporal loads, nothing else)."""
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    buf = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    with torch.cuda.stream(stream):
+        for _ in range(3):
+            q.qtea_read_ceiling(buf, sink, stream=stream)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            q.qtea_read_ceiling(buf, sink, stream=stream)
+        e1.record(stream)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del buf
+    return nbytes / (ms * 1e-3) / 1e9
+
+
+def gpu_clock():
+    """Current shader clock level as the driver reports it, if readable."""
+    import glob
+
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            for line in open(path):
+                if "*" in line:
+                    return line.split(":", 1)[1].replace("*", "").strip()
+        except OSError:
+            continue
+    return None
+
+
 def copy_calibration(nbytes, dev):
     """A plain device copy of known size, for scaling the HBM counters."""
     import torch
@@ -359,6 +397,11 @@ def main():
                "launches_per_step": len(mats), "us_per_launch": round(ms_chain * 1e3 / len(mats), 3),
                "per_role": roles} if not args.grouped_only else None
 
+    clock_after = gpu_clock()
+    ceiling = read_ceiling(dev, stream)
+    log(f"streaming-read ceiling {ceiling:.1f} GB/s; this path {gbs / ceiling:.1%} of it")
+    trit_bytes = sum(m["N"] * m["pm"].desc.n_packs for m in mats)
+    device_bytes = sum(int(m["pm"].desc.bytes_total) for m in mats)
     if grouped:  # leave the grouped outputs in y for the oracle comparison
         with torch.cuda.stream(stream):
             gg.replay()
@@ -387,6 +430,11 @@ def main():
         "us_per_token": round(ms * 1e3, 2),
         "us_per_token_single_replays": spread,
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "read_ceiling": {"gbs": round(ceiling, 1), "frac": round(gbs / ceiling, 4),
+                         "kernel": "read_ceiling_kernel", "bytes": 2 << 30},
+        "trit_bytes_per_token": trit_bytes, "trit_gbs": round(trit_bytes / (ms * 1e-3) / 1e9, 2),
+        "device_bytes_per_token": device_bytes, "device_gbs": round(device_bytes / (ms * 1e-3) / 1e9, 2),
+        "shader_clock_after_timing": clock_after,
         "execution": "grouped" if grouped else "chained",
         "chained": chained,
         "roofline": roof,

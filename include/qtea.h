@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 4
+#define QTEA_ABI_VERSION 5
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -204,6 +204,16 @@ int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, floa
  */
 int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
                        float* Y, void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * Measurement support: stream `bytes` (a multiple of 16) of a device buffer
+ * from HBM with the same 16-byte non-temporal loads the GEMV kernels use,
+ * and nothing else (a fold of the data goes to *sink, device uint32, so the
+ * reads are not removed).  The rate of this kernel on a buffer far beyond the
+ * last-level cache is the streaming-read ceiling the GEMV rates are compared
+ * with.  Does not synchronize.  Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_HIP.
+ */
+int qtea_read_ceiling(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
 
 /*
  * Test support: read the packed buffer back into plain form, bit for bit.

@@ -9,7 +9,7 @@ There is no CPU fallback: if the library is not built, loading it raises.
 Entry points carry the C names: qtea_packed_bytes, qtea_pack,
 qtea_packed_bytes_e4m3, qtea_pack_e4m3, qtea_packed_bytes_g128, qtea_pack_g128,
 qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
-qtea_debug_unpack, qtea_status_string, qtea_abi_version,
+qtea_debug_unpack, qtea_read_ceiling, qtea_status_string, qtea_abi_version,
 qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv.
 """
 from __future__ import annotations
@@ -37,6 +37,7 @@ EXPORTS = (
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
     "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
     "qtea_packed_bytes_e4m3", "qtea_pack_e4m3", "qtea_packed_bytes_g128", "qtea_pack_g128",
+    "qtea_read_ceiling",
 )
 QTEA_LAYOUT_FP16 = 2  # residual values fp16
 QTEA_LAYOUT_E4M3 = 3  # residual values FP8 E4M3
@@ -112,6 +113,8 @@ def load(path: str = LIB_PATH):
     lib.qtea_gemv.argtypes = [pdesc, vp, vp, vp, vp, i64, vp]
     lib.qtea_gemm_lowbatch.restype = i32
     lib.qtea_gemm_lowbatch.argtypes = [pdesc, vp, vp, i32, vp, vp, i64, vp]
+    lib.qtea_read_ceiling.restype = i32
+    lib.qtea_read_ceiling.argtypes = [vp, i64, vp, vp]
     lib.qtea_debug_unpack.restype = i32
     lib.qtea_debug_unpack.argtypes = [pdesc, vp, vp, vp, vp, vp]
     pinfo = ctypes.POINTER(QteaGroupedInfo)
@@ -279,6 +282,13 @@ def qtea_gemm_lowbatch(desc: QteaDesc, packed, X, batch: int, Y, workspace, stre
     _check(load().qtea_gemm_lowbatch(ctypes.byref(desc), _ptr(packed), _ptr(X), int(batch), _ptr(Y),
                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
                                      _stream(stream)), "qtea_gemm_lowbatch")
+
+
+def qtea_read_ceiling(buf, sink, stream=None):
+    """Stream the whole device buffer `buf` once (see include/qtea.h)."""
+    _need_cuda(buf, sink)
+    _check(load().qtea_read_ceiling(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)),
+           "qtea_read_ceiling")
 
 
 def qtea_debug_unpack(desc: QteaDesc, packed, canon_codes=None, trits=None, resid_row=None,

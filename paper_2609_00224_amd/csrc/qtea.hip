@@ -286,6 +286,37 @@ __global__ void mark_salient_kernel(const int32_t* __restrict__ S, const int32_t
   }
 }
 
+// Streaming-read ceiling: grid-stride 16-byte non-temporal loads, eight in
+// flight per thread, 32 workgroups of 256 per CU (the fastest of the shapes
+// measured), folded into one word per thread and one atomic per workgroup.
+constexpr int kCeilUnroll = 8;
+constexpr int kCeilWgPerCu = 32;
+__global__ __launch_bounds__(256) void read_ceiling_kernel(const u32x4* __restrict__ buf, int64_t n16,
+                                                           uint32_t* __restrict__ sink) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  uint32_t f = 0;
+  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (; i + (kCeilUnroll - 1) * stride < n16; i += kCeilUnroll * stride) {
+    u32x4 v[kCeilUnroll];
+#pragma unroll
+    for (int k = 0; k < kCeilUnroll; ++k) v[k] = __builtin_nontemporal_load(buf + i + k * stride);
+#pragma unroll
+    for (int k = 0; k < kCeilUnroll; ++k) f ^= v[k].x + v[k].y + v[k].z + v[k].w;
+  }
+  for (; i < n16; i += stride) {
+    const u32x4 a = __builtin_nontemporal_load(buf + i);
+    f ^= a.x + a.y + a.z + a.w;
+  }
+  __shared__ uint32_t red[256];
+  red[threadIdx.x] = f;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int k = 0; k < 256; ++k) t ^= red[k];
+    atomicXor(sink, t);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Debug unpack (bit-exact read-back of the layout).
 // ---------------------------------------------------------------------------
@@ -1344,6 +1375,18 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
 int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y, void* workspace,
               int64_t workspace_bytes, void* stream) {
   return qtea_gemm_lowbatch(desc, packed, x, 1, y, workspace, workspace_bytes, stream);
+}
+
+int qtea_read_ceiling(const void* buf, int64_t bytes, uint32_t* sink, void* stream) {
+  if (!buf || !sink || bytes <= 0 || bytes % 16 != 0 || (reinterpret_cast<uintptr_t>(buf) & 15))
+    return QTEA_ERR_INVALID_ARG;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return QTEA_ERR_HIP;
+  hipLaunchKernelGGL(read_ceiling_kernel, dim3(kCeilWgPerCu * cus), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const u32x4*>(buf), bytes / 16, sink);
+  return hipGetLastError() == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
 }
 
 int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_codes, int8_t* trits,

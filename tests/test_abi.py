@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert q.qtea_abi_version() == 4
+    assert q.qtea_abi_version() == 5
     assert q.qtea_status_string(0) == "ok"
     for s in range(-6, 0):
         assert q.qtea_status_string(s) != "unknown status"
@@ -117,3 +117,9 @@ def test_g128_packed_bytes_and_host_checks(lib):
 def test_algorithmic_bytes_g128_matches_oracle():
     for N, K, nS in [(4096, 4096, 205), (8192, 28672, 1434), (4, 1, 0), (12, 300, 15)]:
         assert q.algorithmic_bytes_g128(N, K, nS) == oracle.algorithmic_bytes128(N, K, nS, 1)
+
+
+def test_read_ceiling_host_checks(lib):
+    for args in [(None, 16, None, None), (ctypes.c_void_p(16), 15, ctypes.c_void_p(64), None),
+                 (ctypes.c_void_p(8), 16, ctypes.c_void_p(64), None), (ctypes.c_void_p(16), 0, ctypes.c_void_p(64), None)]:
+        assert lib.qtea_read_ceiling(*args) == q.QTEA_ERR_INVALID_ARG
