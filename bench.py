@@ -281,6 +281,14 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
             t_oracle += time.perf_counter() - t0
         passes += 1
     us_token = t_oracle / passes * 1e6
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {
         "value": round(token_bytes * passes / t_oracle / 1e9, 4),
         "unit": "GB/s",
@@ -290,6 +298,7 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
                   f"{token_bytes / 1e9:.3f} GB of packed weights each), {t_oracle:.1f} s of oracle time",
         "us_per_token": round(us_token, 1),
         "gpu_vs_oracle_max_rel_l2": worst,
+        "host": {"cpu_model": model, "usable_cores": len(os.sched_getaffinity(0)), "nproc": os.cpu_count()},
     }
 
 
