@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 5
+#define QTEA_ABI_VERSION 6
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -208,11 +208,18 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
 /*
  * Measurement support: stream `bytes` (a multiple of 16) of a device buffer
  * from HBM with the same 16-byte non-temporal loads the GEMV kernels use,
- * and nothing else (a fold of the data goes to *sink, device uint32, so the
- * reads are not removed).  The rate of this kernel on a buffer far beyond the
- * last-level cache is the streaming-read ceiling the GEMV rates are compared
- * with.  Does not synchronize.  Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_HIP.
+ * and nothing else: each workgroup reads one contiguous chunk of
+ * QTEA_READ_CEILING_CHUNK bytes (the last one may be shorter) and stores its
+ * fold to sink[chunk] (device uint32 [ceil(bytes / QTEA_READ_CEILING_CHUNK)],
+ * caller-owned; the fold is the XOR over the chunk's 16-byte words of the
+ * 32-bit sum of their four little-endian u32 lanes, so the reads are not
+ * removed and can be checked).  The rate of this kernel on a buffer far
+ * beyond the last-level cache, held under load, is the streaming-read
+ * ceiling the GEMV rates are compared with.  Does not synchronize.
+ * Errors: QTEA_ERR_INVALID_ARG (null pointer, size not a positive multiple
+ * of 16, buffer not 16-byte aligned), QTEA_ERR_HIP.
  */
+#define QTEA_READ_CEILING_CHUNK 65536
 int qtea_read_ceiling(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
 
 /*

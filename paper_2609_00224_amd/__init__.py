@@ -284,11 +284,23 @@ def qtea_gemm_lowbatch(desc: QteaDesc, packed, X, batch: int, Y, workspace, stre
                                      _stream(stream)), "qtea_gemm_lowbatch")
 
 
+READ_CEILING_CHUNK = 65536  # QTEA_READ_CEILING_CHUNK
+
+
+def read_ceiling_sink_words(nbytes: int) -> int:
+    """Words of the sink qtea_read_ceiling needs for a buffer of nbytes."""
+    return -(-int(nbytes) // READ_CEILING_CHUNK)
+
+
 def qtea_read_ceiling(buf, sink, stream=None):
-    """Stream the whole device buffer `buf` once (see include/qtea.h)."""
+    """Stream the whole device buffer `buf` once; sink (device, 4-byte
+    elements, at least read_ceiling_sink_words(bytes of buf)) receives one
+    fold per chunk (see include/qtea.h)."""
     _need_cuda(buf, sink)
-    _check(load().qtea_read_ceiling(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)),
-           "qtea_read_ceiling")
+    nbytes = buf.numel() * buf.element_size()
+    if sink.element_size() != 4 or sink.numel() < read_ceiling_sink_words(nbytes):
+        raise ValueError("qtea_read_ceiling: sink needs one 4-byte word per 64 KiB chunk of buf")
+    _check(load().qtea_read_ceiling(_ptr(buf), nbytes, _ptr(sink), _stream(stream)), "qtea_read_ceiling")
 
 
 def qtea_debug_unpack(desc: QteaDesc, packed, canon_codes=None, trits=None, resid_row=None,

@@ -829,7 +829,12 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
     ranges[0] = 0;
     while (u < total_units) {
       const int64_t rem = total_cost - prefix[size_t(u)];
-      const int64_t target = std::max<int64_t>(unit_min, rem / (int64_t(kGuide) * G));
+      // every chunk but the last covers at least half its target, so a
+      // target of twice the remaining cost per remaining chunk of the budget
+      // finishes within the budget with chunks of equal cost, instead of
+      // leaving the whole rest to one workgroup
+      const int64_t left = max_chunks - n_chunks;
+      const int64_t target = std::max({unit_min, rem / (int64_t(kGuide) * G), 2 * rem / left});
       int64_t e = u;
       if (n_chunks + 1 == max_chunks) {
         e = total_units;  // chunk budget spent: the rest is one chunk

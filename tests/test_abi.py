@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert q.qtea_abi_version() == 5
+    assert q.qtea_abi_version() == 6
     assert q.qtea_status_string(0) == "ok"
     for s in range(-6, 0):
         assert q.qtea_status_string(s) != "unknown status"
