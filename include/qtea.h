@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 6
+#define QTEA_ABI_VERSION 7
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -54,6 +54,8 @@ enum qtea_status {
   QTEA_ERR_BATCH = -4,       /* batch outside [1, QTEA_MAX_BATCH]            */
   QTEA_ERR_WORKSPACE = -5,   /* workspace or packed buffer too small         */
   QTEA_ERR_HIP = -6,         /* a HIP runtime call or kernel launch failed   */
+  QTEA_ERR_NOT_POSITIVE = -7,/* a Hessian that is not positive definite
+                                (qtea_quantize, include/qtea_quant.h)      */
 };
 
 /*

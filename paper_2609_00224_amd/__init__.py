@@ -2,7 +2,8 @@
 
 The binding marshals arguments only: every step of the GEMV runs in the HIP
 kernels of ``csrc/qtea.hip``, ``csrc/grouped.hip`` and ``csrc/grouped_mma.hip``
-behind the C ABI of ``include/qtea.h``.  Torch
+behind the C ABI of ``include/qtea.h``, and every step of the offline
+quantizer in those of ``csrc/quant.hip`` behind ``include/qtea_quant.h``.  Torch
 is used to allocate device memory and to name the current HIP stream.
 There is no CPU fallback: if the library is not built, loading it raises.
 
@@ -10,7 +11,8 @@ Entry points carry the C names: qtea_packed_bytes, qtea_pack,
 qtea_packed_bytes_e4m3, qtea_pack_e4m3, qtea_packed_bytes_g128, qtea_pack_g128,
 qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
 qtea_debug_unpack, qtea_read_ceiling, qtea_status_string, qtea_abi_version,
-qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv.
+qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv,
+qtea_quant_hessian, qtea_quant_workspace_bytes, qtea_quantize.
 """
 from __future__ import annotations
 
@@ -28,6 +30,8 @@ QTEA_ERR_BAD_RESIDUAL = -3
 QTEA_ERR_BATCH = -4
 QTEA_ERR_WORKSPACE = -5
 QTEA_ERR_HIP = -6
+QTEA_ERR_NOT_POSITIVE = -7
+QTEA_QUANT_GROUP = 128
 QTEA_MAX_BATCH = 16
 QTEA_DESC_MAGIC = 0x51544541
 
@@ -37,7 +41,7 @@ EXPORTS = (
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
     "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
     "qtea_packed_bytes_e4m3", "qtea_pack_e4m3", "qtea_packed_bytes_g128", "qtea_pack_g128",
-    "qtea_read_ceiling",
+    "qtea_read_ceiling", "qtea_quant_hessian", "qtea_quant_workspace_bytes", "qtea_quantize",
 )
 QTEA_LAYOUT_FP16 = 2  # residual values fp16
 QTEA_LAYOUT_E4M3 = 3  # residual values FP8 E4M3
@@ -66,6 +70,14 @@ class QteaGroupedInfo(ctypes.Structure):
         ("n_chunks", ctypes.c_int32), ("n_split_panels", ctypes.c_int32),
         ("layout", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("n_units", ctypes.c_int64), ("plan_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+    ]
+
+
+class QteaQuantParams(ctypes.Structure):
+    """Mirror of struct qtea_quant_params (include/qtea_quant.h)."""
+    _fields_ = [
+        ("n_salient", ctypes.c_int64), ("lambda_decay", ctypes.c_double), ("damp", ctypes.c_double),
+        ("iters", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
 
@@ -125,6 +137,13 @@ def load(path: str = LIB_PATH):
                                       i32, i32, vp, i64, pinfo, vp]
     lib.qtea_grouped_gemv.restype = i32
     lib.qtea_grouped_gemv.argtypes = [pinfo, vp, vp, i64, vp]
+    lib.qtea_quant_hessian.restype = i32
+    lib.qtea_quant_hessian.argtypes = [vp, i64, i64, vp, vp]
+    lib.qtea_quant_workspace_bytes.restype = i32
+    lib.qtea_quant_workspace_bytes.argtypes = [i64, i64, ctypes.POINTER(i64)]
+    lib.qtea_quantize.restype = i32
+    lib.qtea_quantize.argtypes = [vp, vp, i64, i64, ctypes.POINTER(QteaQuantParams),
+                                  vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, vp]
     _lib = lib
     return lib
 
@@ -441,3 +460,63 @@ def algorithmic_bytes(N: int, K: int, n_salient: int, value_bytes: int = 2) -> i
     entries = (N // 4) * n_salient
     return (N * ((K + 4) // 5) + value_bytes * entries + (2 * entries + 7) // 8 + 2 * N + 2 * K
             + 4 * n_salient)
+
+
+# ---------------------------------------------------------------------------
+# Offline quantizer (include/qtea_quant.h).
+# ---------------------------------------------------------------------------
+def qtea_quant_hessian(X, H, stream=None):
+    """H [K][K] fp64 = (2/n) X^T X for X [n][K] fp32 (device tensors)."""
+    import torch
+
+    _need_cuda(X, H)
+    if X.dtype != torch.float32 or H.dtype != torch.float64 or X.dim() != 2 or H.shape != (X.shape[1], X.shape[1]):
+        raise ValueError("qtea_quant_hessian: X fp32 [n][K], H fp64 [K][K]")
+    _check(load().qtea_quant_hessian(_ptr(X), X.shape[0], X.shape[1], _ptr(H), _stream(stream)), "qtea_quant_hessian")
+
+
+def qtea_quant_workspace_bytes(N: int, K: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load().qtea_quant_workspace_bytes(N, K, ctypes.byref(out)), "qtea_quant_workspace_bytes")
+    return int(out.value)
+
+
+def qtea_quantize(W, H, params: QteaQuantParams, T, alpha, beta, v, S, bitmap, R8, idx, Q, workspace, stream=None):
+    """Quantize W [N][K] (fp64) with Hessian H [K][K] (fp64) into the given
+    output tensors (see include/qtea_quant.h); synchronizes the stream."""
+    _need_cuda(W, H, T, alpha, beta, v, S, bitmap, R8, idx, Q, workspace)
+    N, K = W.shape
+    _check(load().qtea_quantize(_ptr(W), _ptr(H), N, K, ctypes.byref(params), _ptr(T), _ptr(alpha), _ptr(beta),
+                                _ptr(v), _ptr(S), _ptr(bitmap), _ptr(R8), _ptr(idx), _ptr(Q), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(stream)), "qtea_quantize")
+
+
+def quantize_matrix(W, H, n_salient, lambda_decay=1.0, iters=2, damp=0.01, want_q=False, stream=None):
+    """Allocate the outputs and a workspace and quantize one matrix; returns
+    a dict of device tensors (T, alpha, beta, v, S, bitmap, R8, idx, Q)."""
+    import torch
+
+    if W.dtype != torch.float64 or H.dtype != torch.float64:
+        raise ValueError("quantize_matrix: W and H are fp64")
+    N, K = W.shape
+    dev = W.device
+    G = -(-K // QTEA_QUANT_GROUP)
+    out = {
+        "T": torch.empty((N, K), dtype=torch.int8, device=dev),
+        "alpha": torch.empty((N, G), dtype=torch.float16, device=dev),
+        "beta": torch.empty((N, G), dtype=torch.float16, device=dev),
+        "v": torch.empty(K, dtype=torch.float16, device=dev),
+        "S": torch.empty(max(int(n_salient), 1), dtype=torch.int32, device=dev),
+        "bitmap": torch.empty(-(-K // 32), dtype=torch.int32, device=dev),
+        "R8": torch.empty((max(int(n_salient), 1), N // 4), dtype=torch.uint8, device=dev),
+        "idx": torch.empty((max(int(n_salient), 1), N // 4), dtype=torch.uint8, device=dev),
+        "Q": torch.empty((N, K), dtype=torch.float64, device=dev) if want_q else None,
+    }
+    ws = torch.empty(qtea_quant_workspace_bytes(N, K), dtype=torch.uint8, device=dev)
+    params = QteaQuantParams(int(n_salient), float(lambda_decay), float(damp), int(iters), 0)
+    qtea_quantize(W, H, params, out["T"], out["alpha"], out["beta"], out["v"], out["S"], out["bitmap"], out["R8"],
+                  out["idx"], out["Q"], ws, stream=stream)
+    out["S"] = out["S"][:int(n_salient)]
+    out["R8"] = out["R8"][:int(n_salient)]
+    out["idx"] = out["idx"][:int(n_salient)]
+    return out

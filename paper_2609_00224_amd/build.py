@@ -8,7 +8,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", f) for f in ("qtea.hip", "grouped.hip", "grouped_mma.hip")]
+SRCS = [os.path.join(HERE, "csrc", f) for f in ("qtea.hip", "grouped.hip", "grouped_mma.hip", "quant.hip")]
 LIB = os.path.join(HERE, "libqtea.so")
 ARCH = "gfx950"
 

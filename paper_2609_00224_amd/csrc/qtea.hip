@@ -1143,6 +1143,7 @@ const char* qtea_status_string(int status) {
     case QTEA_ERR_BATCH: return "batch outside [1, 16]";
     case QTEA_ERR_WORKSPACE: return "workspace or packed buffer too small";
     case QTEA_ERR_HIP: return "HIP runtime error";
+    case QTEA_ERR_NOT_POSITIVE: return "Hessian not positive definite";
     default: return "unknown status";
   }
 }

@@ -1,0 +1,863 @@
+// QTEA offline quantizer for gfx950 (include/qtea_quant.h), fp64 throughout.
+//
+// Steps of one qtea_quantize call, all on the caller's stream:
+//   1. salient columns (Eq. 3): per-column max of W^2 (atomic max on the
+//      bit patterns of non-negative doubles), times diag(H)^2; each column's
+//      rank counted against every other column (exact, deterministic ties);
+//      one workgroup compacts the selected columns in ascending order.
+//   2. damped Hessian H_d (dead columns fixed), then U with H_d^-1 = U^T U:
+//      H_d = V V^T with V upper (Cholesky from the last column backwards,
+//      32-column blocks: diagonal block in LDS, panel by per-row triangular
+//      solves, symmetric rank-32 update of the leading block), and U = V^-1
+//      (diagonal blocks inverted in LDS, then block rows from the bottom up,
+//      each a product with the rows already inverted).  U is the upper
+//      Cholesky factor of H_d^-1 (unique with a positive diagonal).
+//   3. W transposed into the workspace (column j contiguous over rows, dead
+//      columns zeroed); per 128-column block: the rows' group scale and bias,
+//      then the columns one by one (one thread per row): codes, rescale
+//      refinement (Eq. 4-5, its column mean summed over workgroups in a fixed
+//      order by the next launch), the 1:4 residual, the decayed GPTQ error
+//      (Eq. 6-9) and its update of the block's later columns; after the
+//      block, the trailing columns' rank-128 update.
+// Floating-point contraction is off in this file: every product and sum is
+// rounded as written, in the order the method states it.
+#include <math.h>
+
+#include "qtea_internal.h"
+#include "qtea_quant.h"
+
+#pragma clang fp contract(off)
+
+namespace {
+
+constexpr int kQG = QTEA_QUANT_GROUP;  // columns per group and per GPTQ block
+constexpr int kNB = 32;                // factorization block
+constexpr int kCT = 256;               // threads of the row-parallel kernels
+constexpr int64_t kQAlign = 256;
+constexpr int64_t kQMaxRows = 65536;
+constexpr int64_t kQMaxCols = 65536;
+
+inline int64_t q_up(int64_t x) { return (x + kQAlign - 1) / kQAlign * kQAlign; }
+inline int64_t q_cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct QLayout {
+  int64_t wt, a, u, et, score, flag, rank, dmean, scal, part, vst, total;
+};
+
+// Workspace regions (bytes from the start, 256-byte aligned).
+QLayout q_layout(int64_t N, int64_t K) {
+  QLayout L;
+  int64_t o = 0;
+  L.wt = o;    o = q_up(o + K * N * 8);                 // fp64 [K][N] current weights
+  L.a = o;     o = q_up(o + K * K * 8);                 // fp64 [K][K] H_d, then V (upper)
+  L.u = o;     o = q_up(o + K * K * 8);                 // fp64 [K][K] U (upper, zero below)
+  L.et = o;    o = q_up(o + int64_t(kQG) * N * 8);      // fp64 [128][N] decayed errors of a block
+  L.score = o; o = q_up(o + K * 8);                     // u64/fp64 [K] max W^2, then scores
+  L.flag = o;  o = q_up(o + K * 4);                     // int32 [K] selected
+  L.rank = o;  o = q_up(o + K * 4);                     // int32 [K] salient rank or -1
+  L.dmean = o; o = q_up(o + q_cdiv(K, kQG) * 8);        // fp64 per block: mean of diag U
+  L.scal = o;  o = q_up(o + 64);                        // fp64 mean diag H; int32 status at +8
+  L.part = o;  o = q_up(o + 2 * q_cdiv(N, kCT) * 2 * 8);  // fp64 [2][workgroups][2] column partials
+  L.vst = o;   o = q_up(o + 2 * 8);                     // fp64 [2] previous v
+  L.total = o;
+  return L;
+}
+
+// fp64 -> fp16 bits, nearest with ties to even (subnormals included,
+// magnitudes from 65520 up become infinity); the sign follows x.
+__device__ uint16_t f64_to_f16(double x) {
+  const uint16_t s = signbit(x) ? 0x8000 : 0;
+  const double m = fabs(x);
+  if (isnan(x)) return 0x7E00;
+  if (m >= 65520.0) return s | 0x7C00;
+  if (m < 0x1p-14) return s | uint16_t(rint(m * 0x1p24));  // units of 2^-24; 1024 is 2^-14
+  int e;
+  frexp(m, &e);
+  e -= 1;  // 2^e <= m < 2^(e+1)
+  const int k = int(rint(ldexp(m, 10 - e)));  // 1024..2048 (2048 carries into the exponent)
+  return s | uint16_t(((e + 15) << 10) + (k - 1024));
+}
+
+__device__ double f16_to_f64(uint16_t h) {
+  const int e = (h >> 10) & 31, m = h & 1023;
+  double v = e == 0 ? ldexp(double(m), -24) : e == 31 ? INFINITY : ldexp(double(m + 1024), e - 25);
+  return (h & 0x8000) ? -v : v;
+}
+
+// fp64 -> OCP E4M3 (FN) code: nearest finite value with ties to the even
+// code, magnitudes above 448 saturate to 448; the sign bit follows x < 0.
+__device__ uint8_t f64_to_e4m3(double x) {
+  const uint8_t s = x < 0.0 ? 0x80 : 0;
+  const double m = fabs(x);
+  uint8_t c;
+  if (m > 448.0) {
+    c = 0x7E;
+  } else if (m < 0x1p-6) {
+    c = uint8_t(rint(m * 0x1p9));  // subnormal steps of 2^-9; 8 is 2^-6
+  } else {
+    int e;
+    frexp(m, &e);
+    e -= 1;                                    // -6..8
+    const int k = int(rint(ldexp(m, 3 - e)));  // 8..16 (16 carries into the exponent)
+    c = uint8_t(((e + 7) << 3) + (k - 8));
+  }
+  return s | c;
+}
+
+__device__ double e4m3_to_f64(uint8_t c) {
+  const int e = (c >> 3) & 15, m = c & 7;
+  const double v = e == 0 ? ldexp(double(m), -9) : ldexp(double(8 + m), e - 10);
+  return (c & 0x80) ? -v : v;
+}
+
+__device__ inline int tern(double x, double thr) { return x > thr ? 1 : (x < -thr ? -1 : 0); }
+
+// ---------------------------------------------------------------------------
+// Hessian and salient columns.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void hess_kernel(const float* __restrict__ X, int64_t n, int64_t K, double scale,
+                                                   double* __restrict__ H) {
+  __shared__ double xa[32][65], xb[32][65];
+  const int64_t a0 = int64_t(blockIdx.y) * 64, b0 = int64_t(blockIdx.x) * 64;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  double acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int64_t t0 = 0; t0 < n; t0 += 32) {
+    for (int e = threadIdx.x; e < 32 * 64; e += 256) {
+      const int tt = e >> 6, c = e & 63;
+      const int64_t t = t0 + tt;
+      xa[tt][c] = (t < n && a0 + c < K) ? double(X[t * K + a0 + c]) : 0.0;
+      xb[tt][c] = (t < n && b0 + c < K) ? double(X[t * K + b0 + c]) : 0.0;
+    }
+    __syncthreads();
+    for (int tt = 0; tt < 32; ++tt) {
+      double va[4], vb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        va[i] = xa[tt][ty + 16 * i];
+        vb[i] = xb[tt][tx + 16 * i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += va[i] * vb[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t a = a0 + ty + 16 * i, b = b0 + tx + 16 * j;
+      if (a < K && b < K) H[a * K + b] = scale * acc[i][j];
+    }
+}
+
+__global__ void fill_f64_kernel(double* __restrict__ p, int64_t n, double v) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+// max over a run of rows of W[r][j]^2, merged by an atomic max on the bits
+// (non-negative doubles order like their bit patterns)
+__global__ __launch_bounds__(256) void maxsq_kernel(const double* __restrict__ W, int64_t N, int64_t K,
+                                                    int64_t rows, unsigned long long* __restrict__ out) {
+  const int64_t j = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= K) return;
+  const int64_t r0 = int64_t(blockIdx.y) * rows, r1 = r0 + rows < N ? r0 + rows : N;
+  double m = 0.0;
+  for (int64_t r = r0; r < r1; ++r) {
+    const double w = W[r * K + j];
+    const double s = w * w;
+    m = s > m ? s : m;
+  }
+  atomicMax(out + j, static_cast<unsigned long long>(__double_as_longlong(m)));
+}
+
+// s_j = (max_i W_ij^2 * d_j) * d_j, d_j = H_jj, in place
+__global__ void score_kernel(double* __restrict__ s, const double* __restrict__ H, int64_t K) {
+  const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (j >= K) return;
+  const double d = H[j * K + j];
+  s[j] = (s[j] * d) * d;
+}
+
+// column j is selected when fewer than n_sel columns rank before it
+// (a larger score, or an equal score at a lower column)
+__global__ __launch_bounds__(256) void select_kernel(const double* __restrict__ s, int64_t K, int64_t n_sel,
+                                                     int32_t* __restrict__ flag) {
+  __shared__ double ts[1024];
+  const int64_t j = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const double sj = j < K ? s[j] : 0.0;
+  int64_t rank = 0;
+  for (int64_t k0 = 0; k0 < K; k0 += 1024) {
+    for (int e = threadIdx.x; e < 1024; e += 256) ts[e] = k0 + e < K ? s[k0 + e] : 0.0;
+    __syncthreads();
+    const int lim = K - k0 < 1024 ? int(K - k0) : 1024;
+    for (int e = 0; e < lim; ++e) {
+      const double sk = ts[e];
+      rank += (sk > sj || (sk == sj && k0 + e < j)) ? 1 : 0;
+    }
+    __syncthreads();
+  }
+  if (j < K) flag[j] = rank < n_sel ? 1 : 0;
+}
+
+// one workgroup: selected columns in ascending order, each column's rank
+// among them (or -1), and the bitmap
+__global__ __launch_bounds__(1024) void compact_kernel(const int32_t* __restrict__ flag, int64_t K, int64_t n_sel,
+                                                       int32_t* __restrict__ S, int32_t* __restrict__ rank,
+                                                       uint32_t* __restrict__ bitmap) {
+  __shared__ int32_t wsum[16];
+  __shared__ int32_t base_s;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (threadIdx.x == 0) base_s = 0;
+  __syncthreads();
+  for (int64_t c0 = 0; c0 < K; c0 += 1024) {
+    const int64_t j = c0 + threadIdx.x;
+    const int f = j < K ? flag[j] : 0;
+    const uint64_t bal = __ballot(f);
+    const int pre = __popcll(bal & ((1ull << lane) - 1));
+    if (lane == 0) wsum[wv] = __popcll(bal);
+    if (bitmap && j < K && (lane & 31) == 0) bitmap[j >> 5] = uint32_t(bal >> lane);
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < 16; ++w) {
+      off += w < wv ? wsum[w] : 0;
+      tot += wsum[w];
+    }
+    const int pos = base_s + off + pre;
+    if (j < K) {  // (pos < n_sel always holds unless a score is NaN)
+      rank[j] = f && pos < n_sel ? pos : -1;
+      if (f && pos < n_sel) S[pos] = int32_t(j);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) base_s += tot;
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Damped Hessian, its reverse Cholesky factor V and U = V^-1.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void diag_mean_kernel(const double* __restrict__ H, int64_t K,
+                                                        double* __restrict__ dm) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int64_t j = threadIdx.x; j < K; j += 256) {
+    const double d = H[j * K + j];
+    s += d == 0.0 ? 1.0 : d;
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int i = 0; i < 256; ++i) t += red[i];
+    dm[0] = t / double(K);
+  }
+}
+
+// upper triangle and diagonal of H_d = H (dead diagonal -> 1) + damp mean I
+__global__ void damp_copy_kernel(const double* __restrict__ H, int64_t K, const double* __restrict__ dm,
+                                 double damp, double* __restrict__ A) {
+  const double add = damp * dm[0];
+  for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < K * K; e += int64_t(gridDim.x) * blockDim.x) {
+    const int64_t p = e / K, q = e % K;
+    if (q < p) continue;
+    double h = H[e];
+    if (p == q) h = (h == 0.0 ? 1.0 : h) + add;
+    A[e] = h;
+  }
+}
+
+// diagonal block [c0, c0 + n) of the reverse factorization, in LDS: eliminate
+// columns from the last one down, then V = column / sqrt(pivot)
+__global__ __launch_bounds__(256) void chol_diag_kernel(double* __restrict__ A, int64_t K, int64_t c0, int n,
+                                                        int32_t* __restrict__ status) {
+  __shared__ double D[kNB][kNB + 1];
+  for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
+    const int p = e / kNB, q = e % kNB;
+    D[p][q] = (p <= q && q < n) ? A[(c0 + p) * K + c0 + q] : 0.0;
+  }
+  __syncthreads();
+  for (int c = n - 1; c >= 0; --c) {
+    double piv = D[c][c];
+    if (!(piv > 0.0)) {
+      if (threadIdx.x == 0) status[0] = 1;
+      piv = 1.0;
+    }
+    for (int e = threadIdx.x; e < c * c; e += 256) {
+      const int p = e / c, q = e % c;
+      if (p <= q) D[p][q] -= D[p][c] * (D[q][c] / piv);
+    }
+    __syncthreads();
+  }
+  for (int e = threadIdx.x; e < n * n; e += 256) {
+    const int p = e / n, c = e % n;
+    if (p <= c) {
+      const double piv = D[c][c];
+      A[(c0 + p) * K + c0 + c] = D[p][c] / (piv > 0.0 ? sqrt(piv) : 1.0);
+    }
+  }
+}
+
+// rows p < c0 of the 32 columns [c0, c0 + 32): solve x V_D^T = panel row
+__global__ __launch_bounds__(256) void chol_panel_kernel(double* __restrict__ A, int64_t K, int64_t c0) {
+  __shared__ double D[kNB][kNB + 1];
+  for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
+    const int p = e / kNB, q = e % kNB;
+    D[p][q] = p <= q ? A[(c0 + p) * K + c0 + q] : 0.0;
+  }
+  __syncthreads();
+  const int64_t p = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (p >= c0) return;
+  double* row = A + p * K + c0;
+  double x[kNB];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) x[c] = row[c];
+#pragma unroll
+  for (int c = kNB - 1; c >= 0; --c) {
+    double s = x[c];
+#pragma unroll
+    for (int k = c + 1; k < kNB; ++k) s -= x[k] * D[c][k];
+    x[c] = s / D[c][c];
+  }
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) row[c] = x[c];
+}
+
+// upper triangle of the leading c0 x c0 block -= panel panel^T (64 x 64 tiles)
+__global__ __launch_bounds__(256) void chol_trail_kernel(double* __restrict__ A, int64_t K, int64_t c0) {
+  const int64_t tp = blockIdx.y, tq = blockIdx.x;
+  if (tp > tq) return;
+  __shared__ double Pp[64][kNB + 1], Pq[64][kNB + 1];
+  const int64_t p0 = tp * 64, q0 = tq * 64;
+  for (int e = threadIdx.x; e < 64 * kNB; e += 256) {
+    const int i = e / kNB, k = e % kNB;
+    Pp[i][k] = p0 + i < c0 ? A[(p0 + i) * K + c0 + k] : 0.0;
+    Pq[i][k] = q0 + i < c0 ? A[(q0 + i) * K + c0 + k] : 0.0;
+  }
+  __syncthreads();
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  double acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int k = 0; k < kNB; ++k) {
+    double va[4], vb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      va[i] = Pp[ty + 16 * i][k];
+      vb[i] = Pq[tx + 16 * i][k];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] += va[i] * vb[j];
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t p = p0 + ty + 16 * i, q = q0 + tx + 16 * j;
+      if (p < c0 && q < c0 && p <= q) A[p * K + q] -= acc[i][j];
+    }
+}
+
+// Inverse blocks: block b covers rows/columns [max(0, K - 32(b+1)), K - 32b).
+__device__ inline void inv_block(int64_t K, int64_t b, int64_t* lo, int* n) {
+  const int64_t hi = K - kNB * b;
+  *lo = hi - kNB > 0 ? hi - kNB : 0;
+  *n = int(hi - *lo);
+}
+
+// U_bb = V_bb^-1 for every diagonal block (one workgroup each)
+__global__ __launch_bounds__(64) void trinv_diag_kernel(const double* __restrict__ A, int64_t K,
+                                                        double* __restrict__ U) {
+  __shared__ double Vd[kNB][kNB + 1], Ud[kNB][kNB + 1];
+  int64_t lo;
+  int n;
+  inv_block(K, blockIdx.x, &lo, &n);
+  for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
+    const int p = e / kNB, q = e % kNB;
+    Vd[p][q] = (p <= q && q < n) ? A[(lo + p) * K + lo + q] : 0.0;
+    Ud[p][q] = 0.0;
+  }
+  __syncthreads();
+  const int c = threadIdx.x;  // one column of the inverse per thread
+  if (c < n) {
+    Ud[c][c] = 1.0 / Vd[c][c];
+    for (int i = c - 1; i >= 0; --i) {
+      double s = 0.0;
+      for (int k = i + 1; k <= c; ++k) s += Vd[i][k] * Ud[k][c];
+      Ud[i][c] = -s / Vd[i][i];
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < n * n; e += 64) {
+    const int p = e / n, q = e % n;
+    if (p <= q) U[(lo + p) * K + lo + q] = Ud[p][q];
+  }
+}
+
+// block row b (rows [lo, hi)), columns [hi, K): U = -U_bb (V_b,right U_right)
+__global__ __launch_bounds__(256) void trinv_row_kernel(const double* __restrict__ A, int64_t K, int64_t b,
+                                                        double* __restrict__ U) {
+  __shared__ double Vs[kNB][kNB + 1], Us[kNB][65], At[kNB][65], Ud[kNB][kNB + 1];
+  int64_t lo;
+  int n;
+  inv_block(K, b, &lo, &n);
+  const int64_t hi = lo + n;
+  const int64_t j0 = hi + int64_t(blockIdx.x) * 64;
+  const int64_t kend = j0 + 64 < K ? j0 + 64 : K;  // U[k][j] = 0 for k > j
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  double acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int64_t k0 = hi; k0 < kend; k0 += kNB) {
+    for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
+      const int i = e / kNB, k = e % kNB;
+      Vs[i][k] = (i < n && k0 + k < kend) ? A[(lo + i) * K + k0 + k] : 0.0;
+    }
+    for (int e = threadIdx.x; e < kNB * 64; e += 256) {
+      const int k = e / 64, c = e % 64;
+      Us[k][c] = (k0 + k < kend && j0 + c < K) ? U[(k0 + k) * K + j0 + c] : 0.0;
+    }
+    __syncthreads();
+    for (int k = 0; k < kNB; ++k) {
+      double va[2], vb[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) va[i] = Vs[ty + 16 * i][k];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) vb[j] = Us[k][tx + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += va[i] * vb[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) At[ty + 16 * i][tx + 16 * j] = acc[i][j];
+  for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
+    const int p = e / kNB, q = e % kNB;
+    Ud[p][q] = (p <= q && q < n) ? U[(lo + p) * K + lo + q] : 0.0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = ty + 16 * i, c = tx + 16 * j;
+      if (r < n && j0 + c < K) {
+        double s = 0.0;
+        for (int m = r; m < n; ++m) s += Ud[r][m] * At[m][c];
+        U[(lo + r) * K + j0 + c] = -s;
+      }
+    }
+}
+
+// mean of diag U over each 128-column block
+__global__ void dmean_kernel(const double* __restrict__ U, int64_t K, double* __restrict__ dmean) {
+  const int64_t g = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (g * kQG >= K) return;
+  const int64_t b0 = g * kQG, b1 = b0 + kQG < K ? b0 + kQG : K;
+  double s = 0.0;
+  for (int64_t k = b0; k < b1; ++k) s += U[k * K + k];
+  dmean[g] = s / double(b1 - b0);
+}
+
+// Wt[k][r] = W[r][k], zero for a dead column (H_kk = 0)
+__global__ __launch_bounds__(256) void transpose_kernel(const double* __restrict__ W, int64_t N, int64_t K,
+                                                        const double* __restrict__ H, double* __restrict__ Wt) {
+  __shared__ double tile[32][33];
+  const int64_t k0 = int64_t(blockIdx.x) * 32, r0 = int64_t(blockIdx.y) * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int i = ty; i < 32; i += 8) {
+    const int64_t r = r0 + i, k = k0 + tx;
+    tile[i][tx] = (r < N && k < K) ? W[r * K + k] : 0.0;
+  }
+  __syncthreads();
+  for (int i = ty; i < 32; i += 8) {
+    const int64_t k = k0 + i, r = r0 + tx;
+    if (k < K && r < N) Wt[k * N + r] = H[k * K + k] == 0.0 ? 0.0 : tile[tx][i];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Column-by-column quantization.
+// ---------------------------------------------------------------------------
+// one row's scale and bias of block g from the current weights
+__global__ __launch_bounds__(kCT) void group_params_kernel(const double* __restrict__ Wt, int64_t N, int64_t K,
+                                                           int64_t G, int64_t g, uint16_t* __restrict__ alpha,
+                                                           uint16_t* __restrict__ beta) {
+  const int64_t r = int64_t(blockIdx.x) * kCT + threadIdx.x;
+  if (r >= N) return;
+  const int64_t b0 = g * kQG, b1 = b0 + kQG < K ? b0 + kQG : K;
+  const double n = double(b1 - b0);
+  const double* w = Wt + b0 * N + r;
+  double sw = 0.0;
+  for (int64_t k = 0; k < b1 - b0; ++k) sw += w[k * N];
+  double be = sw / n, sa = 0.0;
+  for (int64_t k = 0; k < b1 - b0; ++k) sa += fabs(w[k * N] - be);
+  double al = sa / n;
+  for (int round = 0; round < 2; ++round) {
+    if (!(al > 0.0)) break;
+    const double thr = al / 2.0;
+    double s1 = 0.0, s2 = 0.0, stw = 0.0;
+    for (int64_t k = 0; k < b1 - b0; ++k) {
+      const double x = w[k * N];
+      const int t = tern(x - be, thr);
+      s1 += double(t);
+      s2 += double(t * t);
+      stw += double(t) * x;
+    }
+    const double det = s2 * n - s1 * s1;
+    if (det > 0.0) {
+      const double a = (n * stw - s1 * sw) / det;
+      if (a > 0.0) {
+        al = a;
+        be = (s2 * sw - s1 * stw) / det;
+      }
+    }
+  }
+  uint16_t a16 = f64_to_f16(al);
+  if ((a16 & 0x7FFF) == 0) a16 = 0x3C00;  // 1.0
+  alpha[r * G + g] = a16;
+  beta[r * G + g] = f64_to_f16(be);
+}
+
+struct ColArgs {
+  double* Wt;
+  const double* U;
+  const double* dmean;
+  const uint16_t* alpha;
+  const uint16_t* beta;
+  const int32_t* rank;
+  double* part_in;   // [workgroups][2] partials of the previous stage
+  double* part_out;  // [workgroups][2] this stage's partials
+  double* vst_in;    // previous v
+  double* vst_out;
+  double* Et;
+  int8_t* T;
+  double* Q;
+  uint16_t* vout;
+  uint8_t* rval;
+  uint8_t* ridx;
+  int64_t N, K, G, g, b0, b1, j;
+  int32_t nwg, iters;
+  double lambda;
+};
+
+enum ColMode { kStart = 0, kRefine = 1, kFinal = 2 };
+
+// v from the previous stage's partials: mean of |x| / alpha over non-zero
+// codes (summed over workgroups in order), rounded to fp16; the previous v
+// when every code is zero
+__device__ double stage_v(const ColArgs& a, double* red) {
+  __shared__ double vv;
+  for (int i = threadIdx.x; i < 2 * a.nwg; i += kCT) red[i] = a.part_in[i];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double su = 0.0, cn = 0.0;
+    for (int w = 0; w < a.nwg; ++w) {
+      su += red[2 * w];
+      cn += red[2 * w + 1];
+    }
+    vv = cn > 0.0 ? f16_to_f64(f64_to_f16(su / cn)) : a.vst_in[0];
+  }
+  __syncthreads();
+  return vv;
+}
+
+// this workgroup's sum of |x| / alpha and count over non-zero codes
+__device__ void stage_partial(const ColArgs& a, double u, double c, double* red) {
+  __syncthreads();
+  red[threadIdx.x] = u;
+  red[kCT + threadIdx.x] = c;
+  __syncthreads();
+  for (int s = kCT / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) {
+      red[threadIdx.x] += red[threadIdx.x + s];
+      red[kCT + threadIdx.x] += red[kCT + threadIdx.x + s];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    a.part_out[2 * blockIdx.x] = red[0];
+    a.part_out[2 * blockIdx.x + 1] = red[kCT];
+  }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
+  __shared__ double red[2 * kQMaxRows / kCT > 2 * kCT ? 2 * kQMaxRows / kCT : 2 * kCT];
+  const int64_t r = int64_t(blockIdx.x) * kCT + threadIdx.x;
+  const bool live = r < a.N;
+  const double al = live ? f16_to_f64(a.alpha[r * a.G + a.g]) : 1.0;
+  const double be = live ? f16_to_f64(a.beta[r * a.G + a.g]) : 0.0;
+  const int64_t j = a.j;
+  const double w = live ? a.Wt[j * a.N + r] : 0.0;
+  const double x = w - be;
+  if (MODE == kStart) {
+    const int t = tern(x, al / 2.0);
+    stage_partial(a, t != 0 ? fabs(x) / al : 0.0, t != 0 ? 1.0 : 0.0, red);
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.vst_out[0] = 1.0;
+    return;
+  }
+  const double v = a.iters > 0 ? stage_v(a, red) : 1.0;
+  if (MODE == kRefine) {
+    const int t = tern(x, v * al / 2.0);
+    stage_partial(a, t != 0 ? fabs(x) / al : 0.0, t != 0 ? 1.0 : 0.0, red);
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.vst_out[0] = v;
+    return;
+  }
+  // final: codes, quantized value, residual, decayed error, in-block update
+  const int t = tern(x, v * al / 2.0);
+  double q = be + (v * al) * double(t);
+  const int32_t srank = a.rank[j];
+  if (srank >= 0) {
+    const double res = w - q;
+    const int lane = threadIdx.x & 63, g0 = lane & ~3;
+    double best = fabs(__shfl(res, g0));
+    int bk = 0;
+#pragma unroll
+    for (int k = 1; k < 4; ++k) {
+      const double m = fabs(__shfl(res, g0 + k));
+      if (m > best) {
+        best = m;
+        bk = k;
+      }
+    }
+    const double rk = __shfl(res, g0 + bk);
+    const uint8_t code = f64_to_e4m3(rk);
+    if (lane - g0 == bk) q += e4m3_to_f64(code);
+    if (live && lane == g0) {
+      a.rval[int64_t(srank) * (a.N / 4) + r / 4] = code;
+      a.ridx[int64_t(srank) * (a.N / 4) + r / 4] = uint8_t(bk);
+    }
+  }
+  const int64_t i = j - a.b0, B = a.b1 - a.b0;
+  const double d = a.U[j * a.K + j];
+  const double gamma = exp((-a.lambda * (d / a.dmean[a.g])) * (double(i) / double(B)));
+  const double e = (gamma * (w - q)) / d;
+  if (live) {
+    a.T[r * a.K + j] = int8_t(t);
+    if (a.Q) a.Q[r * a.K + j] = q;
+    a.Et[i * a.N + r] = e;
+    const double* urow = a.U + j * a.K;
+    for (int64_t k = j + 1; k < a.b1; ++k) a.Wt[k * a.N + r] -= e * urow[k];
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.vout[j] = f64_to_f16(v);
+  if (a.iters > 0 && j + 1 < a.b1) {  // the next column's first assignment
+    const double x2 = live ? a.Wt[(j + 1) * a.N + r] - be : 0.0;
+    const int t2 = tern(x2, al / 2.0);
+    stage_partial(a, t2 != 0 ? fabs(x2) / al : 0.0, t2 != 0 ? 1.0 : 0.0, red);
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.vst_out[0] = 1.0;
+  }
+}
+
+// Wt[k][r] -= sum_{i < B} U[b0 + i][k] Et[i][r] for k in [b1, K)
+__global__ __launch_bounds__(256) void trail_gemm_kernel(double* __restrict__ Wt, const double* __restrict__ U,
+                                                         const double* __restrict__ Et, int64_t N, int64_t K,
+                                                         int64_t b0, int64_t B, int64_t b1) {
+  __shared__ double Us[32][65], Es[32][65];
+  const int64_t r0 = int64_t(blockIdx.x) * 64, k0 = b1 + int64_t(blockIdx.y) * 64;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  double acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int64_t i0 = 0; i0 < B; i0 += 32) {
+    for (int e = threadIdx.x; e < 32 * 64; e += 256) {
+      const int ii = e >> 6, c = e & 63;
+      const bool in = i0 + ii < B;
+      Us[ii][c] = (in && k0 + c < K) ? U[(b0 + i0 + ii) * K + k0 + c] : 0.0;
+      Es[ii][c] = (in && r0 + c < N) ? Et[(i0 + ii) * N + r0 + c] : 0.0;
+    }
+    __syncthreads();
+    for (int ii = 0; ii < 32; ++ii) {
+      double uk[4], er[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        uk[m] = Us[ii][ty + 16 * m];
+        er[m] = Es[ii][tx + 16 * m];
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n) acc[m][n] += uk[m] * er[n];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const int64_t k = k0 + ty + 16 * m, r = r0 + tx + 16 * n;
+      if (k < K && r < N) Wt[k * N + r] -= acc[m][n];
+    }
+}
+
+int grid1(int64_t n, int per) { return int(q_cdiv(n, per) < 65535 * 16 ? q_cdiv(n, per) : 65535 * 16); }
+
+}  // namespace
+
+extern "C" {
+
+int qtea_quant_hessian(const float* X, int64_t n, int64_t K, double* H, void* stream) {
+  if (!X || !H || n < 1 || K < 1 || K > kQMaxCols) return QTEA_ERR_INVALID_ARG;
+  const int64_t T = q_cdiv(K, 64);
+  if (T > 65535) return QTEA_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(hess_kernel, dim3(uint32_t(T), uint32_t(T)), dim3(256), 0, static_cast<hipStream_t>(stream), X,
+                     n, K, 2.0 / double(n), H);
+  return hipGetLastError() == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+}
+
+int qtea_quant_workspace_bytes(int64_t N, int64_t K, int64_t* out_bytes) {
+  // N <= 65536: the column mean's partials (two per 256-row workgroup) fit
+  // one workgroup's reduction buffer
+  if (!out_bytes || N < 4 || N % 4 != 0 || K < 1 || N > kQMaxRows || K > kQMaxCols) return QTEA_ERR_INVALID_ARG;
+  *out_bytes = q_layout(N, K).total;
+  return QTEA_OK;
+}
+
+int qtea_quantize(const double* W, const double* H, int64_t N, int64_t K, const qtea_quant_params* p, int8_t* T,
+                  uint16_t* group_scale, uint16_t* group_bias, uint16_t* col_rescale, int32_t* salient,
+                  uint32_t* salient_bitmap, uint8_t* resid_val, uint8_t* resid_idx, double* Q, void* workspace,
+                  int64_t workspace_bytes, void* stream) {
+  int64_t need = 0;
+  if (qtea_quant_workspace_bytes(N, K, &need) != QTEA_OK) return QTEA_ERR_INVALID_ARG;
+  if (!W || !H || !p || !T || !group_scale || !group_bias || !col_rescale || !resid_val || !resid_idx)
+    return QTEA_ERR_INVALID_ARG;
+  if (p->n_salient < 0 || p->n_salient > K || (p->n_salient > 0 && !salient)) return QTEA_ERR_INVALID_ARG;
+  if (p->iters < 0 || p->iters > QTEA_QUANT_MAX_ITERS || p->reserved != 0) return QTEA_ERR_INVALID_ARG;
+  if (!(p->lambda_decay >= 0.0) || !isfinite(p->lambda_decay) || !(p->damp >= 0.0) || !isfinite(p->damp))
+    return QTEA_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < need) return QTEA_ERR_WORKSPACE;
+  const QLayout L = q_layout(N, K);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  double* Wt = reinterpret_cast<double*>(ws + L.wt);
+  double* A = reinterpret_cast<double*>(ws + L.a);
+  double* U = reinterpret_cast<double*>(ws + L.u);
+  double* Et = reinterpret_cast<double*>(ws + L.et);
+  double* score = reinterpret_cast<double*>(ws + L.score);
+  int32_t* flag = reinterpret_cast<int32_t*>(ws + L.flag);
+  int32_t* rank = reinterpret_cast<int32_t*>(ws + L.rank);
+  double* dmean = reinterpret_cast<double*>(ws + L.dmean);
+  double* dm = reinterpret_cast<double*>(ws + L.scal);
+  int32_t* status = reinterpret_cast<int32_t*>(ws + L.scal + 8);
+  double* part = reinterpret_cast<double*>(ws + L.part);
+  double* vst = reinterpret_cast<double*>(ws + L.vst);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t G = q_cdiv(K, kQG);
+  const int nwg = int(q_cdiv(N, kCT));
+  // (salient may be NULL only when n_salient == 0: then nothing is written to it)
+  int32_t* S = salient ? salient : flag;
+
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, st, status, int64_t(1), 0);
+  hipLaunchKernelGGL(fill_f64_kernel, dim3(grid1(K * K, 256)), dim3(256), 0, st, U, K * K, 0.0);
+  hipLaunchKernelGGL(fill_f64_kernel, dim3(grid1(K, 256)), dim3(256), 0, st, score, K, 0.0);
+  // 1. salient columns
+  const int64_t rows = 256, ry = q_cdiv(N, rows);
+  if (ry > 65535) return QTEA_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(maxsq_kernel, dim3(uint32_t(q_cdiv(K, 256)), uint32_t(ry)), dim3(256), 0, st, W, N, K, rows,
+                     reinterpret_cast<unsigned long long*>(score));
+  hipLaunchKernelGGL(score_kernel, dim3(uint32_t(q_cdiv(K, 256))), dim3(256), 0, st, score, H, K);
+  hipLaunchKernelGGL(select_kernel, dim3(uint32_t(q_cdiv(K, 256))), dim3(256), 0, st, score, K, p->n_salient, flag);
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, st, flag, K, p->n_salient, S, rank, salient_bitmap);
+  // 2. H_d = V V^T, U = V^-1
+  hipLaunchKernelGGL(diag_mean_kernel, dim3(1), dim3(256), 0, st, H, K, dm);
+  hipLaunchKernelGGL(damp_copy_kernel, dim3(grid1(K * K, 256)), dim3(256), 0, st, H, K, dm, p->damp, A);
+  for (int64_t hi = K; hi > 0; hi -= kNB) {
+    const int64_t lo = hi - kNB > 0 ? hi - kNB : 0;
+    hipLaunchKernelGGL(chol_diag_kernel, dim3(1), dim3(256), 0, st, A, K, lo, int(hi - lo), status);
+    if (lo > 0) {
+      hipLaunchKernelGGL(chol_panel_kernel, dim3(uint32_t(q_cdiv(lo, 256))), dim3(256), 0, st, A, K, lo);
+      const int64_t tl = q_cdiv(lo, 64);
+      hipLaunchKernelGGL(chol_trail_kernel, dim3(uint32_t(tl), uint32_t(tl)), dim3(256), 0, st, A, K, lo);
+    }
+  }
+  const int64_t nblk = q_cdiv(K, kNB);
+  hipLaunchKernelGGL(trinv_diag_kernel, dim3(uint32_t(nblk)), dim3(64), 0, st, A, K, U);
+  for (int64_t b = 1; b < nblk; ++b) {
+    const int64_t hi = K - kNB * b;
+    hipLaunchKernelGGL(trinv_row_kernel, dim3(uint32_t(q_cdiv(K - hi, 64))), dim3(256), 0, st, A, K, b, U);
+  }
+  hipLaunchKernelGGL(dmean_kernel, dim3(uint32_t(q_cdiv(G, 256))), dim3(256), 0, st, U, K, dmean);
+  // 3. columns
+  hipLaunchKernelGGL(transpose_kernel, dim3(uint32_t(q_cdiv(K, 32)), uint32_t(q_cdiv(N, 32))), dim3(256), 0, st, W,
+                     N, K, H, Wt);
+  ColArgs a{};
+  a.Wt = Wt;
+  a.U = U;
+  a.dmean = dmean;
+  a.alpha = group_scale;
+  a.beta = group_bias;
+  a.rank = rank;
+  a.Et = Et;
+  a.T = T;
+  a.Q = Q;
+  a.vout = col_rescale;
+  a.rval = resid_val;
+  a.ridx = resid_idx;
+  a.N = N;
+  a.K = K;
+  a.G = G;
+  a.nwg = nwg;
+  a.iters = p->iters;
+  a.lambda = p->lambda_decay;
+  int s = 0;  // partials / previous-v buffer the next stage reads
+  auto stage = [&](int mode) {
+    a.part_in = part + s * nwg * 2;
+    a.part_out = part + (s ^ 1) * nwg * 2;
+    a.vst_in = vst + s;
+    a.vst_out = vst + (s ^ 1);
+    if (mode == kStart)
+      hipLaunchKernelGGL(col_kernel<kStart>, dim3(uint32_t(nwg)), dim3(kCT), 0, st, a);
+    else if (mode == kRefine)
+      hipLaunchKernelGGL(col_kernel<kRefine>, dim3(uint32_t(nwg)), dim3(kCT), 0, st, a);
+    else
+      hipLaunchKernelGGL(col_kernel<kFinal>, dim3(uint32_t(nwg)), dim3(kCT), 0, st, a);
+    s ^= 1;
+  };
+  for (int64_t g = 0; g < G; ++g) {
+    const int64_t b0 = g * kQG, b1 = b0 + kQG < K ? b0 + kQG : K;
+    hipLaunchKernelGGL(group_params_kernel, dim3(uint32_t(nwg)), dim3(kCT), 0, st, Wt, N, K, G, g, group_scale,
+                       group_bias);
+    a.g = g;
+    a.b0 = b0;
+    a.b1 = b1;
+    a.j = b0;
+    if (p->iters > 0) stage(kStart);
+    for (int64_t j = b0; j < b1; ++j) {
+      a.j = j;
+      for (int it = 1; it < p->iters; ++it) stage(kRefine);
+      stage(kFinal);
+    }
+    if (b1 < K)
+      hipLaunchKernelGGL(trail_gemm_kernel, dim3(uint32_t(q_cdiv(N, 64)), uint32_t(q_cdiv(K - b1, 64))), dim3(256), 0,
+                         st, Wt, U, Et, N, K, b0, b1 - b0, b1);
+  }
+  if (hipGetLastError() != hipSuccess) return QTEA_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return QTEA_ERR_HIP;
+  int32_t host_status = 0;
+  if (hipMemcpy(&host_status, status, sizeof(host_status), hipMemcpyDeviceToHost) != hipSuccess) return QTEA_ERR_HIP;
+  return host_status ? QTEA_ERR_NOT_POSITIVE : QTEA_OK;
+}
+
+}  // extern "C"

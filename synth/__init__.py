@@ -24,6 +24,14 @@ available; shapes follow Llama-3-8B, Qwen3-14B and Llama-3-70B linears):
   * for the paper's 128-column quantization groups (groups=128): a scale
     alpha[r][g] ~ U(0.01, 0.03) and a bias beta[r][g] ~ U(-0.005, 0.005)
     per row and group, rounded to fp16.
+
+Quantizer inputs (quant_inputs; stand in for a full-precision linear layer
+and its calibration activations, which are not available): weights
+W ~ N(0, 0.02) in fp64 with 1% of the columns scaled by 4 (outlier input
+channels); calibration rows X = Z M in fp32 with Z ~ N(0, 1) [n][K] and
+M = I + N(0, 0.1 / sqrt(K)) [K][K] (correlated channels), 2% of the channels
+scaled by 5 (high-energy activations); numpy's PCG64 generator seeded by
+`seed`.
 """
 from __future__ import annotations
 
@@ -214,3 +222,17 @@ def layer_inputs(seed, layer, mat, N, K, p0=Fraction(2, 5), frac=Fraction(2, 100
 def activations(seed, layer, mat, B, K) -> np.ndarray:
     """x fp16 [B][K], N(0, 1), independent per (matrix, batch row)."""
     return normal_f16(key(seed, layer, mat, FIELD_X), B * K, 0.0, 1.0).reshape(B, K)
+
+
+def quant_inputs(seed: int, N: int, K: int, n_calib: int):
+    """Full-precision weights W fp64 [N][K] and calibration rows X fp32
+    [n_calib][K] for the offline quantizer (recipe in the module docstring)."""
+    rng = np.random.default_rng(seed)
+    W = rng.normal(0.0, 0.02, size=(N, K))
+    n_out = max(1, K // 100)
+    W[:, rng.choice(K, size=n_out, replace=False)] *= 4.0
+    M = np.eye(K) + rng.normal(0.0, 0.1 / np.sqrt(K), size=(K, K))
+    X = rng.normal(size=(n_calib, K)) @ M
+    n_hot = max(1, K // 50)
+    X[:, rng.choice(K, size=n_hot, replace=False)] *= 5.0
+    return W, X.astype(np.float32)

@@ -1,8 +1,9 @@
-"""The C-ABI library loads and exports every function include/qtea.h
+"""The C-ABI library loads and exports every function include/*.h
 declares; host-side argument checks answer without touching a device."""
 from __future__ import annotations
 
 import ctypes
+import glob
 import os
 import re
 
@@ -12,11 +13,11 @@ import oracle
 import paper_2609_00224_amd as q
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "qtea.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 def _declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(qtea_[a-z_0-9]+)\s*\(", text)))
 
@@ -39,9 +40,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert q.qtea_abi_version() == 6
+    assert q.qtea_abi_version() == 7
     assert q.qtea_status_string(0) == "ok"
-    for s in range(-6, 0):
+    for s in range(-7, 0):
         assert q.qtea_status_string(s) != "unknown status"
     assert q.qtea_status_string(-99) == "unknown status"
 
@@ -123,3 +124,21 @@ def test_read_ceiling_host_checks(lib):
     for args in [(None, 16, None, None), (ctypes.c_void_p(16), 15, ctypes.c_void_p(64), None),
                  (ctypes.c_void_p(8), 16, ctypes.c_void_p(64), None), (ctypes.c_void_p(16), 0, ctypes.c_void_p(64), None)]:
         assert lib.qtea_read_ceiling(*args) == q.QTEA_ERR_INVALID_ARG
+
+
+def test_quantizer_host_checks(lib):
+    out = ctypes.c_int64(0)
+    assert lib.qtea_quant_workspace_bytes(6, 10, ctypes.byref(out)) == q.QTEA_ERR_INVALID_ARG  # N % 4
+    assert lib.qtea_quant_workspace_bytes(8, 0, ctypes.byref(out)) == q.QTEA_ERR_INVALID_ARG
+    assert lib.qtea_quant_workspace_bytes(65540, 8, ctypes.byref(out)) == q.QTEA_ERR_INVALID_ARG
+    assert lib.qtea_quant_workspace_bytes(8, 10, ctypes.byref(out)) == q.QTEA_OK and out.value > 8 * 10 * 8
+    assert lib.qtea_quant_hessian(None, 4, 4, None, None) == q.QTEA_ERR_INVALID_ARG
+    p = q.QteaQuantParams(2, 1.0, 0.01, 2, 0)
+    vp = ctypes.c_void_p(256)
+    args = [vp, vp, 8, 10, ctypes.byref(p)] + [vp] * 10
+    assert lib.qtea_quantize(*args, 0, None) == q.QTEA_ERR_WORKSPACE
+    for bad in (q.QteaQuantParams(11, 1.0, 0.01, 2, 0), q.QteaQuantParams(2, -1.0, 0.01, 2, 0),
+                q.QteaQuantParams(2, 1.0, 0.01, 17, 0), q.QteaQuantParams(2, 1.0, 0.01, 2, 1),
+                q.QteaQuantParams(2, float("nan"), 0.01, 2, 0)):
+        a = [vp, vp, 8, 10, ctypes.byref(bad)] + [vp] * 10
+        assert lib.qtea_quantize(*a, 1 << 30, None) == q.QTEA_ERR_INVALID_ARG
