@@ -306,6 +306,74 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
     }
 
 
+QUANT_LAYER = (("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096), ("down", 4096, 14336))
+QUANT_SALIENT = 0.05  # the paper's salient-column fraction
+QUANT_LAMBDA = 1.0
+QUANT_ITERS = 2
+
+
+def quantizer_main(args):
+    """Offline quantizer: Hessian and quantization of the four matrices of
+    one Llama-3-8B-shaped layer (synthetic full-precision weights and
+    calibration rows); one step = all four matrices."""
+    import torch
+
+    import paper_2609_00224_amd as q
+    import synth
+
+    q.load()
+    assert torch.cuda.is_available(), "no GPU"
+    dev = torch.device("cuda:0")
+    seed = synth.DEFAULT_SEED if args.seed is None else args.seed
+    mats = []
+    for i, (role, N, K) in enumerate(QUANT_LAYER):
+        W, X = synth.quant_inputs(seed + i, N, K, args.calib_rows)
+        mats.append({"role": role, "N": N, "K": K, "W": torch.from_numpy(W).to(dev), "X": torch.from_numpy(X).to(dev),
+                     "H": torch.empty((K, K), dtype=torch.float64, device=dev),
+                     "nS": synth.n_salient(K, QUANT_SALIENT)})
+        log(f"quantizer input {role} {N}x{K} ready")
+    weights = sum(m["N"] * m["K"] for m in mats)
+
+    def step(times=None):
+        for m in mats:
+            t0 = time.perf_counter()
+            q.qtea_quant_hessian(m["X"], m["H"])
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            m["out"] = q.quantize_matrix(m["W"], m["H"], m["nS"], lambda_decay=QUANT_LAMBDA, iters=QUANT_ITERS)
+            t2 = time.perf_counter()
+            if times is not None:
+                times.setdefault(m["role"], []).append((t1 - t0, t2 - t1))
+
+    for _ in range(args.warmup):
+        step()
+    times = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(times)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    per = {m["role"]: {"N": m["N"], "K": m["K"],
+                       "hessian_ms": round(1e3 * sum(a for a, _ in times[m["role"]]) / args.steps, 2),
+                       "quantize_ms": round(1e3 * sum(b for _, b in times[m["role"]]) / args.steps, 2)}
+           for m in mats}
+    for r, v in per.items():
+        log(f"  {r:8s} {v['N']}x{v['K']}: hessian {v['hessian_ms']} ms, quantize {v['quantize_ms']} ms")
+    log(f"quantizer: {weights / sec / 1e6:.1f} M weights/s ({sec * 1e3:.1f} ms per layer)")
+    out = {
+        "metric": "offline QTEA quantization rate, one Llama-3-8B-shaped layer (Hessian + quantize)",
+        "value": round(weights / sec, 1), "unit": "weights/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": "llama3_8b_layer_quantize", "matrices": [list(x) for x in QUANT_LAYER],
+                   "calib_rows": args.calib_rows, "salient_frac": QUANT_SALIENT, "lambda_decay": QUANT_LAMBDA,
+                   "iters": QUANT_ITERS, "seed": seed},
+        "per_matrix": per,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -323,6 +391,9 @@ def main():
     ap.add_argument("--chained-only", action="store_true", help="time only the per-GEMV launches")
     ap.add_argument("--grouped-only", action="store_true",
                     help="skip the per-GEMV launches (profiling the grouped kernel)")
+    ap.add_argument("--quantizer", action="store_true",
+                    help="time the offline quantizer on one Llama-3-8B-shaped layer instead of the GEMV")
+    ap.add_argument("--calib-rows", type=int, default=2048, help="calibration rows per Hessian (--quantizer)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="after the bench, copy this many bytes device-to-device 3 times "
                          "(known-size reference for HBM counters)")
@@ -331,6 +402,10 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               "sharding of this path is described, not built", file=sys.stderr)
         sys.exit(2)
+
+    if args.quantizer:
+        quantizer_main(args)
+        return
 
     import torch
 

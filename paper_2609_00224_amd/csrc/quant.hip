@@ -32,7 +32,7 @@ namespace {
 
 constexpr int kQG = QTEA_QUANT_GROUP;  // columns per group and per GPTQ block
 constexpr int kNB = 32;                // factorization block
-constexpr int kCT = 256;               // threads of the row-parallel kernels
+constexpr int kCT = 64;                // threads of the row-parallel kernels (one wave)
 constexpr int64_t kQAlign = 256;
 constexpr int64_t kQMaxRows = 65536;
 constexpr int64_t kQMaxCols = 65536;
@@ -50,7 +50,7 @@ QLayout q_layout(int64_t N, int64_t K) {
   int64_t o = 0;
   L.wt = o;    o = q_up(o + K * N * 8);                 // fp64 [K][N] current weights
   L.a = o;     o = q_up(o + K * K * 8);                 // fp64 [K][K] H_d, then V (upper)
-  L.u = o;     o = q_up(o + K * K * 8);                 // fp64 [K][K] U (upper, zero below)
+  L.u = o;     o = q_up(o + K * K * 8);                 // fp64 [K][K] U (upper; scratch below)
   L.et = o;    o = q_up(o + int64_t(kQG) * N * 8);      // fp64 [128][N] decayed errors of a block
   L.score = o; o = q_up(o + K * 8);                     // u64/fp64 [K] max W^2, then scores
   L.flag = o;  o = q_up(o + K * 4);                     // int32 [K] selected
@@ -334,59 +334,57 @@ __global__ __launch_bounds__(256) void chol_panel_kernel(double* __restrict__ A,
   for (int c = 0; c < kNB; ++c) row[c] = x[c];
 }
 
-// upper triangle of the leading c0 x c0 block -= panel panel^T (64 x 64 tiles)
+// upper triangle of the leading c0 x c0 block -= panel panel^T: 128 x 128
+// tiles, 8 x 8 outputs per thread (16 LDS reads per 64 products)
 __global__ __launch_bounds__(256) void chol_trail_kernel(double* __restrict__ A, int64_t K, int64_t c0) {
   const int64_t tp = blockIdx.y, tq = blockIdx.x;
   if (tp > tq) return;
-  __shared__ double Pp[64][kNB + 1], Pq[64][kNB + 1];
-  const int64_t p0 = tp * 64, q0 = tq * 64;
-  for (int e = threadIdx.x; e < 64 * kNB; e += 256) {
+  __shared__ double Pp[kNB][129], Pq[kNB][129];  // [k][row of the tile]
+  const int64_t p0 = tp * 128, q0 = tq * 128;
+  for (int e = threadIdx.x; e < 128 * kNB; e += 256) {
     const int i = e / kNB, k = e % kNB;
-    Pp[i][k] = p0 + i < c0 ? A[(p0 + i) * K + c0 + k] : 0.0;
-    Pq[i][k] = q0 + i < c0 ? A[(q0 + i) * K + c0 + k] : 0.0;
+    Pp[k][i] = p0 + i < c0 ? A[(p0 + i) * K + c0 + k] : 0.0;
+    Pq[k][i] = q0 + i < c0 ? A[(q0 + i) * K + c0 + k] : 0.0;
   }
   __syncthreads();
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4];
+  double acc[8][8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
   for (int k = 0; k < kNB; ++k) {
-    double va[4], vb[4];
+    double va[8], vb[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      va[i] = Pp[ty + 16 * i][k];
-      vb[i] = Pq[tx + 16 * i][k];
+    for (int i = 0; i < 8; ++i) {
+      va[i] = Pp[k][ty + 16 * i];
+      vb[i] = Pq[k][tx + 16 * i];
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] += va[i] * vb[j];
+      for (int j = 0; j < 8; ++j) acc[i][j] += va[i] * vb[j];
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       const int64_t p = p0 + ty + 16 * i, q = q0 + tx + 16 * j;
       if (p < c0 && q < c0 && p <= q) A[p * K + q] -= acc[i][j];
     }
 }
 
-// Inverse blocks: block b covers rows/columns [max(0, K - 32(b+1)), K - 32b).
-__device__ inline void inv_block(int64_t K, int64_t b, int64_t* lo, int* n) {
-  const int64_t hi = K - kNB * b;
-  *lo = hi - kNB > 0 ? hi - kNB : 0;
-  *n = int(hi - *lo);
-}
-
-// U_bb = V_bb^-1 for every diagonal block (one workgroup each)
+// U = V^-1 by recursive doubling: the 32 x 32 diagonal blocks (from the
+// top left, the last one ragged) are inverted in LDS; then at block size
+// s = 32, 64, ... each pair of neighbouring inverted blocks A = [2ps, 2ps+s)
+// and C = [2ps+s, 2ps+2s) is joined by U_AC = -U_A (V_AC U_C), two batched
+// products per level.  The intermediate V_AC U_C is kept transposed in U's
+// lower triangle (the mirror of U_AC), which nothing else reads.
 __global__ __launch_bounds__(64) void trinv_diag_kernel(const double* __restrict__ A, int64_t K,
                                                         double* __restrict__ U) {
   __shared__ double Vd[kNB][kNB + 1], Ud[kNB][kNB + 1];
-  int64_t lo;
-  int n;
-  inv_block(K, blockIdx.x, &lo, &n);
+  const int64_t lo = int64_t(blockIdx.x) * kNB;
+  const int n = int(K - lo < kNB ? K - lo : kNB);
   for (int e = threadIdx.x; e < kNB * kNB; e += 64) {
     const int p = e / kNB, q = e % kNB;
     Vd[p][q] = (p <= q && q < n) ? A[(lo + p) * K + lo + q] : 0.0;
@@ -409,63 +407,70 @@ __global__ __launch_bounds__(64) void trinv_diag_kernel(const double* __restrict
   }
 }
 
-// block row b (rows [lo, hi)), columns [hi, K): U = -U_bb (V_b,right U_right)
-__global__ __launch_bounds__(256) void trinv_row_kernel(const double* __restrict__ A, int64_t K, int64_t b,
-                                                        double* __restrict__ U) {
-  __shared__ double Vs[kNB][kNB + 1], Us[kNB][65], At[kNB][65], Ud[kNB][kNB + 1];
-  int64_t lo;
-  int n;
-  inv_block(K, b, &lo, &n);
-  const int64_t hi = lo + n;
-  const int64_t j0 = hi + int64_t(blockIdx.x) * 64;
-  const int64_t kend = j0 + 64 < K ? j0 + 64 : K;  // U[k][j] = 0 for k > j
+// MODE 0: T = V_AC U_C, stored as U[C][A] = T^T.  MODE 1: U_AC = -U_A T.
+// Pair p = blockIdx.z; tile of 64 rows of A (blockIdx.y) x 64 columns of C
+// (blockIdx.x); the triangular factor's zero half is skipped by index.
+template <int MODE>
+__global__ __launch_bounds__(256) void trinv_join_kernel(const double* __restrict__ A, int64_t K, int64_t s,
+                                                         double* __restrict__ U) {
+  __shared__ double La[16][65], Lb[16][65];
+  const int64_t a0 = int64_t(blockIdx.z) * 2 * s, c0 = a0 + s;
+  if (c0 >= K) return;
+  const int64_t cn = K - c0 < s ? K - c0 : s;  // columns of C
+  const int64_t i0 = int64_t(blockIdx.y) * 64, j0 = int64_t(blockIdx.x) * 64;
+  if (i0 >= s || j0 >= cn) return;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[2][4];
+  double acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
-  for (int64_t k0 = hi; k0 < kend; k0 += kNB) {
-    for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
-      const int i = e / kNB, k = e % kNB;
-      Vs[i][k] = (i < n && k0 + k < kend) ? A[(lo + i) * K + k0 + k] : 0.0;
-    }
-    for (int e = threadIdx.x; e < kNB * 64; e += 256) {
-      const int k = e / 64, c = e % 64;
-      Us[k][c] = (k0 + k < kend && j0 + c < K) ? U[(k0 + k) * K + j0 + c] : 0.0;
+  // MODE 0: k over C columns [0, j0 + 64); MODE 1: k over A rows [i0, s)
+  const int64_t kb = MODE == 0 ? 0 : i0;
+  const int64_t ke = MODE == 0 ? (j0 + 64 < cn ? j0 + 64 : cn) : s;
+  for (int64_t k0 = kb; k0 < ke; k0 += 16) {
+    for (int e = threadIdx.x; e < 16 * 64; e += 256) {
+      const int kk = e >> 6, m = e & 63;
+      const int64_t k = k0 + kk, i = i0 + m, j = j0 + m;
+      double va = 0.0, vb = 0.0;
+      if (k < ke) {
+        if (MODE == 0) {
+          va = i < s ? A[(a0 + i) * K + c0 + k] : 0.0;                 // V_AC[i][k]
+          vb = (j < cn && k <= j) ? U[(c0 + k) * K + c0 + j] : 0.0;    // U_C[k][j]
+        } else {
+          va = (i < s && k >= i) ? U[(a0 + i) * K + a0 + k] : 0.0;     // U_A[i][k]
+          vb = j < cn ? U[(c0 + j) * K + a0 + k] : 0.0;                // T[k][j] = U[C j][A k]
+        }
+      }
+      La[kk][m] = va;
+      Lb[kk][m] = vb;
     }
     __syncthreads();
-    for (int k = 0; k < kNB; ++k) {
-      double va[2], vb[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) va[i] = Vs[ty + 16 * i][k];
+    for (int kk = 0; kk < 16; ++kk) {
+      double va[4], vb[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) vb[j] = Us[k][tx + 16 * j];
+      for (int m = 0; m < 4; ++m) {
+        va[m] = La[kk][ty + 16 * m];
+        vb[m] = Lb[kk][tx + 16 * m];
+      }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += va[i] * vb[j];
+        for (int n = 0; n < 4; ++n) acc[m][n] += va[m] * vb[n];
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int m = 0; m < 4; ++m)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) At[ty + 16 * i][tx + 16 * j] = acc[i][j];
-  for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
-    const int p = e / kNB, q = e % kNB;
-    Ud[p][q] = (p <= q && q < n) ? U[(lo + p) * K + lo + q] : 0.0;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = ty + 16 * i, c = tx + 16 * j;
-      if (r < n && j0 + c < K) {
-        double s = 0.0;
-        for (int m = r; m < n; ++m) s += Ud[r][m] * At[m][c];
-        U[(lo + r) * K + j0 + c] = -s;
+    for (int n = 0; n < 4; ++n) {
+      const int64_t i = i0 + ty + 16 * m, j = j0 + tx + 16 * n;
+      if (i < s && j < cn) {
+        if (MODE == 0)
+          U[(c0 + j) * K + a0 + i] = acc[m][n];
+        else
+          U[(a0 + i) * K + c0 + j] = -acc[m][n];
       }
     }
 }
@@ -569,16 +574,22 @@ enum ColMode { kStart = 0, kRefine = 1, kFinal = 2 };
 // when every code is zero
 __device__ double stage_v(const ColArgs& a, double* red) {
   __shared__ double vv;
-  for (int i = threadIdx.x; i < 2 * a.nwg; i += kCT) red[i] = a.part_in[i];
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double su = 0.0, cn = 0.0;
-    for (int w = 0; w < a.nwg; ++w) {
-      su += red[2 * w];
-      cn += red[2 * w + 1];
-    }
-    vv = cn > 0.0 ? f16_to_f64(f64_to_f16(su / cn)) : a.vst_in[0];
+  double su = 0.0, cn = 0.0;  // each thread: workgroups t, t + kCT, ... in order
+  for (int w = threadIdx.x; w < a.nwg; w += kCT) {
+    su += a.part_in[2 * w];
+    cn += a.part_in[2 * w + 1];
   }
+  red[threadIdx.x] = su;
+  red[kCT + threadIdx.x] = cn;
+  __syncthreads();
+  for (int s = kCT / 2; s > 0; s >>= 1) {  // fixed tree order
+    if (threadIdx.x < s) {
+      red[threadIdx.x] += red[threadIdx.x + s];
+      red[kCT + threadIdx.x] += red[kCT + threadIdx.x + s];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) vv = red[kCT] > 0.0 ? f16_to_f64(f64_to_f16(red[0] / red[kCT])) : a.vst_in[0];
   __syncthreads();
   return vv;
 }
@@ -604,7 +615,7 @@ __device__ void stage_partial(const ColArgs& a, double u, double c, double* red)
 
 template <int MODE>
 __global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
-  __shared__ double red[2 * kQMaxRows / kCT > 2 * kCT ? 2 * kQMaxRows / kCT : 2 * kCT];
+  __shared__ double red[2 * kCT];
   const int64_t r = int64_t(blockIdx.x) * kCT + threadIdx.x;
   const bool live = r < a.N;
   const double al = live ? f16_to_f64(a.alpha[r * a.G + a.g]) : 1.0;
@@ -658,8 +669,21 @@ __global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
     a.T[r * a.K + j] = int8_t(t);
     if (a.Q) a.Q[r * a.K + j] = q;
     a.Et[i * a.N + r] = e;
+    // eight columns at a time: their loads are issued before any store
     const double* urow = a.U + j * a.K;
-    for (int64_t k = j + 1; k < a.b1; ++k) a.Wt[k * a.N + r] -= e * urow[k];
+    double* wt = a.Wt + r;
+    int64_t k = j + 1;
+    for (; k + 8 <= a.b1; k += 8) {
+      double wv[8], uv[8];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) {
+        uv[m] = urow[k + m];
+        wv[m] = wt[(k + m) * a.N];
+      }
+#pragma unroll
+      for (int m = 0; m < 8; ++m) wt[(k + m) * a.N] = wv[m] - e * uv[m];
+    }
+    for (; k < a.b1; ++k) wt[k * a.N] -= e * urow[k];
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) a.vout[j] = f64_to_f16(v);
   if (a.iters > 0 && j + 1 < a.b1) {  // the next column's first assignment
@@ -729,8 +753,6 @@ int qtea_quant_hessian(const float* X, int64_t n, int64_t K, double* H, void* st
 }
 
 int qtea_quant_workspace_bytes(int64_t N, int64_t K, int64_t* out_bytes) {
-  // N <= 65536: the column mean's partials (two per 256-row workgroup) fit
-  // one workgroup's reduction buffer
   if (!out_bytes || N < 4 || N % 4 != 0 || K < 1 || N > kQMaxRows || K > kQMaxCols) return QTEA_ERR_INVALID_ARG;
   *out_bytes = q_layout(N, K).total;
   return QTEA_OK;
@@ -788,15 +810,19 @@ int qtea_quantize(const double* W, const double* H, int64_t N, int64_t K, const 
     hipLaunchKernelGGL(chol_diag_kernel, dim3(1), dim3(256), 0, st, A, K, lo, int(hi - lo), status);
     if (lo > 0) {
       hipLaunchKernelGGL(chol_panel_kernel, dim3(uint32_t(q_cdiv(lo, 256))), dim3(256), 0, st, A, K, lo);
-      const int64_t tl = q_cdiv(lo, 64);
+      const int64_t tl = q_cdiv(lo, 128);
       hipLaunchKernelGGL(chol_trail_kernel, dim3(uint32_t(tl), uint32_t(tl)), dim3(256), 0, st, A, K, lo);
     }
   }
   const int64_t nblk = q_cdiv(K, kNB);
   hipLaunchKernelGGL(trinv_diag_kernel, dim3(uint32_t(nblk)), dim3(64), 0, st, A, K, U);
-  for (int64_t b = 1; b < nblk; ++b) {
-    const int64_t hi = K - kNB * b;
-    hipLaunchKernelGGL(trinv_row_kernel, dim3(uint32_t(q_cdiv(K - hi, 64))), dim3(256), 0, st, A, K, b, U);
+  for (int64_t sz = kNB; sz < K; sz *= 2) {
+    const int64_t pairs = q_cdiv(K, 2 * sz), t = q_cdiv(sz, 64);
+    if (pairs > 65535) return QTEA_ERR_INVALID_ARG;
+    hipLaunchKernelGGL(trinv_join_kernel<0>, dim3(uint32_t(t), uint32_t(t), uint32_t(pairs)), dim3(256), 0, st, A, K,
+                       sz, U);
+    hipLaunchKernelGGL(trinv_join_kernel<1>, dim3(uint32_t(t), uint32_t(t), uint32_t(pairs)), dim3(256), 0, st, A, K,
+                       sz, U);
   }
   hipLaunchKernelGGL(dmean_kernel, dim3(uint32_t(q_cdiv(G, 256))), dim3(256), 0, st, U, K, dmean);
   // 3. columns
