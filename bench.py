@@ -306,6 +306,7 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
     }
 
 
+FP64_PEAK_TFLOPS = 78.6  # MI355X dense fp64 (vector and matrix)
 QUANT_LAYER = (("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096), ("down", 4096, 14336))
 QUANT_SALIENT = 0.05  # the paper's salient-column fraction
 QUANT_LAMBDA = 1.0
@@ -361,6 +362,18 @@ def quantizer_main(args):
     for r, v in per.items():
         log(f"  {r:8s} {v['N']}x{v['K']}: hessian {v['hessian_ms']} ms, quantize {v['quantize_ms']} ms")
     log(f"quantizer: {weights / sec / 1e6:.1f} M weights/s ({sec * 1e3:.1f} ms per layer)")
+    # algorithmic fp64 work per step: Hessian 2 n K^2, reverse Cholesky K^3/3,
+    # triangular inverse K^3/3, GPTQ error updates 2 N K (K - 1) / 2
+    flops = sum(2.0 * args.calib_rows * m["K"] ** 2 + 2.0 * m["K"] ** 3 / 3 + float(m["N"]) * m["K"] * (m["K"] - 1)
+                for m in mats)
+    roof = {"bound": "alu", "achieved": round(flops / sec / 1e12, 3), "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(flops / sec / 1e12 / FP64_PEAK_TFLOPS, 4), "traffic": None,
+            "kernel": "whole quantizer (all kernels of the step)", "flops_per_step": flops}
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = quantizer_cpu_baseline(mats[1], seed + 1, args.calib_rows)
+        log(f"oracle: {cpu['value'] / 1e6:.2f} M weights/s on the {cpu['sample']}; GPU outputs equal: "
+            f"{cpu['gpu_vs_oracle']}")
     out = {
         "metric": "offline QTEA quantization rate, one Llama-3-8B-shaped layer (Hessian + quantize)",
         "value": round(weights / sec, 1), "unit": "weights/s", "n_gpus": 1, "steps": args.steps,
@@ -370,8 +383,47 @@ def quantizer_main(args):
                    "calib_rows": args.calib_rows, "salient_frac": QUANT_SALIENT, "lambda_decay": QUANT_LAMBDA,
                    "iters": QUANT_ITERS, "seed": seed},
         "per_matrix": per,
+        "roofline": roof,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def quantizer_cpu_baseline(m, seed, calib_rows):
+    """The quantizer oracle (fp64 numpy) on one whole matrix of the layer,
+    timed, and the GPU's outputs for that matrix compared with it."""
+    import numpy as np
+
+    import synth
+    from oracle import quantizer as qz
+
+    W, X = synth.quant_inputs(seed, m["N"], m["K"], calib_rows)
+    t0 = time.perf_counter()
+    ref = qz.quantize(W, qz.hessian(X), m["nS"], lam=QUANT_LAMBDA, iters=QUANT_ITERS)
+    t = time.perf_counter() - t0
+    o = m["out"]
+    f16 = lambda a: np.asarray(a, np.float16).view(np.uint16)
+    eq = {
+        "codes": bool(np.array_equal(o["T"].cpu().numpy(), ref["T"])),
+        "alpha_beta_v": bool(np.array_equal(o["alpha"].cpu().numpy().view(np.uint16), f16(ref["alpha"]))
+                             and np.array_equal(o["beta"].cpu().numpy().view(np.uint16), f16(ref["beta"]))
+                             and np.array_equal(o["v"].cpu().numpy().view(np.uint16), f16(ref["v"]))),
+        "salient_and_residual": bool(np.array_equal(o["S"].cpu().numpy(), ref["S"])
+                                     and np.array_equal(o["R8"].cpu().numpy(), ref["rval"])
+                                     and np.array_equal(o["idx"].cpu().numpy(), ref["ridx"])),
+    }
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(m["N"] * m["K"] / t, 1), "unit": "weights/s", "cores": len(os.sched_getaffinity(0)),
+            "kind": "oracle", "sample": f"{m['role']} matrix {m['N']}x{m['K']} (Hessian from {calib_rows} rows "
+            f"+ quantization), {t:.1f} s of oracle time", "gpu_vs_oracle": eq,
+            "host": {"cpu_model": model, "nproc": os.cpu_count()}}
 
 
 def main():
