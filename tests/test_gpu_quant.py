@@ -143,3 +143,9 @@ def test_quantized_matrix_through_grouped_gemv():
     ref = out["Q"].cpu().numpy() @ x[0].astype(np.float64)
     got = y.cpu().numpy()[0].astype(np.float64)
     assert np.linalg.norm(got - ref) <= 1e-3 * np.linalg.norm(ref)
+
+
+def test_quantize_full_size_matrix():
+    """A whole Llama-3-8B-shaped O projection (4096 x 4096, 205 salient
+    columns, the paper's settings), bit-exact against the oracle."""
+    _check(4096, 4096, 205, 1.0, 2, 8)
