@@ -33,6 +33,7 @@ namespace {
 constexpr int kQG = QTEA_QUANT_GROUP;  // columns per group and per GPTQ block
 constexpr int kNB = 32;                // factorization block
 constexpr int kCT = 64;                // threads of the row-parallel kernels (one wave)
+constexpr int kColChunk = 16;          // later columns of a block updated per workgroup
 constexpr int64_t kQAlign = 256;
 constexpr int64_t kQMaxRows = 65536;
 constexpr int64_t kQMaxCols = 65536;
@@ -636,7 +637,10 @@ __global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
     if (blockIdx.x == 0 && threadIdx.x == 0) a.vst_out[0] = v;
     return;
   }
-  // final: codes, quantized value, residual, decayed error, in-block update
+  // final: codes, quantized value, residual, decayed error, in-block update;
+  // workgroup (x, y) updates chunk y of the block's later columns, and only
+  // the y = 0 workgroups write the column's results
+  const bool primary = blockIdx.y == 0;
   const int t = tern(x, v * al / 2.0);
   double q = be + (v * al) * double(t);
   const int32_t srank = a.rank[j];
@@ -656,7 +660,7 @@ __global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
     const double rk = __shfl(res, g0 + bk);
     const uint8_t code = f64_to_e4m3(rk);
     if (lane - g0 == bk) q += e4m3_to_f64(code);
-    if (live && lane == g0) {
+    if (primary && live && lane == g0) {
       a.rval[int64_t(srank) * (a.N / 4) + r / 4] = code;
       a.ridx[int64_t(srank) * (a.N / 4) + r / 4] = uint8_t(bk);
     }
@@ -665,15 +669,20 @@ __global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
   const double d = a.U[j * a.K + j];
   const double gamma = exp((-a.lambda * (d / a.dmean[a.g])) * (double(i) / double(B)));
   const double e = (gamma * (w - q)) / d;
-  if (live) {
+  if (live && primary) {
     a.T[r * a.K + j] = int8_t(t);
     if (a.Q) a.Q[r * a.K + j] = q;
     a.Et[i * a.N + r] = e;
-    // eight columns at a time: their loads are issued before any store
+  }
+  if (live) {
+    // this workgroup's chunk of the block's later columns, eight at a time:
+    // their loads are issued before any store
     const double* urow = a.U + j * a.K;
     double* wt = a.Wt + r;
-    int64_t k = j + 1;
-    for (; k + 8 <= a.b1; k += 8) {
+    const int64_t kb = j + 1 + int64_t(blockIdx.y) * kColChunk;
+    const int64_t ke = kb + kColChunk < a.b1 ? kb + kColChunk : a.b1;
+    int64_t k = kb;
+    for (; k + 8 <= ke; k += 8) {
       double wv[8], uv[8];
 #pragma unroll
       for (int m = 0; m < 8; ++m) {
@@ -683,10 +692,11 @@ __global__ __launch_bounds__(kCT) void col_kernel(ColArgs a) {
 #pragma unroll
       for (int m = 0; m < 8; ++m) wt[(k + m) * a.N] = wv[m] - e * uv[m];
     }
-    for (; k < a.b1; ++k) wt[k * a.N] -= e * urow[k];
+    for (; k < ke; ++k) wt[k * a.N] -= e * urow[k];
   }
+  if (!primary) return;
   if (blockIdx.x == 0 && threadIdx.x == 0) a.vout[j] = f64_to_f16(v);
-  if (a.iters > 0 && j + 1 < a.b1) {  // the next column's first assignment
+  if (a.iters > 0 && j + 1 < a.b1) {  // the next column's first assignment (in chunk 0)
     const double x2 = live ? a.Wt[(j + 1) * a.N + r] - be : 0.0;
     const int t2 = tern(x2, al / 2.0);
     stage_partial(a, t2 != 0 ? fabs(x2) / al : 0.0, t2 != 0 ? 1.0 : 0.0, red);
@@ -857,8 +867,10 @@ int qtea_quantize(const double* W, const double* H, int64_t N, int64_t K, const 
       hipLaunchKernelGGL(col_kernel<kStart>, dim3(uint32_t(nwg)), dim3(kCT), 0, st, a);
     else if (mode == kRefine)
       hipLaunchKernelGGL(col_kernel<kRefine>, dim3(uint32_t(nwg)), dim3(kCT), 0, st, a);
-    else
-      hipLaunchKernelGGL(col_kernel<kFinal>, dim3(uint32_t(nwg)), dim3(kCT), 0, st, a);
+    else {
+      const int64_t later = a.b1 - a.j - 1, ny = later > 0 ? q_cdiv(later, kColChunk) : 1;
+      hipLaunchKernelGGL(col_kernel<kFinal>, dim3(uint32_t(nwg), uint32_t(ny)), dim3(kCT), 0, st, a);
+    }
     s ^= 1;
   };
   for (int64_t g = 0; g < G; ++g) {
