@@ -7,8 +7,8 @@
 //      one workgroup compacts the selected columns in ascending order.
 //   2. damped Hessian H_d (dead columns fixed), then U with H_d^-1 = U^T U:
 //      H_d = V V^T with V upper (Cholesky from the last column backwards,
-//      32-column blocks: diagonal block in LDS, panel by per-row triangular
-//      solves, symmetric rank-32 update of the leading block), and U = V^-1
+//      64-column blocks: diagonal block in LDS, panel by per-row triangular
+//      solves, symmetric rank-64 update of the leading block), and U = V^-1
 //      (diagonal blocks inverted in LDS, then block rows from the bottom up,
 //      each a product with the rows already inverted).  U is the upper
 //      Cholesky factor of H_d^-1 (unique with a positive diagonal).
@@ -31,7 +31,8 @@
 namespace {
 
 constexpr int kQG = QTEA_QUANT_GROUP;  // columns per group and per GPTQ block
-constexpr int kNB = 32;                // factorization block
+constexpr int kNB = 64;                // factorization block
+constexpr int kNBH = 32;               // panel columns staged per LDS pass of the trailing update
 constexpr int kCT = 64;                // threads of the row-parallel kernels (one wave)
 constexpr int kColChunk = 16;          // later columns of a block updated per workgroup
 constexpr int64_t kQAlign = 256;
@@ -310,7 +311,7 @@ __global__ __launch_bounds__(256) void chol_diag_kernel(double* __restrict__ A, 
   }
 }
 
-// rows p < c0 of the 32 columns [c0, c0 + 32): solve x V_D^T = panel row
+// rows p < c0 of the 64 columns [c0, c0 + 64): solve x V_D^T = panel row
 __global__ __launch_bounds__(256) void chol_panel_kernel(double* __restrict__ A, int64_t K, int64_t c0) {
   __shared__ double D[kNB][kNB + 1];
   for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
@@ -335,36 +336,40 @@ __global__ __launch_bounds__(256) void chol_panel_kernel(double* __restrict__ A,
   for (int c = 0; c < kNB; ++c) row[c] = x[c];
 }
 
-// upper triangle of the leading c0 x c0 block -= panel panel^T: 128 x 128
-// tiles, 8 x 8 outputs per thread (16 LDS reads per 64 products)
+// upper triangle of the leading c0 x c0 block -= panel panel^T (the block's
+// 64 columns): 128 x 128 tiles, 8 x 8 outputs per thread (16 LDS reads per
+// 64 products), the panel staged 32 columns at a time
 __global__ __launch_bounds__(256) void chol_trail_kernel(double* __restrict__ A, int64_t K, int64_t c0) {
   const int64_t tp = blockIdx.y, tq = blockIdx.x;
   if (tp > tq) return;
-  __shared__ double Pp[kNB][129], Pq[kNB][129];  // [k][row of the tile]
+  __shared__ double Pp[kNBH][129], Pq[kNBH][129];  // [k][row of the tile]
   const int64_t p0 = tp * 128, q0 = tq * 128;
-  for (int e = threadIdx.x; e < 128 * kNB; e += 256) {
-    const int i = e / kNB, k = e % kNB;
-    Pp[k][i] = p0 + i < c0 ? A[(p0 + i) * K + c0 + k] : 0.0;
-    Pq[k][i] = q0 + i < c0 ? A[(q0 + i) * K + c0 + k] : 0.0;
-  }
-  __syncthreads();
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   double acc[8][8];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
-  for (int k = 0; k < kNB; ++k) {
-    double va[8], vb[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      va[i] = Pp[k][ty + 16 * i];
-      vb[i] = Pq[k][tx + 16 * i];
+  for (int h = 0; h < kNB; h += kNBH) {
+    for (int e = threadIdx.x; e < 128 * kNBH; e += 256) {
+      const int i = e / kNBH, k = e % kNBH;
+      Pp[k][i] = p0 + i < c0 ? A[(p0 + i) * K + c0 + h + k] : 0.0;
+      Pq[k][i] = q0 + i < c0 ? A[(q0 + i) * K + c0 + h + k] : 0.0;
     }
+    __syncthreads();
+    for (int k = 0; k < kNBH; ++k) {
+      double va[8], vb[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < 8; ++i) {
+        va[i] = Pp[k][ty + 16 * i];
+        vb[i] = Pq[k][tx + 16 * i];
+      }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[i][j] += va[i] * vb[j];
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[i][j] += va[i] * vb[j];
+    }
+    __syncthreads();
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -375,9 +380,9 @@ __global__ __launch_bounds__(256) void chol_trail_kernel(double* __restrict__ A,
     }
 }
 
-// U = V^-1 by recursive doubling: the 32 x 32 diagonal blocks (from the
+// U = V^-1 by recursive doubling: the 64 x 64 diagonal blocks (from the
 // top left, the last one ragged) are inverted in LDS; then at block size
-// s = 32, 64, ... each pair of neighbouring inverted blocks A = [2ps, 2ps+s)
+// s = 64, 128, ... each pair of neighbouring inverted blocks A = [2ps, 2ps+s)
 // and C = [2ps+s, 2ps+2s) is joined by U_AC = -U_A (V_AC U_C), two batched
 // products per level.  The intermediate V_AC U_C is kept transposed in U's
 // lower triangle (the mirror of U_AC), which nothing else reads.
