@@ -285,6 +285,17 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
             t_oracle += time.perf_counter() - t0
         passes += 1
     us_token = t_oracle / passes * 1e6
+    single = None
+    if len(inputs) <= 4:  # the single GEMV and the one-layer workloads: one thread as well
+        t1, p1 = 0.0, 0
+        while t1 < min_s / 2:
+            for args in inputs:
+                t0 = time.perf_counter()
+                gemv(*args, nthreads=1)
+                t1 += time.perf_counter() - t0
+            p1 += 1
+        single = {"value": round(token_bytes * p1 / t1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                  "us_per_step": round(t1 / p1 * 1e6, 1)}
     model = None
     try:
         for line in open("/proc/cpuinfo"):
@@ -301,6 +312,7 @@ def cpu_baseline(mats, wl, seed, B, min_s=10.0):
         "sample": f"{passes} whole tokens of {wl.name} at batch {B} ({len(mats)} GEMVs, "
                   f"{token_bytes / 1e9:.3f} GB of packed weights each), {t_oracle:.1f} s of oracle time",
         "us_per_token": round(us_token, 1),
+        "single_thread": single,
         "gpu_vs_oracle_max_rel_l2": worst,
         "host": {"cpu_model": model, "usable_cores": len(os.sched_getaffinity(0)), "nproc": os.cpu_count()},
     }
@@ -311,6 +323,73 @@ QUANT_LAYER = (("qkv", 6144, 4096), ("o", 4096, 4096), ("gate_up", 28672, 4096),
 QUANT_SALIENT = 0.05  # the paper's salient-column fraction
 QUANT_LAMBDA = 1.0
 QUANT_ITERS = 2
+
+
+def cold_main(args):
+    """Warm and cold timing of a small workload (one GEMV, one layer), each
+    as C steps back to back in one graph: warm repeats one copy, whose packed
+    bytes stay in the caches; cold walks C copies, each its own seeded
+    weights, so every step streams its weights from HBM."""
+    import dataclasses
+
+    import torch
+
+    import paper_2609_00224_amd as q
+    import synth
+    from synth.workloads import WORKLOADS
+
+    q.load()
+    assert torch.cuda.is_available(), "no GPU"
+    dev = torch.device("cuda:0")
+    base = WORKLOADS[args.workload]
+    assert base.layers == 1, "--cold-copies takes a one-layer workload"
+    C, B = args.cold_copies, args.batch
+    seed = synth.DEFAULT_SEED if args.seed is None else args.seed
+    mats = build_stack(dataclasses.replace(base, layers=C), B, dev, seed)
+    per = len(base.shapes)
+    copies = [mats[i * per:(i + 1) * per] for i in range(C)]
+    step_bytes = sum(m["bytes"] for m in copies[0])
+    stream = torch.cuda.Stream(device=dev)
+    plans = [q.plan_grouped([m["pm"] for m in c], [m["x"] for m in c], [m["y"] for m in c], batch=B) for c in copies]
+    ws = torch.zeros(max(max(q.qtea_workspace_bytes(m["pm"].desc, B) for m in mats), 4), dtype=torch.uint8,
+                     device=dev)
+
+    def graph(fn):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            fn()
+            stream.synchronize()
+            with torch.cuda.graph(g, stream=stream):
+                fn()
+        stream.synchronize()
+        return g
+
+    def grouped(cs):
+        return lambda: [plans[i].run(stream=stream) for i in cs]
+
+    def chained(cs):
+        return lambda: [q.qtea_gemm_lowbatch(m["pm"].desc, m["pm"].packed, m["x"], B, m["y"], ws, stream=stream)
+                        for i in cs for m in copies[i]]
+
+    res = {}
+    for name, mk in (("grouped", grouped), ("chained", chained)):
+        # both graphs run C steps back to back; warm repeats copy 0, cold walks the copies
+        reps, warm_reps = max(1, args.steps // C), max(1, args.warmup // C)
+        warm = time_graph(graph(mk([0] * C)), stream, reps, warm_reps) / C
+        cold = time_graph(graph(mk(range(C))), stream, reps, warm_reps) / C
+        res[name] = {"warm_us": round(warm * 1e3, 2), "cold_us": round(cold * 1e3, 2),
+                     "warm_gbs": round(step_bytes / (warm * 1e-3) / 1e9, 1),
+                     "cold_gbs": round(step_bytes / (cold * 1e-3) / 1e9, 1)}
+        log(f"{base.name} B={B} {name}: warm {res[name]['warm_us']} us ({res[name]['warm_gbs']} GB/s), cold "
+            f"{res[name]['cold_us']} us ({res[name]['cold_gbs']} GB/s) over {C} copies "
+            f"({C * step_bytes / 1e6:.0f} MB)")
+    out = {"metric": "weight-stream GB/s and us per step, warm and cold", "unit": "GB/s",
+           "value": res["grouped"]["cold_gbs"], "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": base.name, "batch": B, "copies": C, "bytes_per_step": step_bytes,
+                      "cold_bytes": C * step_bytes, "seed": seed},
+           "grouped": res["grouped"], "chained": res["chained"]}
+    print(json.dumps(out), flush=True)
 
 
 def quantizer_main(args):
@@ -446,6 +525,9 @@ def main():
     ap.add_argument("--quantizer", action="store_true",
                     help="time the offline quantizer on one Llama-3-8B-shaped layer instead of the GEMV")
     ap.add_argument("--calib-rows", type=int, default=2048, help="calibration rows per Hessian (--quantizer)")
+    ap.add_argument("--cold-copies", type=int, default=0,
+                    help="time the workload warm (one copy replayed) and cold (rotating through this many "
+                         "copies, each with its own weights, far beyond the 256 MB last-level cache)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="after the bench, copy this many bytes device-to-device 3 times "
                          "(known-size reference for HBM counters)")
@@ -457,6 +539,9 @@ def main():
 
     if args.quantizer:
         quantizer_main(args)
+        return
+    if args.cold_copies:
+        cold_main(args)
         return
 
     import torch
