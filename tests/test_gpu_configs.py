@@ -11,7 +11,7 @@ grouped call over the whole set of matrices):
 The 14B- and 70B-shaped stacks are taken two layers deep (every matrix shape
 of the layer at full size; the kernels see the same shapes as in the full
 stacks).  Outputs: every row of matrices up to 4096 x 14336 elements, else
-the first and last 64 rows and 512 random rows, against the fp64 oracle
+the first and last 64 rows and 1024 random rows, against the fp64 oracle
 within the tolerance of gpu_cases.  Decode: the first layer's packed codes
 and residual rows read back bit-exactly.
 """
@@ -80,7 +80,7 @@ def _stack(name, layers):
 def _sample_rows(N, K, rng):
     if N * K <= 4096 * 14336:
         return np.arange(N, dtype=np.int64)
-    rnd = rng.choice(np.arange(64, N - 64), size=512, replace=False)
+    rnd = rng.choice(np.arange(64, N - 64), size=1024, replace=False)
     return np.unique(np.concatenate([np.arange(64), np.arange(N - 64, N), rnd])).astype(np.int64)
 
 
