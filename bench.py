@@ -414,16 +414,33 @@ def quantizer_main(args):
         log(f"quantizer input {role} {N}x{K} ready")
     weights = sum(m["N"] * m["K"] for m in mats)
 
-    def step(times=None):
-        for m in mats:
+    # The matrices are independent and the library is reentrant: each gets
+    # its own stream and host thread (the column phase of one matrix keeps
+    # only a few dozen CUs busy, so the four overlap).
+    from concurrent.futures import ThreadPoolExecutor
+
+    streams = [torch.cuda.Stream(device=dev) for _ in mats]
+    pool = ThreadPoolExecutor(max_workers=len(mats)) if args.quant_concurrent else None
+
+    def one(m, st, times):
+        with torch.cuda.stream(st):
             t0 = time.perf_counter()
-            q.qtea_quant_hessian(m["X"], m["H"])
-            torch.cuda.synchronize()
+            q.qtea_quant_hessian(m["X"], m["H"], stream=st)
+            st.synchronize()
             t1 = time.perf_counter()
-            m["out"] = q.quantize_matrix(m["W"], m["H"], m["nS"], lambda_decay=QUANT_LAMBDA, iters=QUANT_ITERS)
+            m["out"] = q.quantize_matrix(m["W"], m["H"], m["nS"], lambda_decay=QUANT_LAMBDA, iters=QUANT_ITERS,
+                                         stream=st)
             t2 = time.perf_counter()
-            if times is not None:
-                times.setdefault(m["role"], []).append((t1 - t0, t2 - t1))
+        if times is not None:
+            times.setdefault(m["role"], []).append((t1 - t0, t2 - t1))
+
+    def step(times=None):
+        if pool is None:
+            for m, st in zip(mats, streams):
+                one(m, st, times)
+        else:
+            for f in [pool.submit(one, m, st, times) for m, st in zip(mats, streams)]:
+                f.result()
 
     for _ in range(args.warmup):
         step()
@@ -460,7 +477,8 @@ def quantizer_main(args):
         "vs_baseline": None, "dtype": "f64", "data": "synthetic",
         "config": {"workload": "llama3_8b_layer_quantize", "matrices": [list(x) for x in QUANT_LAYER],
                    "calib_rows": args.calib_rows, "salient_frac": QUANT_SALIENT, "lambda_decay": QUANT_LAMBDA,
-                   "iters": QUANT_ITERS, "seed": seed},
+                   "iters": QUANT_ITERS, "seed": seed,
+                   "execution": "four streams, one host thread each" if args.quant_concurrent else "sequential"},
         "per_matrix": per,
         "roofline": roof,
         "cpu_baseline": cpu,
@@ -525,6 +543,8 @@ def main():
     ap.add_argument("--quantizer", action="store_true",
                     help="time the offline quantizer on one Llama-3-8B-shaped layer instead of the GEMV")
     ap.add_argument("--calib-rows", type=int, default=2048, help="calibration rows per Hessian (--quantizer)")
+    ap.add_argument("--quant-sequential", dest="quant_concurrent", action="store_false",
+                    help="quantize the layer's matrices one after another instead of on four streams")
     ap.add_argument("--cold-copies", type=int, default=0,
                     help="time the workload warm (one copy replayed) and cold (rotating through this many "
                          "copies, each with its own weights, far beyond the 256 MB last-level cache)")

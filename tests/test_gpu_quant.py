@@ -149,3 +149,32 @@ def test_quantize_full_size_matrix():
     """A whole Llama-3-8B-shaped O projection (4096 x 4096, 205 salient
     columns, the paper's settings), bit-exact against the oracle."""
     _check(4096, 4096, 205, 1.0, 2, 8)
+
+
+def test_quantize_concurrent_streams_match_sequential():
+    """Two matrices quantized at the same time on two streams from two host
+    threads (the library keeps no state between calls) give exactly the
+    results of one after the other."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    _report("quantize two matrices concurrently on two streams")
+    cases = [synth.quant_inputs(11, 128, 520, 600), synth.quant_inputs(12, 256, 300, 600)]
+    Hs = [_gpu_hessian(X) for _, X in cases]
+    Ws = [_dev(W) for W, _ in cases]
+    seq = [q.quantize_matrix(W, H, 20) for W, H in zip(Ws, Hs)]
+    streams = [torch.cuda.Stream() for _ in cases]
+
+    def run(i):
+        with torch.cuda.stream(streams[i]):
+            return q.quantize_matrix(Ws[i], Hs[i], 20, stream=streams[i])
+
+    with ThreadPoolExecutor(max_workers=2) as pool:
+        con = list(pool.map(run, range(2)))
+    torch.cuda.synchronize()
+    for a, b in zip(seq, con):
+        for key in ("T", "alpha", "beta", "v", "S", "bitmap", "R8", "idx"):
+            assert torch.equal(a[key], b[key]), key
