@@ -178,3 +178,12 @@ def test_quantize_concurrent_streams_match_sequential():
     for a, b in zip(seq, con):
         for key in ("T", "alpha", "beta", "v", "S", "bitmap", "R8", "idx"):
             assert torch.equal(a[key], b[key]), key
+
+
+@pytest.mark.parametrize("N,K,nS,lam,iters,seed", [
+    (8, 1, 1, 1.0, 2, 21),     # one column: one block, one factor element, salient
+    (4, 5, 0, 1.0, 2, 22),     # the smallest row count (one four-row group)
+    (16, 70, 70, 1.0, 2, 23),  # every column salient, two factorization blocks
+])
+def test_quantize_degenerate_shapes(N, K, nS, lam, iters, seed):
+    _check(N, K, nS, lam, iters, seed)
