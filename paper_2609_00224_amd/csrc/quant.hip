@@ -1,6 +1,7 @@
 // QTEA offline quantizer for gfx950 (include/qtea_quant.h), fp64 throughout.
 //
 // Steps of one qtea_quantize call, all on the caller's stream:
+//   0. (qtea_quant_hessian) H = (2/n) X^T X in 128 x 128 tiles.
 //   1. salient columns (Eq. 3): per-column max of W^2 (atomic max on the
 //      bit patterns of non-negative doubles), times diag(H)^2; each column's
 //      rank counted against every other column (exact, deterministic ties);
@@ -20,7 +21,11 @@
 //      (Eq. 6-9) and its update of the block's later columns; after the
 //      block, the trailing columns' rank-128 update.
 // Floating-point contraction is off in this file: every product and sum is
-// rounded as written, in the order the method states it.
+// rounded as written, in the order the method states it.  The dense products
+// (Hessian, factorization, inverse, trailing update) accumulate with explicit
+// fused multiply-adds: in the Hessian the products of fp32 inputs are exact
+// in fp64, so fusing changes nothing; elsewhere their summation order is the
+// kernel's own anyway.
 #include <math.h>
 
 #include "qtea_internal.h"
@@ -119,40 +124,41 @@ __device__ inline int tern(double x, double thr) { return x > thr ? 1 : (x < -th
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void hess_kernel(const float* __restrict__ X, int64_t n, int64_t K, double scale,
                                                    double* __restrict__ H) {
-  __shared__ double xa[32][65], xb[32][65];
-  const int64_t a0 = int64_t(blockIdx.y) * 64, b0 = int64_t(blockIdx.x) * 64;
+  // 128 x 128 output tile, 8 x 8 per thread, calibration rows staged 16 at a time
+  __shared__ double xa[16][129], xb[16][129];
+  const int64_t a0 = int64_t(blockIdx.y) * 128, b0 = int64_t(blockIdx.x) * 128;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4];
+  double acc[8][8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
-  for (int64_t t0 = 0; t0 < n; t0 += 32) {
-    for (int e = threadIdx.x; e < 32 * 64; e += 256) {
-      const int tt = e >> 6, c = e & 63;
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
+  for (int64_t t0 = 0; t0 < n; t0 += 16) {
+    for (int e = threadIdx.x; e < 16 * 128; e += 256) {
+      const int tt = e >> 7, c = e & 127;
       const int64_t t = t0 + tt;
       xa[tt][c] = (t < n && a0 + c < K) ? double(X[t * K + a0 + c]) : 0.0;
       xb[tt][c] = (t < n && b0 + c < K) ? double(X[t * K + b0 + c]) : 0.0;
     }
     __syncthreads();
-    for (int tt = 0; tt < 32; ++tt) {
-      double va[4], vb[4];
+    for (int tt = 0; tt < 16; ++tt) {
+      double va[8], vb[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int i = 0; i < 8; ++i) {
         va[i] = xa[tt][ty + 16 * i];
         vb[i] = xb[tt][tx + 16 * i];
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += va[i] * vb[j];
+        for (int j = 0; j < 8; ++j) acc[i][j] = fma(va[i], vb[j], acc[i][j]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       const int64_t a = a0 + ty + 16 * i, b = b0 + tx + 16 * j;
       if (a < K && b < K) H[a * K + b] = scale * acc[i][j];
     }
@@ -367,7 +373,7 @@ __global__ __launch_bounds__(256) void chol_trail_kernel(double* __restrict__ A,
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] += va[i] * vb[j];
+        for (int j = 0; j < 8; ++j) acc[i][j] = fma(va[i], vb[j], acc[i][j]);
     }
     __syncthreads();
   }
@@ -463,7 +469,7 @@ __global__ __launch_bounds__(256) void trinv_join_kernel(const double* __restric
 #pragma unroll
       for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int n = 0; n < 4; ++n) acc[m][n] += va[m] * vb[n];
+        for (int n = 0; n < 4; ++n) acc[m][n] = fma(va[m], vb[n], acc[m][n]);
     }
     __syncthreads();
   }
@@ -739,7 +745,7 @@ __global__ __launch_bounds__(256) void trail_gemm_kernel(double* __restrict__ Wt
 #pragma unroll
       for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int n = 0; n < 4; ++n) acc[m][n] += uk[m] * er[n];
+        for (int n = 0; n < 4; ++n) acc[m][n] = fma(uk[m], er[n], acc[m][n]);
     }
     __syncthreads();
   }
@@ -760,7 +766,7 @@ extern "C" {
 
 int qtea_quant_hessian(const float* X, int64_t n, int64_t K, double* H, void* stream) {
   if (!X || !H || n < 1 || K < 1 || K > kQMaxCols) return QTEA_ERR_INVALID_ARG;
-  const int64_t T = q_cdiv(K, 64);
+  const int64_t T = q_cdiv(K, 128);
   if (T > 65535) return QTEA_ERR_INVALID_ARG;
   hipLaunchKernelGGL(hess_kernel, dim3(uint32_t(T), uint32_t(T)), dim3(256), 0, static_cast<hipStream_t>(stream), X,
                      n, K, 2.0 / double(n), H);
