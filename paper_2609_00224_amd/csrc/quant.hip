@@ -38,6 +38,7 @@ namespace {
 constexpr int kQG = QTEA_QUANT_GROUP;  // columns per group and per GPTQ block
 constexpr int kNB = 64;                // factorization block
 constexpr int kNBH = 32;               // panel columns staged per LDS pass of the trailing update
+static_assert(kNB <= 64, "the diagonal block's elimination maps one column per lane of a wave");
 constexpr int kCT = 64;                // threads of the row-parallel kernels (one wave)
 constexpr int kColChunk = 16;          // later columns of a block updated per workgroup
 constexpr int64_t kQAlign = 256;
@@ -302,9 +303,12 @@ __global__ __launch_bounds__(256) void chol_diag_kernel(double* __restrict__ A, 
       if (threadIdx.x == 0) status[0] = 1;
       piv = 1.0;
     }
-    for (int e = threadIdx.x; e < c * c; e += 256) {
-      const int p = e / c, q = e % c;
-      if (p <= q) D[p][q] -= D[p][c] * (D[q][c] / piv);
+    // lane q = tid % 64 of the four row phases p = tid / 64, +4, ... (no
+    // per-element division); D[q][c] / piv is the same factor for a column
+    const int q = threadIdx.x & 63;
+    if (q < c) {
+      const double f = D[q][c] / piv;
+      for (int p = threadIdx.x >> 6; p <= q; p += 4) D[p][q] -= D[p][c] * f;
     }
     __syncthreads();
   }
