@@ -525,22 +525,38 @@ __global__ __launch_bounds__(256) void transpose_kernel(const double* __restrict
 __global__ __launch_bounds__(kCT) void group_params_kernel(const double* __restrict__ Wt, int64_t N, int64_t K,
                                                            int64_t G, int64_t g, uint16_t* __restrict__ alpha,
                                                            uint16_t* __restrict__ beta) {
+  // the row's block values are read from memory once, eight loads in flight,
+  // into this thread's LDS column; the passes below read them there
+  __shared__ double wl[kQG][kCT];
   const int64_t r = int64_t(blockIdx.x) * kCT + threadIdx.x;
   if (r >= N) return;
   const int64_t b0 = g * kQG, b1 = b0 + kQG < K ? b0 + kQG : K;
-  const double n = double(b1 - b0);
-  const double* w = Wt + b0 * N + r;
+  const int nb = int(b1 - b0);
+  const double n = double(nb);
+  {
+    const double* src = Wt + b0 * N + r;
+    int k = 0;
+    for (; k + 8 <= nb; k += 8) {
+      double v[8];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) v[m] = src[int64_t(k + m) * N];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) wl[k + m][threadIdx.x] = v[m];
+    }
+    for (; k < nb; ++k) wl[k][threadIdx.x] = src[int64_t(k) * N];
+  }
+  auto w = [&](int k) { return wl[k][threadIdx.x]; };
   double sw = 0.0;
-  for (int64_t k = 0; k < b1 - b0; ++k) sw += w[k * N];
+  for (int k = 0; k < nb; ++k) sw += w(k);
   double be = sw / n, sa = 0.0;
-  for (int64_t k = 0; k < b1 - b0; ++k) sa += fabs(w[k * N] - be);
+  for (int k = 0; k < nb; ++k) sa += fabs(w(k) - be);
   double al = sa / n;
   for (int round = 0; round < 2; ++round) {
     if (!(al > 0.0)) break;
     const double thr = al / 2.0;
     double s1 = 0.0, s2 = 0.0, stw = 0.0;
-    for (int64_t k = 0; k < b1 - b0; ++k) {
-      const double x = w[k * N];
+    for (int k = 0; k < nb; ++k) {
+      const double x = w(k);
       const int t = tern(x - be, thr);
       s1 += double(t);
       s2 += double(t * t);
