@@ -83,6 +83,8 @@ int qtea_quant_workspace_bytes(int64_t N, int64_t K, int64_t* out_bytes);
  *                 j/32 set for a salient column
  *   resid_val     device uint8 [n_salient][N/4]: E4M3 residual codes
  *   resid_idx     device uint8 [n_salient][N/4]: row within the four-row group
+ *                 (salient, resid_val and resid_idx may be NULL when
+ *                 n_salient is 0)
  *   Q             device fp64 [N][K] (or NULL): the dequantized weights
  *                 beta + (v alpha) t plus the residual
  *   workspace     device, >= qtea_quant_workspace_bytes(N, K)

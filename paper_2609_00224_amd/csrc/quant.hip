@@ -805,9 +805,9 @@ int qtea_quantize(const double* W, const double* H, int64_t N, int64_t K, const 
                   int64_t workspace_bytes, void* stream) {
   int64_t need = 0;
   if (qtea_quant_workspace_bytes(N, K, &need) != QTEA_OK) return QTEA_ERR_INVALID_ARG;
-  if (!W || !H || !p || !T || !group_scale || !group_bias || !col_rescale || !resid_val || !resid_idx)
+  if (!W || !H || !p || !T || !group_scale || !group_bias || !col_rescale) return QTEA_ERR_INVALID_ARG;
+  if (p->n_salient < 0 || p->n_salient > K || (p->n_salient > 0 && (!salient || !resid_val || !resid_idx)))
     return QTEA_ERR_INVALID_ARG;
-  if (p->n_salient < 0 || p->n_salient > K || (p->n_salient > 0 && !salient)) return QTEA_ERR_INVALID_ARG;
   if (p->iters < 0 || p->iters > QTEA_QUANT_MAX_ITERS || p->reserved != 0) return QTEA_ERR_INVALID_ARG;
   if (!(p->lambda_decay >= 0.0) || !isfinite(p->lambda_decay) || !(p->damp >= 0.0) || !isfinite(p->damp))
     return QTEA_ERR_INVALID_ARG;

@@ -142,3 +142,9 @@ def test_quantizer_host_checks(lib):
                 q.QteaQuantParams(2, float("nan"), 0.01, 2, 0)):
         a = [vp, vp, 8, 10, ctypes.byref(bad)] + [vp] * 10
         assert lib.qtea_quantize(*a, 1 << 30, None) == q.QTEA_ERR_INVALID_ARG
+    # salient outputs are required only when there are salient columns
+    none_sal = [vp, vp, 8, 10, ctypes.byref(p), vp, vp, vp, vp, None, None, None, None, None]
+    assert lib.qtea_quantize(*none_sal, vp, 0, None) == q.QTEA_ERR_INVALID_ARG  # two salient columns, no outputs
+    p0 = q.QteaQuantParams(0, 1.0, 0.01, 2, 0)
+    none_sal[4] = ctypes.byref(p0)
+    assert lib.qtea_quantize(*none_sal, vp, 0, None) == q.QTEA_ERR_WORKSPACE  # accepted up to the workspace
