@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 7
+#define QTEA_ABI_VERSION 8
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -294,14 +294,35 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
  * Run a planned grouped GEMV: one persistent launch, followed by a small
  * second launch that sums the parts of split panels (when the plan has
  * any, info->n_split_panels).  `workspace` (>= info->workspace_bytes) holds
- * the chunk queue counter (its first 4 bytes) and the partial rows of split
- * panels.  The counter must be zero before the first call (zero-fill the
- * workspace once); every completed call leaves it at zero.  Calls that may
- * overlap in time must not share a workspace.  fp32 accumulation, run-to-run
+ * the chunk queue's counters and error flags (its first 256 bytes) and the
+ * partial rows of split panels.  Zero-fill it once before the first call;
+ * every call leaves the counters at zero (see qtea_grouped_status for the
+ * error flags).  Calls that may overlap in time must not share a workspace.  fp32 accumulation, run-to-run
  * deterministic (parts are summed in a fixed order).
  */
 int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* workspace,
                       int64_t workspace_bytes, void* stream);
+
+/*
+ * Error flags a grouped workspace has collected, read into *flags (host);
+ * synchronizes `stream` (after the calls whose outcome is wanted).  The
+ * batch-1 launch hands out chunks from a counter in the workspace and
+ * checks its own accounting:
+ *   QTEA_QUEUE_STALE  a take found the counter past the plan's count: the
+ *                     counter did not start at zero (a workspace that was
+ *                     not zero-filled, or one left by a call that did not
+ *                     complete); that take yields no chunk, so some outputs
+ *                     of the call were not written
+ *   QTEA_QUEUE_COUNT  the launch's takes did not add up to the plan's count
+ * Either flag means the outputs of the flagged call are not to be used.
+ * The last workgroup of every launch leaves the counters at zero, so the
+ * next call starts clean; the flags stay set until the workspace is
+ * zero-filled again (qtea_workspace_init).  Errors: QTEA_ERR_INVALID_ARG
+ * (null pointer), QTEA_ERR_HIP.
+ */
+#define QTEA_QUEUE_STALE 1u
+#define QTEA_QUEUE_COUNT 2u
+int qtea_grouped_status(const void* workspace, uint32_t* flags, void* stream);
 
 #ifdef __cplusplus
 }

@@ -11,7 +11,7 @@ Entry points carry the C names: qtea_packed_bytes, qtea_pack,
 qtea_packed_bytes_e4m3, qtea_pack_e4m3, qtea_packed_bytes_g128, qtea_pack_g128,
 qtea_workspace_bytes, qtea_workspace_init, qtea_gemv, qtea_gemm_lowbatch,
 qtea_debug_unpack, qtea_read_ceiling, qtea_status_string, qtea_abi_version,
-qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv,
+qtea_grouped_plan_bytes, qtea_grouped_plan, qtea_grouped_gemv, qtea_grouped_status,
 qtea_quant_hessian, qtea_quant_workspace_bytes, qtea_quantize.
 """
 from __future__ import annotations
@@ -33,6 +33,7 @@ QTEA_ERR_HIP = -6
 QTEA_ERR_NOT_POSITIVE = -7
 QTEA_QUANT_GROUP = 128
 QTEA_MAX_BATCH = 16
+QTEA_ABI_VERSION = 8  # the header this binding mirrors
 QTEA_DESC_MAGIC = 0x51544541
 
 # Every function the header declares (checked by tests/test_abi.py).
@@ -40,6 +41,7 @@ EXPORTS = (
     "qtea_status_string", "qtea_abi_version", "qtea_packed_bytes", "qtea_pack",
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
     "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
+    "qtea_grouped_status",
     "qtea_packed_bytes_e4m3", "qtea_pack_e4m3", "qtea_packed_bytes_g128", "qtea_pack_g128",
     "qtea_read_ceiling", "qtea_quant_hessian", "qtea_quant_workspace_bytes", "qtea_quantize",
 )
@@ -137,6 +139,8 @@ def load(path: str = LIB_PATH):
                                       i32, i32, vp, i64, pinfo, vp]
     lib.qtea_grouped_gemv.restype = i32
     lib.qtea_grouped_gemv.argtypes = [pinfo, vp, vp, i64, vp]
+    lib.qtea_grouped_status.restype = i32
+    lib.qtea_grouped_status.argtypes = [vp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.qtea_quant_hessian.restype = i32
     lib.qtea_quant_hessian.argtypes = [vp, i64, i64, vp, vp]
     lib.qtea_quant_workspace_bytes.restype = i32
@@ -358,6 +362,19 @@ def qtea_grouped_gemv(info: QteaGroupedInfo, plan, workspace, stream=None):
     _check(load().qtea_grouped_gemv(ctypes.byref(info), _ptr(plan), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _stream(stream)),
            "qtea_grouped_gemv")
+
+
+QTEA_QUEUE_STALE = 1  # a chunk-queue take found the counter past the plan's count
+QTEA_QUEUE_COUNT = 2  # a launch's takes did not add up to the plan's count
+
+
+def qtea_grouped_status(workspace, stream=None) -> int:
+    """Error flags a grouped workspace has collected (0: none); synchronizes
+    the stream.  Zero-filling the workspace clears them."""
+    _need_cuda(workspace)
+    out = ctypes.c_uint32(0)
+    _check(load().qtea_grouped_status(_ptr(workspace), ctypes.byref(out), _stream(stream)), "qtea_grouped_status")
+    return int(out.value)
 
 
 @dataclass

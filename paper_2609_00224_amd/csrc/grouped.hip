@@ -57,7 +57,8 @@ constexpr int kResCols8 = 32;
 static_assert(kSlicePacks * 4 == 256, "one table row of 256 bytes per code");
 
 static_assert(kSliceCols % 64 == 0, "staging by whole waves");
-static_assert(kSlicePacks * 8 == kGT, "one 27-code build task per thread, codes 0..215");
+static_assert(kSlicePacks == 64 && kSlicePacks * 8 == kGT,
+              "one 27-code build task per thread, codes 0..215, one wave per pair of leading trits");
 static_assert(kSliceCols <= kGT, "one staged column per thread");
 
 
@@ -82,6 +83,42 @@ static_assert(2 * kResCols * 32 == 1024 && 2 * kResCols8 * 16 == 1024,
 static_assert(kWgPerCu * GLds<8>::BYTES <= 160 * 1024, "two workgroups per CU");
 
 
+
+// The chunk queue's words in the first bytes of the workspace: word 0 the
+// take counter, word 1 error flags (sticky until the workspace is
+// zero-filled again), words 2-3 a 64-bit exit word: the count of finished
+// workgroups (high half) and of the chunks they ran (low half).  The
+// workgroup whose exit completes a multiple of the grid checks that the
+// launch ran every chunk once and took exactly the plan's count, and leaves
+// the take counter and the exit word at zero for the next launch.  A take
+// past the plan's count yields no chunk, so every index stays in range,
+// and sets kQueueStale.  A launch that finds the words in a state a
+// completed launch does not leave reports it, one way or the other.
+constexpr uint32_t kQueueStale = 1u;  // a take found the counter past the plan's count
+constexpr uint32_t kQueueCount = 2u;  // the launch's chunks or takes did not add up to the plan's
+
+__device__ __forceinline__ void queue_exit(uint32_t* counters, uint32_t n_grabs, uint32_t n_chunks,
+                                           uint32_t my_chunks) {
+  if (threadIdx.x != 0) return;
+  // Relaxed: every queue word is read and written only by device-scope
+  // atomics, which the device performs at one coherence point, and each
+  // workgroup's takes have returned before it issues its exit, so the exit
+  // that completes the count comes after every take of the launch.  (An
+  // acquire-release here would write back and invalidate the L2 of the
+  // workgroup's XCD at every exit, under the other workgroups' loads.)
+  uint64_t* ew = reinterpret_cast<uint64_t*>(counters + 2);
+  const uint64_t old = __hip_atomic_fetch_add(ew, (uint64_t(1) << 32) | my_chunks, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
+  if ((uint32_t(old >> 32) + 1u) % gridDim.x != 0u) return;
+  const uint32_t ran = uint32_t(old) + my_chunks;
+  const uint32_t taken = __hip_atomic_load(counters, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (ran != n_chunks || taken != n_grabs)
+    __hip_atomic_fetch_or(counters + 1, kQueueCount, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(counters, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(ew, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 // Selector of v_perm_b32 that forms (byte k of src1) << 8 | (byte k of src0).
 __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
@@ -115,9 +152,13 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // at the first unit of a chunk, one chunk ahead of need.  The next chunk's
   // record is loaded at the top of every unit and first used after the
   // table build's barrier, so a chunk switch does not wait for it.
-  if (g >= NC) return;
+  const uint32_t n_grabs = uint32_t(H->n_grabs);
+  if (g >= NC) {
+    queue_exit(counters, n_grabs, uint32_t(NC), 0u);
+    return;
+  }
   int c = g, cn = g + G;
-  const uint32_t last_take = uint32_t(H->n_grabs - 1);
+  uint32_t my_chunks = 1;  // chunks this workgroup has started
   int* cnext_lds = flag + 1;  // chunk taken from the queue, published at the unit's last barrier
 
   const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, l16 = lane & 15;
@@ -337,15 +378,15 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     // d4 d3) for d4 d3 < 22 writes 27 codes; pass 1: task (pack, d2) writes
     // the nine codes 22 d2 d1 d0, so that no wave does two 27-code tasks.
     {
-      const int p = tid & (kSlicePacks - 1);
+      const int p = lane;
       const float a0 = a_lds[5 * p], a1 = a_lds[5 * p + 1], a2 = a_lds[5 * p + 2];
       const float a3 = a_lds[5 * p + 3], a4 = a_lds[5 * p + 4];
-      const int top = tid / kSlicePacks;  // 0..7: d4 d3 in base 3
-      const int d4 = (top * 11) >> 5;
-      const int d3 = top - 3 * d4;
-      const float t4 = d4 == 0 ? -a4 : (d4 == 2 ? a4 : 0.0f);
-      const float t3 = d3 == 0 ? -a3 : (d3 == 2 ? a3 : 0.0f);
-      const float base = t4 + t3;
+      // the wave's task: d4 d3 = w in base 3 (wave-uniform), so the two
+      // leading trits are uniform signs and their part is one product and
+      // one fused multiply-add (both exact but the last rounding, as t4 + t3)
+      const int d4 = (w * 11) >> 5;
+      const int d3 = w - 3 * d4;
+      const float base = __builtin_fmaf(float(d3 - 1), a3, float(d4 - 1) * a4);
       lds_char* dst = (lds_char*)smem + p * 4 + (27 * d3 + 81 * d4) * 256;
 #pragma unroll
       for (int e2 = 0; e2 < 3; ++e2) {
@@ -396,8 +437,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const int n_grp = min(nxt.slice * kSliceGroups + q, n_ng - 1), n_t0 = nxt.panel * TPP + wt;
     const uint32_t smask = has_next ? 0xffffffffu : 0u;
     const uint32_t lane_off = ((uint32_t(n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & smask;
-#pragma unroll
-    for (int t = 0; t < RB; ++t) acc[t] = pstart ? 0.0f : acc[t];
+    // (the sums restart after every panel end: a part starts right after one)
     // layout 4: the sum of x over this quarter's group, for the first
     // quarter of each group (the other adds no bias)
     float xq = 0.0f;
@@ -443,7 +483,16 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     }
 
     // 4. residual of this slice: each lane's four rows accumulate in registers
-    // over the panel's slices (fixed order: deterministic)
+    // over the panel's slices (fixed order: deterministic).  A product goes
+    // to the row its 2-bit position names without a compare per row: x's
+    // fp16 bits shifted left by 16 * position put x in that row's 16-bit
+    // lane of a 64-bit word and zeros in the other three, and each row adds
+    // R times its lane in one mixed-precision multiply-add (fp16 operands,
+    // fp32 sum; R x is exact in fp32, so each sum is rounded once, as R x
+    // added to it).  E4M3 values enter as fp16 bits of value * 2^-8 (the
+    // seven magnitude bits at bits 7..13; exact, subnormal codes included)
+    // and the sums are scaled back by 2^8 at the panel end: bit for bit the
+    // unscaled sums, since no product or sum comes near fp32's limits.
     const int s_lo = s_lo_c, s_hi = s_hi_c;
     const int ncol = s_hi - s_lo;
     const int grow = cur.panel * (RP / 4) + gi;  // global four-row group
@@ -451,37 +500,47 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const uint32_t gsh = 2u * uint32_t(g16);
 #pragma unroll
     for (int k = 0; k < 4; ++k) racc[k] = pstart ? 0.0f : racc[k];
+    // R (fp16 bits, or an E4M3 byte) times x (fp16 bits) into row `pos` of the group
+    auto radd = [&](uint32_t rbits, uint32_t pos, uint32_t xbits) {
+      const uint32_t rh = F8 ? ((rbits & 0x7fu) << 7) | ((rbits & 0x80u) << 8) : rbits;
+      const _Float16 r = __builtin_bit_cast(_Float16, uint16_t(rh));
+      const uint64_t x4 = uint64_t(xbits) << (pos << 4);  // xbits: zero above bit 15
+      const half2_t xl = __builtin_bit_cast(half2_t, uint32_t(x4)), xh = __builtin_bit_cast(half2_t, uint32_t(x4 >> 32));
+      racc[0] = __builtin_fmaf(float(r), float(xl.x), racc[0]);
+      racc[1] = __builtin_fmaf(float(r), float(xl.y), racc[1]);
+      racc[2] = __builtin_fmaf(float(r), float(xh.x), racc[2]);
+      racc[3] = __builtin_fmaf(float(r), float(xh.y), racc[3]);
+    };
     {
       // stage in this wave's own LDS area: only this wave reads it back, and a
       // wave's LDS accesses complete in order, so no barrier is needed.  The
-      // column indices are replaced by the columns' activations.
+      // column indices are replaced by the fp16 bits of the columns' activations.
       char* rv_w = lds + L::RV + w * 1024;
       uint32_t* ri_w = reinterpret_cast<uint32_t*>(lds + L::RI + w * 256);
       *reinterpret_cast<u32x4*>(rv_w + 16 * lane) = rvq;
-      const int xc = xcol(int(ris));
-      const uint32_t xw = __float_as_uint(xr_lds[xc >= 0 && xc < kSliceCols ? xc : 0]);
-      ri_w[lane] = lane < 32 ? ris : xw;
+      auto xbits_at = [&](uint32_t col) -> uint32_t {
+        const int xc = xcol(int(col));
+        const float xf = xr_lds[xc >= 0 && xc < kSliceCols ? xc : 0];
+        return uint32_t(__builtin_bit_cast(uint16_t, (_Float16)xf));  // exact: x is an fp16 value
+      };
+      ri_w[lane] = lane < 32 ? ris : xbits_at(ris);
       asm volatile("" ::: "memory");
       const int nc = grow_ok ? (ncol < RC ? ncol : RC) : 0;
-      // columns [c0, c1) with their position words and activations at ri_w
-      // (value rows of 512 bytes per tile: 32 bytes per fp16 column, 16 per E4M3 one)
+      // columns [c0, min(c1, c0 + 16)) with their position words and activations
+      // at ri_w (value rows of 512 bytes per tile: 32 bytes per fp16 column,
+      // 16 per E4M3 one); the lane's columns c0 + rq + QR i
       auto columns = [&](int c0, int c1) {
-        for (int c = c0 + rq; c < c1; c += QR) {
-          const float rv = F8 ? e4m3_to_float(reinterpret_cast<const uint8_t*>(rv_w)[512 * rtile + 16 * c + g16])
-                              : h2f(reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * c + g16]);
-          const uint32_t idx = (ri_w[16 * rtile + c - c0] >> gsh) & 3u;
-          const float xv = __uint_as_float(ri_w[32 + c - c0]);
-          const float t = rv * xv;
-#pragma unroll
-          for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+        const int ce = (c1 < c0 + 16 ? c1 : c0 + 16) - c0;
+        for (int cl = rq; cl < ce; cl += QR) {  // column within the batch of 16
+          const uint32_t rb = F8 ? uint32_t(reinterpret_cast<const uint8_t*>(rv_w)[512 * rtile + 16 * (c0 + cl) + g16])
+                                 : uint32_t(reinterpret_cast<const uint16_t*>(rv_w)[256 * rtile + 16 * cl + g16]);
+          radd(rb, (ri_w[16 * rtile + cl] >> gsh) & 3u, ri_w[32 + cl]);
         }
       };
-      columns(0, nc < 16 ? nc : 16);
+      columns(0, nc);
       if (F8 && ncol > 16) {  // uniform: columns 16..31 through the same words area
         asm volatile("" ::: "memory");  // after the reads above (same wave: in order)
-        const int xc2 = xcol(int(ris2));
-        const uint32_t xw2 = __float_as_uint(xr_lds[xc2 >= 0 && xc2 < kSliceCols ? xc2 : 0]);
-        ri_w[lane] = lane < 32 ? ris2 : xw2;
+        ri_w[lane] = lane < 32 ? ris2 : xbits_at(ris2);
         asm volatile("" ::: "memory");
         columns(16, nc);
       }
@@ -491,11 +550,10 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       for (int s = s_lo + RC + rq; s < s_hi; s += QR) {
         if (grow_ok) {
           const int64_t vi = rval_index(grow, s, pr.nS);
-          const float rv = F8 ? e4m3_to_float(reinterpret_cast<gu8*>(gptr(pr.rval))[vi]) : h2f(gptr(pr.rval)[vi]);
-          const float t = rv * xr_lds[xcol(gptr(pr.S)[s])];
-          const uint32_t idx = (gptr(pr.ridx)[T * pr.nS + s] >> gsh) & 3u;
-#pragma unroll
-          for (int k = 0; k < 4; ++k) racc[k] += idx == uint32_t(k) ? t : 0.0f;
+          const uint32_t rb = F8 ? uint32_t(reinterpret_cast<gu8*>(gptr(pr.rval))[vi]) : uint32_t(gptr(pr.rval)[vi]);
+          const float xf = xr_lds[xcol(gptr(pr.S)[s])];
+          const uint32_t xb = uint32_t(__builtin_bit_cast(uint16_t, (_Float16)xf));
+          radd(rb, (gptr(pr.ridx)[T * pr.nS + s] >> gsh) & 3u, xb);
         }
       }
     }
@@ -503,9 +561,11 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     // the previous unit's build and residual, are behind the last barrier)
     stage(nxt, sb ^ 1);
     if (take && tid == 0) {
-      *cnext_lds = 2 * G + int(taken);
-      // the last of the launch's takes resets the queue for the next launch
-      if (taken == last_take) __hip_atomic_store(counters, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // a take past the plan's count (a queue counter left over from a call
+      // that did not complete) yields no chunk and is reported
+      const bool ok = taken < n_grabs;
+      *cnext_lds = ok ? 2 * G + int(taken) : NC;
+      if (!ok) __hip_atomic_fetch_or(counters + 1, kQueueStale, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     if (pend) {
       // the group's four row sums over its QR lanes (shuffles, fixed order)
@@ -514,7 +574,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       for (int k = 0; k < 4; ++k) {
         float h = racc[k];
         if (QR == 4) h += __shfl_xor(h, 16);
-        r4[k] = h + __shfl_xor(h, 32);
+        h += __shfl_xor(h, 32);
+        r4[k] = F8 ? h * 256.0f : h;  // E4M3 sums were taken at 2^-8
       }
       if (rq == 0) {
 #pragma unroll
@@ -530,6 +591,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       for (int t = 0; t < RB; ++t) {
         const float s2 = acc[t] + __shfl_xor(acc[t], 16);
         tot[t] = s2 + __shfl_xor(s2, 32);
+        acc[t] = 0.0f;
       }
       float val[RF];
       int prow[RF];
@@ -564,6 +626,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     if (take) ctaken = __builtin_amdgcn_readfirstlane(*cnext_lds);  // written before the last barrier
     chunk_first = chunk_last;
     if (chunk_last) {
+      ++my_chunks;
       c = cn;
       u = rec_cn.ub;
       ue = rec_cn.ue;
@@ -578,6 +641,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     if (!G128) load_alpha(nxt, al);  // and of its row scales
     cur = nxt;
   }
+  queue_exit(counters, n_grabs, uint32_t(NC), my_chunks);
 }
 
 // Sums the parts of every split panel in chunk order (deterministic) and
@@ -912,6 +976,17 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   info->n_units = total_units;
   info->plan_bytes = need;
   info->workspace_bytes = kAlign + 2 * n_chunks * RP * int64_t(batch) * 4;
+  return QTEA_OK;
+}
+
+int qtea_grouped_status(const void* workspace, uint32_t* flags, void* stream) {
+  if (!workspace || !flags) return QTEA_ERR_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t h = 0;
+  if (hipMemcpyAsync(&h, static_cast<const uint32_t*>(workspace) + 1, 4, hipMemcpyDeviceToHost, st) != hipSuccess)
+    return QTEA_ERR_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return QTEA_ERR_HIP;
+  *flags = h;
   return QTEA_OK;
 }
 

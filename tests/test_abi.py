@@ -40,7 +40,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert q.qtea_abi_version() == 7
+    hdr = open(os.path.join(ROOT, "include", "qtea.h")).read()
+    assert int(re.search(r"#define QTEA_ABI_VERSION (\d+)", hdr).group(1)) == q.QTEA_ABI_VERSION
+    assert q.qtea_abi_version() == q.QTEA_ABI_VERSION
     assert q.qtea_status_string(0) == "ok"
     for s in range(-7, 0):
         assert q.qtea_status_string(s) != "unknown status"

@@ -202,3 +202,56 @@ def test_grouped_errors():
     with pytest.raises(q.QteaError) as e:
         q.qtea_grouped_gemv(info, plan, small)
     assert e.value.status == q.QTEA_ERR_WORKSPACE
+
+
+def test_grouped_queue_left_over_counter_is_flagged():
+    """A chunk-queue counter that does not start at zero (as after a call
+    that did not complete, or a workspace that was not zero-filled) is set
+    from the host: the launch stays in bounds, reports the condition through
+    qtea_grouped_status, and leaves the counters at zero, so the next call
+    (after the workspace is zero-filled, which clears the flags) is exact."""
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    cases = _synth_group(2, seed=9)
+    _report("grouped queue: left-over counters (8 matrices)")
+    mats = [gpu_pack(c) for c in cases]
+    xs = [to_dev(c["x"]) for c in cases]
+    ys = [torch.full((1, c["N"]), float("nan"), dtype=torch.float32, device="cuda") for c in cases]
+    gp = q.plan_grouped(mats, xs, ys)
+    info, ws = gp.info, gp.workspace
+    assert info.n_chunks > 2 * info.grid, "the plan should hand out chunks from the queue"
+
+    def run_clean():
+        for y in ys:
+            y.fill_(float("nan"))
+        gp.run()
+        torch.cuda.synchronize()
+        assert q.qtea_grouped_status(ws) == 0
+        return [y.cpu().numpy() for y in ys]
+
+    first = run_clean()
+    for c, y in zip(cases, first):
+        ref, wmax = oracle_rows(c)
+        assert_close(y, ref, c["x"], wmax, f"grouped {c['N']}x{c['K']}")
+    # workspace words: [0] take counter, [1] flags, [2] chunks run, [3] workgroups finished
+    words = ws[:16].view(torch.int32)
+    for start_take, start_exit in ((5, 0), (-(2 ** 31), 0), (0, 3)):
+        _report(f"grouped queue: take counter {start_take & 0xffffffff}, exit count {start_exit}")
+        words[0] = start_take
+        words[3] = start_exit
+        torch.cuda.synchronize()
+        gp.run()
+        flags = q.qtea_grouped_status(ws)
+        assert flags & (q.QTEA_QUEUE_STALE | q.QTEA_QUEUE_COUNT), "left-over counters not reported"
+        if start_take < 0:
+            assert flags & q.QTEA_QUEUE_STALE
+        if start_exit == 0:
+            assert words[0].item() == 0 and words[2].item() == 0 and words[3].item() == 0, "counters not reset"
+        ws.zero_()
+        again = run_clean()
+        for a, b in zip(first, again):
+            assert np.array_equal(a, b)
+
+

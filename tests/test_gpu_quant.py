@@ -105,6 +105,24 @@ def test_quantize_matches_oracle(N, K, nS, lam, iters, seed):
     _check(N, K, nS, lam, iters, seed)
 
 
+@pytest.mark.parametrize("case", ["A", "B", "C"])
+def test_salient_choice_hand_derived_eq3(case):
+    """The GPU's salient column on the hand-derived Eq. 3 cases of the
+    oracle's pins (each case flips under a mean over rows, diag(H) to the
+    first power, or |W| in place of W^2): expected column written by hand."""
+    import paper_2609_00224_amd as q
+
+    _report(f"quantize salient hand case {case}")
+    W, H, chosen = {
+        "A": ([[-3.0, 2.0], [0.0, 2.0], [0.0, 2.0], [0.0, 2.0]], [[1.0, 0.0], [0.0, 1.0]], 0),
+        "B": ([[2.0, 1.0], [0.0, 0.0], [0.0, 0.0], [0.0, 0.0]], [[1.0, 0.9], [0.9, 3.0]], 1),
+        "C": ([[0.0, 0.0], [2.0, 0.0], [0.0, -1.0], [0.0, 0.0]], [[1.0, 1.2], [1.2, 1.5]], 0),
+    }[case]
+    out = q.quantize_matrix(_dev(np.array(W)), _dev(np.array(H)), 1)
+    assert out["S"].cpu().tolist() == [chosen]
+    assert int(out["bitmap"][0].item()) == 1 << chosen
+
+
 def test_quantize_dead_channel():
     _check(48, 200, 10, 1.0, 2, 5, dead=7)
 

@@ -12,9 +12,11 @@ not come from the oracle itself:
   * a matrix that is exactly beta + c alpha t is reproduced exactly;
   * the E4M3 rounding against torch's float8_e4m3fn conversion and the
     format's tie and saturation rules;
-  * the salient set is the subset of that size with the largest score sum
-    (brute force over subsets) and is invariant under row permutations and
-    positive scalings;
+  * the salient score of Eq. 3 on hand-derived cases whose choice flips
+    under a mean over rows, diag(H) to the first power, or |W| in place of
+    W^2; the salient set is the subset of that size with the largest score
+    sum (brute force over subsets) and is invariant under row permutations
+    and positive scalings;
   * the Hessian against explicit sums; the 1:4 residual structure; and the
     GPTQ result's Hessian-weighted error below round-to-nearest.
 """
@@ -192,6 +194,47 @@ def test_salient_is_best_subset_and_invariant():
     assert 7 in qz.select_salient(qz.salient_scores(W2, H), 1)
     # ties go to the lower column
     np.testing.assert_array_equal(qz.select_salient(np.array([1.0, 2.0, 2.0, 2.0]), 2), [1, 2])
+
+
+def test_salient_score_hand_derived_eq3():
+    """Eq. 3, s_j = max_i W_ij^2 diag(H)_j^2, on three hand-made cases whose
+    expected salient column flips under each plausible misreading.  Every
+    value below is derived by hand from the formula, not by the oracle.
+
+    Case A, maximum over rows (not the mean), W squared (a negative entry):
+      H = I (diag 1, 1); column 0 = (-3, 0, 0, 0), column 1 = (2, 2, 2, 2).
+      max_i W^2 d^2:  col 0: 9 * 1 = 9,     col 1: 4 * 1 = 4      -> {0}
+      mean_i W^2 d^2: col 0: 9/4 = 2.25,    col 1: 4              -> {1}
+      max_i W d^2 (no square): col 0: 0,    col 1: 2              -> {1}
+    Case B, diag(H) squared (not to the first power, not left out):
+      diag H = (1, 3); column 0 = (2, 0, 0, 0), column 1 = (1, 0, 0, 0).
+      W^2 d^2: col 0: 4 * 1 = 4,  col 1: 1 * 9 = 9                 -> {1}
+      W^2 d:   col 0: 4,          col 1: 1 * 3 = 3                 -> {0}
+      W^2:     col 0: 4,          col 1: 1                         -> {0}
+    Case C, W squared (not |W|):
+      diag H = (1, 1.5); column 0 = (0, 2, 0, 0), column 1 = (0, 0, -1, 0).
+      W^2 d^2: col 0: 4 * 1 = 4,  col 1: 1 * 2.25 = 2.25           -> {0}
+      |W| d^2: col 0: 2 * 1 = 2,  col 1: 1 * 2.25 = 2.25           -> {1}
+    Off-diagonal entries of H are set large in B and C: a score that read
+    a row or column of H instead of its diagonal changes the picture.
+    """
+    WA = np.array([[-3.0, 2.0], [0.0, 2.0], [0.0, 2.0], [0.0, 2.0]])
+    HA = np.eye(2)
+    WB = np.array([[2.0, 1.0], [0.0, 0.0], [0.0, 0.0], [0.0, 0.0]])
+    HB = np.array([[1.0, 0.9], [0.9, 3.0]])
+    WC = np.array([[0.0, 0.0], [2.0, 0.0], [0.0, -1.0], [0.0, 0.0]])
+    HC = np.array([[1.0, 1.2], [1.2, 1.5]])
+    for W, H, scores, chosen in ((WA, HA, [9.0, 4.0], [0]),
+                                 (WB, HB, [4.0, 9.0], [1]),
+                                 (WC, HC, [4.0, 2.25], [0])):
+        np.testing.assert_array_equal(qz.salient_scores(W, H), scores)
+        np.testing.assert_array_equal(qz.select_salient(qz.salient_scores(W, H), 1), chosen)
+    # the same choice through the whole quantizer (one salient column, one
+    # four-row residual group): case A's column 0, on a positive-definite H
+    out = qz.quantize(WA, HA, 1, lam=1.0, iters=2, group=2)
+    np.testing.assert_array_equal(out["S"], [0])
+    out = qz.quantize(WB, HB, 1, lam=1.0, iters=2, group=2)
+    np.testing.assert_array_equal(out["S"], [1])
 
 
 def test_hessian_explicit_sums():
