@@ -155,7 +155,10 @@ def kernel_name(B, grouped=False, rows_per_panel=1024, e4m3=False, g128=False):
         return f"grouped_mma_kernel<{1 if B <= 8 else 2}, {f8}>"
     if grouped:
         return f"grouped_gemv_kernel<{rows_per_panel // 128}, {f8}, false>"  # 8 waves x 16 rows per row block
-    return f"fk_gemv_kernel<{B}>" if B <= 4 else f"lut_gemv_kernel<{B}, 2>"
+    # one matrix per launch (qtea_gemm_lowbatch): the same kernels in their single-problem form
+    if B > 1:
+        return f"grouped_mma_kernel<{1 if B <= 8 else 2}, {f8}, true>"
+    return f"grouped_gemv_kernel<4, {f8}, {'true' if g128 else 'false'}, true>"
 
 
 def traffic_per_launch(kernel, algorithmic_bytes, workload="llama3_8b_stack batch 1"):

@@ -160,10 +160,10 @@ int qtea_pack_e4m3(const int8_t* trits, int64_t N, int64_t K, const uint16_t* ro
  *   other arguments          as qtea_pack_e4m3
  *   packed                   >= qtea_packed_bytes_g128(...)
  *
- * A matrix in this layout runs through the grouped entry points at batch 1
- * (qtea_grouped_plan / qtea_grouped_gemv); qtea_gemv, qtea_gemm_lowbatch and
- * qtea_workspace_bytes answer QTEA_ERR_INVALID_ARG for it.  qtea_debug_unpack
- * returns its codes as [N][26 ceil(K/128)], group after group.
+ * A matrix in this layout runs at batch 1: through qtea_gemv (or
+ * qtea_gemm_lowbatch with batch 1) and the grouped entry points; a larger
+ * batch answers QTEA_ERR_BATCH.  qtea_debug_unpack returns its codes as
+ * [N][26 ceil(K/128)], group after group.
  */
 int qtea_packed_bytes_g128(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes);
 int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* group_scale,
@@ -173,12 +173,17 @@ int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* gr
 
 /*
  * Workspace bytes that qtea_gemv (batch = 1) / qtea_gemm_lowbatch need for
- * this matrix at this batch size.  The workspace holds per-K-slice partial
- * sums and per-row-block arrival counters.  It must be zero-filled before
- * its first use (qtea_workspace_init or any zero fill); every call that
- * runs to completion leaves the counters at zero again, so one workspace
- * serves any sequence of stream-ordered calls.  Calls that may overlap in
- * time must not share a workspace.
+ * this matrix at this batch size on the current device.  A call splits the
+ * matrix's output panels (512 rows at batch 1, 1024 above) and its K range
+ * into work units over one launch; a panel whose units fall to more than
+ * one workgroup is summed by the last of them to arrive.  The workspace
+ * holds one arrival counter per panel and two slots of partial rows per
+ * workgroup.  It must be zero-filled before its first use
+ * (qtea_workspace_init or any zero fill); every call that runs to
+ * completion leaves the counters at zero again, so one workspace serves any
+ * sequence of stream-ordered calls.  Calls that may overlap in time must
+ * not share a workspace.  Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_BATCH
+ * (batch outside 1..16, or above 1 for the grouped format), QTEA_ERR_HIP.
  */
 int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes);
 
@@ -188,12 +193,18 @@ int qtea_workspace_init(void* workspace, int64_t bytes, void* stream);
 
 /*
  * y = W x for one activation vector (batch 1).
- *   packed      device buffer filled by qtea_pack for *desc
+ *   packed      device buffer filled by qtea_pack, qtea_pack_e4m3 or
+ *               qtea_pack_g128 for *desc
  *   x           device fp16 [K]
  *   y           device fp32 [N]
  *   workspace   device, >= qtea_workspace_bytes(desc, 1), see above
- * fp32 accumulation; results are run-to-run deterministic (fixed reduction
- * order).  Identical to qtea_gemm_lowbatch with batch 1.
+ * One launch, no host work beyond argument checks (graph-capturable).  fp32
+ * accumulation; results are run-to-run deterministic (partial sums are
+ * added in a fixed order).  Identical to qtea_gemm_lowbatch with batch 1.
+ * Errors: QTEA_ERR_INVALID_ARG (null pointer, invalid descriptor, a matrix
+ * whose packed codes or residual values take 2 GiB or more: the kernels
+ * use 32-bit offsets), QTEA_ERR_WORKSPACE (workspace smaller than
+ * qtea_workspace_bytes), QTEA_ERR_HIP (launch failure).
  */
 int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y,
               void* workspace, int64_t workspace_bytes, void* stream);
@@ -202,7 +213,10 @@ int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, floa
  * Y = X W^T for 1 <= batch <= QTEA_MAX_BATCH activation rows (low-batch
  * decode: one token per row).
  *   X  device fp16 [batch][K] row-major;  Y  device fp32 [batch][N] row-major.
- * Errors as qtea_gemv plus QTEA_ERR_BATCH.
+ * Batch 1 runs the table-lookup kernel, batch 2..16 the matrix-core kernel
+ * (fp16 products of the exact ternary codes with the activations split
+ * into two fp16 halves, fp32 accumulation).  Errors as qtea_gemv plus
+ * QTEA_ERR_BATCH.
  */
 int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
                        float* Y, void* workspace, int64_t workspace_bytes, void* stream);

@@ -131,10 +131,15 @@ __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
 // sum is scaled by its row's alpha[r][g] as it is added, and the quarter
 // holding the first half of a group adds beta[r][g] times the group's sum
 // of x.
-template <int RB, bool F8, bool G128 = false>
+//
+// ONE: a single problem launched on its own (GOne): no plan and no queue;
+// workgroup g takes the contiguous run of units [g U / G, (g + 1) U / G), and
+// a panel split between runs is summed by the last of its workgroups to
+// arrive (counters[panel] in the workspace, partial rows in `part`).
+template <int RB, bool F8, bool G128 = false, bool ONE = false>
 __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __restrict__ plan,
                                                            float* __restrict__ part,
-                                                           uint32_t* __restrict__ counters) {
+                                                           uint32_t* __restrict__ counters, const GOne one) {
   using L = GLds<RB>;
   constexpr int RP = L::RP, TPW = L::TPW, GPW = L::GPW, QR = L::QR;
   constexpr int TPP = RP / 64;  // tiles per panel
@@ -145,19 +150,37 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 
   const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
   const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
-  const GChunk* CR = reinterpret_cast<const GChunk*>(plan + H->off_chunks);
-  const int g = blockIdx.x, G = H->n_wg, NC = H->n_chunks;
+  const GChunk* CR = reinterpret_cast<const GChunk*>(plan + (ONE ? 0 : H->off_chunks));
+  auto PR = [&](int m) -> const GProblem& {
+    if constexpr (ONE) return one.pr;
+    else return P[m];
+  };
+  // the unit after c within its problem list (ONE: within the problem)
+  auto adv = [&](Cursor c) -> Cursor {
+    if constexpr (ONE) {
+      if (++c.slice == one.pr.n_slices) {
+        c.slice = 0;
+        ++c.panel;
+      }
+      return c;
+    } else {
+      return advance(c, P);
+    }
+  };
+  const int g = blockIdx.x;
+  const int G = ONE ? int(gridDim.x) : H->n_wg, NC = ONE ? int(gridDim.x) : H->n_chunks;
   // Chunks g and g + G are this workgroup's first two; every later chunk is
   // taken from the queue counters[0] (2G + the count before the increment)
   // at the first unit of a chunk, one chunk ahead of need.  The next chunk's
   // record is loaded at the top of every unit and first used after the
-  // table build's barrier, so a chunk switch does not wait for it.
-  const uint32_t n_grabs = uint32_t(H->n_grabs);
-  if (g >= NC) {
+  // table build's barrier, so a chunk switch does not wait for it.  (ONE:
+  // one run per workgroup, nothing taken.)
+  const uint32_t n_grabs = ONE ? 0u : uint32_t(H->n_grabs);
+  if (!ONE && g >= NC) {
     queue_exit(counters, n_grabs, uint32_t(NC), 0u);
     return;
   }
-  int c = g, cn = g + G;
+  int c = g, cn = ONE ? NC : g + G;
   uint32_t my_chunks = 1;  // chunks this workgroup has started
   int* cnext_lds = flag + 1;  // chunk taken from the queue, published at the unit's last barrier
 
@@ -181,9 +204,18 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     slotreg[d] = r;
   }
 
-  GChunk rec_c = CR[c];
-  int u = rec_c.ub, ue = rec_c.ue;
-  Cursor cur{rec_c.m, rec_c.panel, rec_c.slice};
+  int u, ue;
+  Cursor cur;
+  if constexpr (ONE) {
+    u = int(one_first(g, one.n_units, G));
+    ue = int(one_first(g + 1, one.n_units, G));
+    cur = Cursor{0, u / one.pr.n_slices, u % one.pr.n_slices};
+  } else {
+    const GChunk rec_c = CR[c];
+    u = rec_c.ub;
+    ue = rec_c.ue;
+    cur = Cursor{rec_c.m, rec_c.panel, rec_c.slice};
+  }
 
   // Loads.  Every load is unconditional, from an index clamped into its
   // array (groups past the matrix read a real group whose table entries are
@@ -201,7 +233,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
                 : uint32_t(s * kSliceCols + tid);
   };
   auto load_xv = [&](const Cursor c, uint16_t& xr, uint16_t& vr) {
-    const GProblem& pr = P[c.m];
+    const GProblem& pr = PR(c.m);
     const uint32_t kx = uint32_t(pr.K), kv = uint32_t(pr.n_groups * kGroupCols);
     const uint32_t col = real_col(c.slice), dcol = uint32_t(c.slice * kSliceCols + tid);
     xr = gptr(pr.x)[col < kx ? col : kx - 1];
@@ -211,7 +243,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   constexpr int RF = RB / 4;
   static_assert(RB % 4 == 0, "row blocks in multiples of the quarters");
   auto load_alpha = [&](const Cursor c, uint16_t (&al)[RF]) {
-    const GProblem& pr = P[c.m];
+    const GProblem& pr = PR(c.m);
     const uint32_t np = uint32_t(pr.n_pad);
 #pragma unroll
     for (int i = 0; i < RF; ++i) {
@@ -232,7 +264,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   u32x4 rvq;
   uint32_t ris, ris2 = 0;
   auto load_res = [&](const Cursor c, const int s_lo, const int s_hi) {
-    const GProblem& pr = P[c.m];
+    const GProblem& pr = PR(c.m);
     const bool any = pr.nS > 0;
     const uint32_t nS = uint32_t(pr.nS), n_tiles = uint32_t(pr.n_pad >> 6);
     const uint32_t tile0 = uint32_t(c.panel * TPP + w * TPW);
@@ -255,14 +287,14 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // (lane 0 reads the first bound, the other lanes the second): a scalar load
   // here would be waited for at once, and the salient list is read from HBM
   auto load_spos = [&](const Cursor c) -> int {
-    const GProblem& pr = P[c.m];
+    const GProblem& pr = PR(c.m);
     const int g0 = c.slice * kSliceGroups;
     const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
     return gptr(pr.spos)[lane == 0 ? g0 : g1];
   };
   // byte offset of the 16-byte unit (row block t, group of the quarter) of unit c
   auto w_off = [&](const Cursor c, int t) -> uint32_t {
-    const GProblem& pr = P[c.m];
+    const GProblem& pr = PR(c.m);
     const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
     const int grp = min(c.slice * kSliceGroups + q, ng - 1);
     const int tl = min(c.panel * TPP + wt + (kGW / 4) * t, n_tiles - 1);
@@ -277,12 +309,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   load_xv(cur, xr, vr);
 #pragma unroll
   for (int t = 0; t < RB; ++t) {
-    W[t] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, t)));
+    W[t] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(PR(cur.m).trits) + w_off(cur, t)));
     __builtin_amdgcn_sched_barrier(0);  // the loop's order of the weight loads
   }
   int s_lo_c, s_hi_c;  // salient range of the current unit
   {
-    const GProblem& pr = P[cur.m];
+    const GProblem& pr = PR(cur.m);
     const int g0 = cur.slice * kSliceGroups;
     const int g1 = g0 + kSliceGroups < pr.n_groups ? g0 + kSliceGroups : pr.n_groups;
     s_lo_c = cptr(pr.spos)[g0];
@@ -294,7 +326,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // layout 4: (alpha | beta << 16) of row block t's row in the quarter's group, one unit ahead
   uint32_t AB[G128 ? RB : 1];
   auto ab_at = [&](const Cursor c, int t) -> uint32_t {
-    const GProblem& pr = P[c.m];
+    const GProblem& pr = PR(c.m);
     const int n_sg = pr.n_groups >> 1, n_tiles = int(pr.n_pad >> 6);
     const int sg = min(2 * c.slice + (q >> 1), n_sg - 1);
     const int tl = min(c.panel * TPP + wt + (kGW / 4) * t, n_tiles - 1);
@@ -308,7 +340,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // stage a slice's activations in buffer b: a_j = v_j x_j (exact in fp32) and x_j
   auto stage = [&](const Cursor c, int b) {
     if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
-      const GProblem& pr = P[c.m];
+      const GProblem& pr = PR(c.m);
       const int gcol = int(real_col(c.slice)), dcol = c.slice * kSliceCols + tid;
       const bool xin = gcol < pr.K && (!G128 || tid % 160 < kScaleCols);
       const float xf = xin ? h2f(xr) : 0.0f;
@@ -347,11 +379,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   int ctaken = NC;  // chunk taken at the current chunk's first unit (NC: none)
 
   for (int it = 0;; ++it) {
-    const GProblem& pr = P[cur.m];
+    const GProblem& pr = PR(cur.m);
     const bool chunk_last = u + 1 == ue;
     const bool has_next = !chunk_last || cn < NC;
-    const GChunk rec_cn = CR[min(cn, NC - 1)];
-    const Cursor nxt = !chunk_last ? advance(cur, P) : (has_next ? Cursor{rec_cn.m, rec_cn.panel, rec_cn.slice} : cur);
+    GChunk rec_cn{};
+    if constexpr (!ONE) rec_cn = CR[min(cn, NC - 1)];
+    const Cursor nxt = !chunk_last ? adv(cur) : (has_next ? Cursor{rec_cn.m, rec_cn.panel, rec_cn.slice} : cur);
     const bool pstart = (cur.slice == 0) || chunk_first;
     const bool pend = (cur.slice == pr.n_slices - 1) || chunk_last;
     if (pstart) {
@@ -359,7 +392,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       part_at_chunk_start = chunk_first;
     }
     // at a chunk's first unit, take the chunk after the next one from the queue
-    const bool take = chunk_first && cn < NC;
+    const bool take = !ONE && chunk_first && cn < NC;
     uint32_t taken = 0;
     if (take && tid == 0) taken = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int col0 = cur.slice * kSliceCols;
@@ -420,8 +453,13 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 
     // 2. the next unit's activations and salient range (nxt == cur after the
     // run's last unit: harmless reloads)
-    load_xv(nxt, xr, vr);
-    const int spv = load_spos(nxt);
+    // (ONE: a workgroup's last unit loads nothing more; its last waits are
+    // on the critical path of the launch)
+    int spv = 0;
+    if (!ONE || has_next) {
+      load_xv(nxt, xr, vr);
+      spv = load_spos(nxt);
+    }
 
     // 3. lookups; each 16-byte unit, once read, is refilled with the next
     // unit's bytes (after the run's last unit all lanes read one 16-byte unit)
@@ -430,7 +468,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     // all refills), through a buffer resource over the next matrix's packed
     // bytes (loads past its end would return zeros).  After the run's last
     // unit every lane reads the first 16 bytes of the matrix.
-    const GProblem& pn = P[nxt.m];
+    const GProblem& pn = PR(nxt.m);
     const int n_ng = pn.n_groups, n_nt = int(pn.n_pad >> 6);
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint8_t*>(pn.trits), 0, int(uint32_t(n_nt) * uint32_t(n_ng) * (kTileRows * kGroupPacks)), kBufferWord3);
@@ -478,7 +516,8 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       // (a load issued earlier would need other registers and a copy at the
       // loop edge, and the copy would wait for the load)
       const uint32_t tile_off = (uint32_t(min(n_t0 + (kGW / 4) * t, n_nt - 1)) * uint32_t(n_ng) * (kTileRows * kGroupPacks)) & smask;
-      W[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, int(lane_off), int(tile_off), kAuxNT));
+      if (!ONE || has_next)
+        W[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, int(lane_off), int(tile_off), kAuxNT));
       __builtin_amdgcn_sched_barrier(0);
     }
 
@@ -559,7 +598,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     }
     // the next unit's activations into the other buffer (its last readers,
     // the previous unit's build and residual, are behind the last barrier)
-    stage(nxt, sb ^ 1);
+    if (!ONE || has_next) stage(nxt, sb ^ 1);
     if (take && tid == 0) {
       // a take past the plan's count (a queue counter left over from a call
       // that did not complete) yields no chunk and is reported
@@ -612,6 +651,39 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 #pragma unroll
         for (int i = 0; i < RF; ++i)
           if (row0 + prow[i] < pr.N) y[row0 + prow[i]] = val[i];
+      } else if constexpr (ONE) {
+        // split panel of a single problem: this run's part goes to its slot
+        // (2g, or 2g + 1 for a part starting after the run's first unit) with
+        // device-coherent stores, and the last of the panel's workgroups to
+        // arrive sums the parts in run order
+        // (one row per lane: device-scope stores that write through, which
+        // measured faster here than plain stores and a release at the
+        // arrival, whose write-back of the XCD's L2 dominates so few bytes)
+        float* dst = part + (2 * int64_t(g) + (part_at_chunk_start ? 0 : 1)) * RP;
+#pragma unroll
+        for (int i = 0; i < RF; ++i) store_coherent(dst + prow[i], val[i]);
+        const int64_t ns = one.pr.n_slices, p0 = int64_t(cur.panel) * ns;
+        const int ga = one_owner(p0, one.n_units, G), gb = one_owner(p0 + ns - 1, one.n_units, G);
+        __builtin_amdgcn_s_waitcnt(0);  // the part is complete before its arrival is counted
+        __syncthreads();
+        if (tid == 0) {
+          const uint32_t before = __hip_atomic_fetch_add(counters + cur.panel, 1u, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+          const bool last = before == uint32_t(gb - ga);
+          if (last) __hip_atomic_store(counters + cur.panel, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          flag[2] = last;
+        }
+        __syncthreads();
+        if (flag[2]) {
+          const int odd0 = one_first(ga, one.n_units, G) < p0 ? 1 : 0;
+          // LDS scratch: the table region, free until the next unit's build
+          sum_parts<kGT>(part, RP, ga, gb, odd0, reinterpret_cast<float4*>(lds), [&](int e, float4 v) {
+            if (row0 + e < pr.N) {  // N % 4 == 0: four rows all in or all out
+#pragma unroll
+              for (int i = 0; i < 4; ++i) y[row0 + e + i] = v[i];
+            }
+          });
+        }
       } else {
         // split panel: this chunk's part goes to its partial slot (2c for a
         // part holding the chunk's first unit, 2c + 1 for a part starting
@@ -641,7 +713,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     if (!G128) load_alpha(nxt, al);  // and of its row scales
     cur = nxt;
   }
-  queue_exit(counters, n_grabs, uint32_t(NC), my_chunks);
+  if constexpr (!ONE) queue_exit(counters, n_grabs, uint32_t(NC), my_chunks);
 }
 
 // Sums the parts of every split panel in chunk order (deterministic) and
@@ -698,11 +770,11 @@ int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
   return *n_slices * *n_panels;
 }
 
-template <int RB, bool F8, bool G128 = false>
+template <int RB, bool F8, bool G128 = false, bool ONE = false>
 hipError_t set_lds_attr() {
   static bool done = false;
   if (!done) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB, F8, G128>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_gemv_kernel<RB, F8, G128, ONE>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, GLds<RB>::BYTES);
     if (e != hipSuccess) return e;
     done = true;
@@ -737,11 +809,79 @@ hipError_t launch_grouped(const uint8_t* plan, int grid, int n_splits, float* pa
   const hipError_t e = set_lds_attr<RB, F8, G128>();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((grouped_gemv_kernel<RB, F8, G128>), dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan,
-                     part, counters);
+                     part, counters, GOne{});
   if (n_splits > 0) {
     constexpr int RP = GLds<RB>::RP;
     hipLaunchKernelGGL(grouped_reduce_kernel<RP>, dim3(n_splits), dim3(RP / 4), 0, st, plan, part);
   }
+  return hipGetLastError();
+}
+
+// The problem record of one packed matrix with its activations and outputs.
+void fill_problem(const qtea_desc& d, const void* packed, const uint16_t* x, float* y, int RP, GProblem& pr) {
+  const uint8_t* pk = static_cast<const uint8_t*>(packed);
+  pr = GProblem{};
+  pr.trits = pk + d.off_trits;
+  pr.alpha = reinterpret_cast<const uint16_t*>(pk + d.off_alpha);
+  pr.v = reinterpret_cast<const uint16_t*>(pk + d.off_v);
+  pr.S = reinterpret_cast<const int32_t*>(pk + d.off_salient);
+  pr.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
+  pr.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
+  pr.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
+  Layout lm;  // regions the descriptor does not list
+  make_layout(d.N, d.K, d.n_salient, &lm, int(d.layout));  // succeeds: desc_ok checked it
+  pr.vs = reinterpret_cast<const uint32_t*>(pk + lm.off_vs);
+  pr.x = x;
+  pr.y = y;
+  pr.N = d.N;
+  pr.K = d.K;
+  pr.n_pad = d.n_pad;
+  pr.n_groups = int32_t(d.n_groups);
+  pr.nS = int32_t(d.n_salient);
+  int ns, np;
+  units_for(d, RP, &ns, &np);
+  pr.n_slices = ns;
+  pr.n_panels = np;
+  pr.unit_base = 0;
+}
+
+// The kernels address the packed bytes and the residual with 32-bit offsets.
+bool offsets_fit(const qtea_desc& d) {
+  const int64_t trit_bytes = d.n_pad * d.n_groups * kGroupPacks;
+  const int64_t resid_bytes = (d.n_pad / 4) * d.n_salient * (d.layout == kLayout ? 2 : 1);
+  return trit_bytes < (int64_t(1) << 31) && resid_bytes < (int64_t(1) << 31);
+}
+
+// Launch shape of one matrix on its own (qtea_gemv, qtea_gemm_lowbatch):
+// batch 1 runs the table kernel on 512-row panels, two workgroups per CU at
+// most; batch 2..16 the matrix-core kernel on its 1024-row panels, one per
+// CU.  Every workgroup takes the same number of units (the least that fits
+// the grid), so no workgroup carries more than the others.  The workspace
+// holds one arrival counter per panel, then two partial-row slots per
+// workgroup.
+constexpr int kOneRB = 4;
+struct OneShape {
+  int rp, n_panels, n_slices, grid;
+  int64_t n_units, off_part, ws_bytes;
+};
+bool one_shape(const qtea_desc& d, int batch, OneShape* o) {
+  const int max_wg = batch == 1 ? grid_size() : cu_count();
+  if (max_wg < 1) return false;
+  o->rp = batch == 1 ? GLds<kOneRB>::RP : grouped_mma_rows_per_panel();
+  o->n_units = units_for(d, o->rp, &o->n_slices, &o->n_panels);
+  const int64_t per = cdiv(o->n_units, max_wg);
+  o->grid = int(cdiv(o->n_units, per));
+  o->off_part = align_up(4 * int64_t(o->n_panels), kAlign);
+  o->ws_bytes = o->off_part + 2 * int64_t(o->grid) * o->rp * batch * 4;
+  return true;
+}
+
+template <bool F8, bool G128>
+hipError_t launch_one_b1(const GOne& one, int grid, float* part, uint32_t* counters, hipStream_t st) {
+  const hipError_t e = set_lds_attr<kOneRB, F8, G128, true>();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((grouped_gemv_kernel<kOneRB, F8, G128, true>), dim3(grid), dim3(kGT), GLds<kOneRB>::BYTES, st,
+                     nullptr, part, counters, one);
   return hipGetLastError();
 }
 
@@ -780,10 +920,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   for (int m = 0; m < n_problems; ++m) {
     if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
     if (descs[m].layout != layout) return QTEA_ERR_INVALID_ARG;  // one residual format per plan
-    // the kernel addresses the packed bytes and the residual with 32-bit offsets
-    const int64_t trit_bytes = descs[m].n_pad * descs[m].n_groups * kGroupPacks;
-    const int64_t resid_bytes = (descs[m].n_pad / 4) * descs[m].n_salient * (layout == kLayout ? 2 : 1);
-    if (trit_bytes >= (int64_t(1) << 31) || resid_bytes >= (int64_t(1) << 31)) return QTEA_ERR_INVALID_ARG;
+    if (!offsets_fit(descs[m])) return QTEA_ERR_INVALID_ARG;
   }
 
   // rows per panel: the largest that still gives every workgroup several units
@@ -825,31 +962,10 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   for (int m = 0; m < n_problems; ++m) {
     const int src = order[size_t(m)];
     const qtea_desc& d = descs[src];
-    const uint8_t* pk = static_cast<const uint8_t*>(packed[src]);
-    GProblem& pr = P[m];
-    pr.trits = pk + d.off_trits;
-    pr.alpha = reinterpret_cast<const uint16_t*>(pk + d.off_alpha);
-    pr.v = reinterpret_cast<const uint16_t*>(pk + d.off_v);
-    pr.S = reinterpret_cast<const int32_t*>(pk + d.off_salient);
-    pr.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
-    pr.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
-    pr.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
-    {
-      Layout lm;  // regions the descriptor does not list
-      make_layout(d.N, d.K, d.n_salient, &lm, int(d.layout));  // succeeds: desc_ok checked it
-      pr.vs = reinterpret_cast<const uint32_t*>(pk + lm.off_vs);
-    }
-    pr.x = x[src];
-    pr.y = y[src];
-    pr.N = d.N;
-    pr.K = d.K;
-    pr.n_pad = d.n_pad;
-    pr.n_groups = int32_t(d.n_groups);
-    pr.nS = int32_t(d.n_salient);
     int ns, np;
     units_for(d, RP, &ns, &np);
-    pr.n_slices = ns;
-    pr.n_panels = np;
+    GProblem& pr = P[m];
+    fill_problem(d, packed[src], x[src], y[src], RP, pr);
     pr.unit_base = total_units;
     for (int p = 0; p < np; ++p) {
       const int64_t rows = std::min<int64_t>(RP, d.n_pad - int64_t(p) * RP);
@@ -977,6 +1093,50 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   info->plan_bytes = need;
   info->workspace_bytes = kAlign + 2 * n_chunks * RP * int64_t(batch) * 4;
   return QTEA_OK;
+}
+
+int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes) {
+  if (!out_bytes || !desc_ok(desc)) return QTEA_ERR_INVALID_ARG;
+  if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
+  if (desc->layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;  // the grouped format runs at batch 1
+  OneShape o;
+  if (!one_shape(*desc, batch, &o)) return QTEA_ERR_HIP;
+  *out_bytes = o.ws_bytes;
+  return QTEA_OK;
+}
+
+int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
+                       float* Y, void* workspace, int64_t workspace_bytes, void* stream) {
+  if (!desc_ok(desc) || !packed || !X || !Y || !offsets_fit(*desc)) return QTEA_ERR_INVALID_ARG;
+  if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
+  const qtea_desc& d = *desc;
+  const bool f8 = d.layout != kLayout, g128 = d.layout == kLayoutG128;
+  if (g128 && batch != 1) return QTEA_ERR_BATCH;
+  OneShape o;
+  if (!one_shape(d, batch, &o)) return QTEA_ERR_HIP;
+  if (!workspace || workspace_bytes < o.ws_bytes) return QTEA_ERR_WORKSPACE;
+  GOne one{};
+  fill_problem(d, packed, X, Y, o.rp, one.pr);
+  one.n_units = int32_t(o.n_units);
+  one.batch = batch;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
+  float* part = reinterpret_cast<float*>(ws + o.off_part);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (batch > 1)
+    e = launch_one_mma(one, o.grid, f8, part, counters, st);
+  else if (g128)
+    e = launch_one_b1<true, true>(one, o.grid, part, counters, st);
+  else
+    e = f8 ? launch_one_b1<true, false>(one, o.grid, part, counters, st)
+           : launch_one_b1<false, false>(one, o.grid, part, counters, st);
+  return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+}
+
+int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y, void* workspace,
+              int64_t workspace_bytes, void* stream) {
+  return qtea_gemm_lowbatch(desc, packed, x, 1, y, workspace, workspace_bytes, stream);
 }
 
 int qtea_grouped_status(const void* workspace, uint32_t* flags, void* stream) {

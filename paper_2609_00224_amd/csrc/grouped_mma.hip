@@ -149,9 +149,13 @@ __device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
 }
 
 // F8: residual values are E4M3 bytes (layout 3), else fp16 (layout 2).
-template <int NB, bool F8>
+// ONE: a single problem launched on its own (GOne, no plan): workgroup g
+// takes the units [g U / G, (g + 1) U / G), and a panel split between runs
+// is summed by the last of its workgroups to arrive (counters[panel]).
+template <int NB, bool F8, bool ONE = false>
 __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
-                                                          float* __restrict__ part) {
+                                                          float* __restrict__ part,
+                                                          uint32_t* __restrict__ counters, const GOne one) {
   using L = MLds<NB>;
   constexpr int BP = 8 * NB;  // batch rows per hi (or lo) column set
   extern __shared__ float smem[];
@@ -160,11 +164,26 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 
   const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
   const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
-  const GChunk* CR = reinterpret_cast<const GChunk*>(plan + H->off_chunks);
-  const int g = blockIdx.x, NC = H->n_chunks, B = H->batch;
-  if (g >= NC) return;
-  const GChunk rc = CR[g];
-  const int ub = rc.ub, ue = rc.ue;
+  auto PR = [&](int m) -> const GProblem& {
+    if constexpr (ONE) return one.pr;
+    else return P[m];
+  };
+  const int g = blockIdx.x, G = int(gridDim.x);
+  const int B = ONE ? one.batch : H->batch;
+  int ub, ue;
+  Cursor cur;
+  if constexpr (ONE) {
+    ub = int(one_first(g, one.n_units, G));
+    ue = int(one_first(g + 1, one.n_units, G));
+    cur = Cursor{0, ub / one.pr.n_slices, ub % one.pr.n_slices};
+  } else {
+    const GChunk* CR = reinterpret_cast<const GChunk*>(plan + H->off_chunks);
+    if (g >= H->n_chunks) return;
+    const GChunk rc = CR[g];
+    ub = rc.ub;
+    ue = rc.ue;
+    cur = Cursor{rc.m, rc.panel, rc.slice};
+  }
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -172,18 +191,31 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   const int rs = jr & 3;                     // byte rotation left after the tile's 4q
 
   // decode tables, copy = the lane's index in its half-wave: digits 0-3 of
-  // code c as fp16 at c * 256 + 8 copy, digit 4 in the T4 table
-  for (int e = tid; e < kCodes * 32; e += kMT) {
-    const int c = e >> 5, cp = e & 31;
-    int d0 = c % 3, r1 = c / 3, d1 = r1 % 3, r2 = r1 / 3, d2 = r2 % 3, r3 = r2 / 3, d3 = r3 % 3, d4 = r3 / 3;
-    _Float16 t[4] = {(_Float16)(d0 - 1), (_Float16)(d1 - 1), (_Float16)(d2 - 1), (_Float16)(d3 - 1)};
-    u32x2 m;
-    __builtin_memcpy(&m, t, 8);
-    *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = m;
-    const _Float16 t4[2] = {(_Float16)(d4 - 1), (_Float16)0};
-    uint32_t m4;
-    __builtin_memcpy(&m4, t4, 4);
-    *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = m4;
+  // code c as fp16 at c * 256 + 8 copy, digit 4 in the T4 table.  One copy
+  // of each code is computed (in the first image buffer, free until the
+  // first images are built), then every copy is written from it.
+  {
+    uint32_t* one_copy = reinterpret_cast<uint32_t*>(lds + L::IMG);  // [243][3] words
+    if (tid < kCodes) {
+      const int c = tid;
+      const int d0 = c % 3, r1 = c / 3, d1 = r1 % 3, r2 = r1 / 3, d2 = r2 % 3, r3 = r2 / 3, d3 = r3 % 3, d4 = r3 / 3;
+      _Float16 t[4] = {(_Float16)(d0 - 1), (_Float16)(d1 - 1), (_Float16)(d2 - 1), (_Float16)(d3 - 1)};
+      u32x2 m;
+      __builtin_memcpy(&m, t, 8);
+      const _Float16 t4[2] = {(_Float16)(d4 - 1), (_Float16)0};
+      uint32_t m4;
+      __builtin_memcpy(&m4, t4, 4);
+      one_copy[3 * c] = m.x;
+      one_copy[3 * c + 1] = m.y;
+      one_copy[3 * c + 2] = m4;
+    }
+    __syncthreads();
+    for (int e = tid; e < kCodes * 32; e += kMT) {
+      const int c = e >> 5, cp = e & 31;
+      *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = u32x2{one_copy[3 * c], one_copy[3 * c + 1]};
+      *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = one_copy[3 * c + 2];
+    }
+    __syncthreads();  // the first images overwrite the computed copy
   }
   if (tid < 3) bigf[tid] = 0;
   __syncthreads();  // flags cleared before the first images can set one
@@ -192,7 +224,6 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   const uint32_t lane_base = uint32_t(8 * (lane & 31));
   const uint32_t sel_rot = 0x07060504u - 0x01010101u * uint32_t(rs);
 
-  Cursor cur{rc.m, rc.panel, rc.slice};
 
   // x and v of the image this thread builds: pairs p = tid + kMT i of (batch
   // row b = p / 320, slice column c = p % 320); their image byte offsets (hi
@@ -219,7 +250,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   uint16_t xr[NPAIR];
   uint32_t vr[NPAIR];
   auto load_xv = [&](const Cursor cc) {
-    const GProblem& pr = P[cc.m];
+    const GProblem& pr = PR(cc.m);
     const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(pr.x), 0, int(2 * uint32_t(B) * uint32_t(pr.K)), kBufferWord3);
     const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
@@ -262,7 +293,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   // weight bytes of unit cc, MFMA row tile q: row 16 (jr >> 2) + 4q + (jr & 3)
   // of the wave's 64-row tile, group kb of the slice
   auto w_off = [&](const Cursor cc, int q) -> uint32_t {
-    const GProblem& pr = P[cc.m];
+    const GProblem& pr = PR(cc.m);
     const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
     const int grp = min(cc.slice * kSliceGroups + kb, ng - 1);
     const int tl = min(cc.panel * (kMRP / 64) + w, n_tiles - 1);
@@ -273,7 +304,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   u32x4 W[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q)
-    W[q] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(P[cur.m].trits) + w_off(cur, q)));
+    W[q] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(PR(cur.m).trits) + w_off(cur, q)));
   load_xv(cur);
   const bool big0 = build(0, 1.0f, 0);  // the run's first unit starts a part
   if (big0) bigf[0] = 1;
@@ -288,9 +319,19 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   bool part_first = true;  // the open panel part began at the run's first unit
 
   for (int it = 0, u = ub; u < ue; ++it, ++u) {
-    const GProblem& pr = P[cur.m];
+    const GProblem& pr = PR(cur.m);
     const bool has_next = u + 1 < ue;
-    const Cursor nxt = has_next ? advance(cur, P) : cur;
+    Cursor nxt = cur;
+    if (has_next) {
+      if constexpr (ONE) {
+        if (++nxt.slice == one.pr.n_slices) {
+          nxt.slice = 0;
+          ++nxt.panel;
+        }
+      } else {
+        nxt = advance(cur, P);
+      }
+    }
     const bool pstart = (cur.slice == 0) || (u == ub);
     const bool pend = (cur.slice == pr.n_slices - 1) || !has_next;
     if (pstart) {
@@ -314,7 +355,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     load_xv(nxt);
 
     // next unit's weight bytes through a buffer resource over its matrix
-    const GProblem& pn = P[nxt.m];
+    const GProblem& pn = PR(nxt.m);
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint8_t*>(pn.trits), 0,
         int(uint32_t(pn.n_pad >> 6) * uint32_t(pn.n_groups) * (kTileRows * kGroupPacks)), kBufferWord3);
@@ -506,6 +547,43 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) C[q][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       }
+      if constexpr (ONE) {
+        if (!owned) {
+          // the last of the panel's workgroups to arrive sums its parts in
+          // run order (slot 2k for a part at its run's first unit, 2k + 1
+          // for one starting later: only the first run's part can)
+          const int64_t ns = pr.n_slices, p0 = int64_t(cur.panel) * ns;
+          const int ga = one_owner(p0, one.n_units, G), gb = one_owner(p0 + ns - 1, one.n_units, G);
+          // every wave's stores have reached the cache before the arrival;
+          // the arrival's release then writes them back for the other XCDs
+          // (measured faster here than device-scope stores, which write
+          // through one partly filled line at a time)
+          __builtin_amdgcn_s_waitcnt(0);
+          __syncthreads();
+          if (tid == 0) {
+            const uint32_t before = __hip_atomic_fetch_add(counters + cur.panel, 1u, __ATOMIC_RELEASE,
+                                                           __HIP_MEMORY_SCOPE_AGENT);
+            const bool last = before == uint32_t(gb - ga);
+            if (last) __hip_atomic_store(counters + cur.panel, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            bigf[3] = last;
+            if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other parts, visible to this XCD
+          }
+          __syncthreads();
+          if (bigf[3]) {
+            const int odd0 = one_first(ga, one.n_units, G) < p0 ? 1 : 0;
+            const int64_t prow0 = int64_t(cur.panel) * kMRP;
+            // LDS scratch: the B-operand images, free until the next unit's build
+            sum_parts<kMT>(part, int64_t(kMRP) * B, ga, gb, odd0, reinterpret_cast<float4*>(lds + L::IMG),
+                           [&](int e, float4 v) {
+                             const int b = e / kMRP, r = e - b * kMRP;
+                             if (prow0 + r < pr.N) {  // N % 4 == 0
+#pragma unroll
+                               for (int i = 0; i < 4; ++i) pr.y[int64_t(b) * pr.N + prow0 + r + i] = v[i];
+                             }
+                           });
+          }
+        }
+      }
     }
     // the next unit's images into the other buffer, after the part end's
     // reads of the gather array (a next unit after a part end starts a new
@@ -522,16 +600,17 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   }
 }
 
-template <int NB, bool F8>
-hipError_t launch(const uint8_t* plan, int grid, float* part, hipStream_t st) {
+template <int NB, bool F8, bool ONE>
+hipError_t launch(const uint8_t* plan, int grid, float* part, uint32_t* counters, const GOne& one, hipStream_t st) {
   static bool done = false;
   if (!done) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_mma_kernel<NB, F8>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&grouped_mma_kernel<NB, F8, ONE>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, MLds<NB>::BYTES);
     if (e != hipSuccess) return e;
     done = true;
   }
-  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8>), dim3(grid), dim3(kMT), MLds<NB>::BYTES, st, plan, part);
+  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8, ONE>), dim3(grid), dim3(kMT), MLds<NB>::BYTES, st, plan, part,
+                     counters, one);
   return hipGetLastError();
 }
 
@@ -540,8 +619,18 @@ hipError_t launch(const uint8_t* plan, int grid, float* part, hipStream_t st) {
 int grouped_mma_rows_per_panel() { return kMRP; }
 
 hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8, float* part, hipStream_t st) {
-  if (f8) return batch <= 8 ? launch<1, true>(plan, grid, part, st) : launch<2, true>(plan, grid, part, st);
-  return batch <= 8 ? launch<1, false>(plan, grid, part, st) : launch<2, false>(plan, grid, part, st);
+  const GOne none{};
+  if (f8) return batch <= 8 ? launch<1, true, false>(plan, grid, part, nullptr, none, st)
+                            : launch<2, true, false>(plan, grid, part, nullptr, none, st);
+  return batch <= 8 ? launch<1, false, false>(plan, grid, part, nullptr, none, st)
+                    : launch<2, false, false>(plan, grid, part, nullptr, none, st);
+}
+
+hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint32_t* counters, hipStream_t st) {
+  if (f8) return one.batch <= 8 ? launch<1, true, true>(nullptr, grid, part, counters, one, st)
+                                : launch<2, true, true>(nullptr, grid, part, counters, one, st);
+  return one.batch <= 8 ? launch<1, false, true>(nullptr, grid, part, counters, one, st)
+                        : launch<2, false, true>(nullptr, grid, part, counters, one, st);
 }
 
 }  // namespace qtea_grouped

@@ -105,25 +105,44 @@ def test_g128_synth_8b_shapes():
         assert_precise(y[:, rows], ref, f"g128 {N}x{c['K']}")
 
 
-def test_g128_entry_points_that_refuse_it():
+def test_g128_per_matrix_gemv_dyadic_exact():
+    """qtea_gemv takes the grouped format at batch 1 (the table kernel on one
+    problem); bit-exact on dyadic inputs, twice on one workspace."""
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    for i, (N, K, nS) in enumerate(SHAPES):
+        c = g128_dyadic_case(60 + i, N, K, 1, nS)
+        _report(f"per-matrix gemv, grouped format, dyadic {N}x{K} nS={nS}")
+        pm = gpu_pack_g128(c)
+        x = to_dev(c["x"])
+        ws = q.new_workspace(pm.desc, 1)
+        ref, _ = oracle_rows_g128(c, need_wmax=False)
+        for _ in range(2):
+            y = torch.full((1, N), float("nan"), dtype=torch.float32, device="cuda")
+            q.qtea_gemv(pm.desc, pm.packed, x, y, ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(y.cpu().numpy().astype(np.float64), ref), (N, K)
+
+
+def test_g128_batch_above_one_refused():
     import torch
 
     import paper_2609_00224_amd as q
 
     c = g128_dyadic_case(1, 256, 500, 1, 10)
     pm = gpu_pack_g128(c)
-    x = to_dev(c["x"])
-    y = torch.empty((1, 256), dtype=torch.float32, device="cuda")
-    _report("refusals: per-matrix GEMV, workspace size, batch 2")
+    _report("refusals: batch 2 in the grouped format")
     with pytest.raises(q.QteaError) as e:
-        q.qtea_workspace_bytes(pm.desc, 1)
-    assert e.value.status == q.QTEA_ERR_INVALID_ARG
-    ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
-    with pytest.raises(q.QteaError) as e:
-        q.qtea_gemv(pm.desc, pm.packed, x, y, ws)
-    assert e.value.status == q.QTEA_ERR_INVALID_ARG
+        q.qtea_workspace_bytes(pm.desc, 2)
+    assert e.value.status == q.QTEA_ERR_BATCH
+    ws = torch.zeros(1 << 22, dtype=torch.uint8, device="cuda")
     x2 = to_dev(np.concatenate([c["x"], c["x"]]))
     y2 = torch.empty((2, 256), dtype=torch.float32, device="cuda")
+    with pytest.raises(q.QteaError) as e:
+        q.qtea_gemm_lowbatch(pm.desc, pm.packed, x2, 2, y2, ws)
+    assert e.value.status == q.QTEA_ERR_BATCH
     with pytest.raises(q.QteaError) as e:
         q.plan_grouped([pm], [x2], [y2], batch=2)
     assert e.value.status == q.QTEA_ERR_BATCH
