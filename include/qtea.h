@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define QTEA_ABI_VERSION 8
+#define QTEA_ABI_VERSION 9
 #define QTEA_MAX_BATCH 16
 
 enum qtea_status {
@@ -220,6 +220,25 @@ int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, floa
  */
 int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
                        float* Y, void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation as qtea_gemm_lowbatch, through the same kernels, without a
+ * workspace argument.  The library keeps its own fixed workspace of
+ * QTEA_NOALLOC_SCRATCH_BYTES per GPU, a device array held until the process
+ * ends; this call allocates nothing (no hipMalloc, no hipFree).  Its first
+ * call on a device enqueues a zero fill of the array's counter words on
+ * `stream`; every call that completes leaves them at zero.  Every call on
+ * one GPU uses that GPU's array: calls that may overlap in time on one GPU
+ * (other streams, other host threads) race and must not be made.
+ * Errors as qtea_gemm_lowbatch, with QTEA_ERR_WORKSPACE for a call whose
+ * workspace (qtea_workspace_bytes) would not fit the array: batch 1 always
+ * fits a 256-CU device; larger batches fit when the matrix's panels do.
+ */
+#define QTEA_NOALLOC_SCRATCH_BYTES (16 * 1048576 + 65536)
+int qtea_gemm_lowbatch_noalloc(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,
+                               float* Y, void* stream);
 
 /*
  * Measurement support: stream `bytes` (a multiple of 16) of a device buffer

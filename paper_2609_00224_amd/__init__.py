@@ -33,7 +33,7 @@ QTEA_ERR_HIP = -6
 QTEA_ERR_NOT_POSITIVE = -7
 QTEA_QUANT_GROUP = 128
 QTEA_MAX_BATCH = 16
-QTEA_ABI_VERSION = 8  # the header this binding mirrors
+QTEA_ABI_VERSION = 9  # the header this binding mirrors
 QTEA_DESC_MAGIC = 0x51544541
 
 # Every function the header declares (checked by tests/test_abi.py).
@@ -41,7 +41,7 @@ EXPORTS = (
     "qtea_status_string", "qtea_abi_version", "qtea_packed_bytes", "qtea_pack",
     "qtea_workspace_bytes", "qtea_workspace_init", "qtea_gemv", "qtea_gemm_lowbatch",
     "qtea_debug_unpack", "qtea_grouped_plan_bytes", "qtea_grouped_plan", "qtea_grouped_gemv",
-    "qtea_grouped_status",
+    "qtea_grouped_status", "qtea_gemm_lowbatch_noalloc",
     "qtea_packed_bytes_e4m3", "qtea_pack_e4m3", "qtea_packed_bytes_g128", "qtea_pack_g128",
     "qtea_read_ceiling", "qtea_quant_hessian", "qtea_quant_workspace_bytes", "qtea_quantize",
 )
@@ -139,6 +139,8 @@ def load(path: str = LIB_PATH):
                                       i32, i32, vp, i64, pinfo, vp]
     lib.qtea_grouped_gemv.restype = i32
     lib.qtea_grouped_gemv.argtypes = [pinfo, vp, vp, i64, vp]
+    lib.qtea_gemm_lowbatch_noalloc.restype = i32
+    lib.qtea_gemm_lowbatch_noalloc.argtypes = [pdesc, vp, vp, i32, vp, vp]
     lib.qtea_grouped_status.restype = i32
     lib.qtea_grouped_status.argtypes = [vp, ctypes.POINTER(ctypes.c_uint32), vp]
     lib.qtea_quant_hessian.restype = i32
@@ -362,6 +364,17 @@ def qtea_grouped_gemv(info: QteaGroupedInfo, plan, workspace, stream=None):
     _check(load().qtea_grouped_gemv(ctypes.byref(info), _ptr(plan), _ptr(workspace),
                                     workspace.numel() * workspace.element_size(), _stream(stream)),
            "qtea_grouped_gemv")
+
+
+QTEA_NOALLOC_SCRATCH_BYTES = 16 * 1048576 + 65536
+
+
+def qtea_gemm_lowbatch_noalloc(desc: QteaDesc, packed, X, batch: int, Y, stream=None):
+    """qtea_gemm_lowbatch with the library's own fixed device workspace (no
+    allocation; calls that overlap on one GPU race)."""
+    _need_cuda(packed, X, Y)
+    _check(load().qtea_gemm_lowbatch_noalloc(ctypes.byref(desc), _ptr(packed), _ptr(X), int(batch), _ptr(Y),
+                                             _stream(stream)), "qtea_gemm_lowbatch_noalloc")
 
 
 QTEA_QUEUE_STALE = 1  # a chunk-queue take found the counter past the plan's count

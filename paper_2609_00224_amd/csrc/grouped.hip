@@ -37,6 +37,7 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "grouped_plan.h"
@@ -885,6 +886,58 @@ hipError_t launch_one_b1(const GOne& one, int grid, float* part, uint32_t* count
   return hipGetLastError();
 }
 
+// One matrix on its own (arguments checked by the caller): the panels'
+// arrival counters at `counters` (zero on entry, left at zero), the partial
+// rows of split panels at `part` (2 grid slots of rp x batch floats).
+int one_launch(const qtea_desc& d, const void* packed, const uint16_t* X, int batch, float* Y, const OneShape& o,
+               uint32_t* counters, float* part, hipStream_t st) {
+  const bool f8 = d.layout != kLayout, g128 = d.layout == kLayoutG128;
+  GOne one{};
+  fill_problem(d, packed, X, Y, o.rp, one.pr);
+  one.n_units = int32_t(o.n_units);
+  one.batch = batch;
+  hipError_t e;
+  if (batch > 1)
+    e = launch_one_mma(one, o.grid, f8, part, counters, st);
+  else if (g128)
+    e = launch_one_b1<true, true>(one, o.grid, part, counters, st);
+  else
+    e = f8 ? launch_one_b1<true, false>(one, o.grid, part, counters, st)
+           : launch_one_b1<false, false>(one, o.grid, part, counters, st);
+  return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+}
+
+// The allocation-free variant's workspace: a file-scope device array, one
+// copy per GPU, held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in for the
+// symbol): the device address comes from hipGetSymbolAddress, once per
+// device with that device current, and is kept per device.  Layout: the
+// panels' arrival counters in the first kNoallocCounterBytes (zero-filled
+// once, at the first call on the device, and left at zero by every call that
+// completes), then the partial rows.
+constexpr int64_t kNoallocCounterBytes = 65536;
+static __device__ __align__(256) uint8_t scratch[QTEA_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_on_current_device(void** out, hipStream_t st) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return QTEA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return QTEA_ERR_HIP;
+    // a fill kernel (not a memset node) on the caller's stream, ordered
+    // before this call's kernels
+    const int rc = qtea_workspace_init(p, kNoallocCounterBytes, st);
+    if (rc != QTEA_OK) return rc;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return QTEA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1109,34 +1162,37 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
                        float* Y, void* workspace, int64_t workspace_bytes, void* stream) {
   if (!desc_ok(desc) || !packed || !X || !Y || !offsets_fit(*desc)) return QTEA_ERR_INVALID_ARG;
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
-  const qtea_desc& d = *desc;
-  const bool f8 = d.layout != kLayout, g128 = d.layout == kLayoutG128;
-  if (g128 && batch != 1) return QTEA_ERR_BATCH;
+  if (desc->layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;
   OneShape o;
-  if (!one_shape(d, batch, &o)) return QTEA_ERR_HIP;
+  if (!one_shape(*desc, batch, &o)) return QTEA_ERR_HIP;
   if (!workspace || workspace_bytes < o.ws_bytes) return QTEA_ERR_WORKSPACE;
-  GOne one{};
-  fill_problem(d, packed, X, Y, o.rp, one.pr);
-  one.n_units = int32_t(o.n_units);
-  one.batch = batch;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
-  float* part = reinterpret_cast<float*>(ws + o.off_part);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e;
-  if (batch > 1)
-    e = launch_one_mma(one, o.grid, f8, part, counters, st);
-  else if (g128)
-    e = launch_one_b1<true, true>(one, o.grid, part, counters, st);
-  else
-    e = f8 ? launch_one_b1<true, false>(one, o.grid, part, counters, st)
-           : launch_one_b1<false, false>(one, o.grid, part, counters, st);
-  return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
+  return one_launch(*desc, packed, X, batch, Y, o, reinterpret_cast<uint32_t*>(ws),
+                    reinterpret_cast<float*>(ws + o.off_part), static_cast<hipStream_t>(stream));
 }
 
 int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y, void* workspace,
               int64_t workspace_bytes, void* stream) {
   return qtea_gemm_lowbatch(desc, packed, x, 1, y, workspace, workspace_bytes, stream);
+}
+
+int qtea_gemm_lowbatch_noalloc(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch, float* Y,
+                               void* stream) {
+  if (!desc_ok(desc) || !packed || !X || !Y || !offsets_fit(*desc)) return QTEA_ERR_INVALID_ARG;
+  if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
+  if (desc->layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;
+  OneShape o;
+  if (!one_shape(*desc, batch, &o)) return QTEA_ERR_HIP;
+  const int64_t part_bytes = o.ws_bytes - o.off_part;
+  if (4 * int64_t(o.n_panels) > kNoallocCounterBytes || part_bytes > QTEA_NOALLOC_SCRATCH_BYTES - kNoallocCounterBytes)
+    return QTEA_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* p = nullptr;
+  const int rc = scratch_on_current_device(&p, st);
+  if (rc != QTEA_OK) return rc;
+  uint8_t* ws = static_cast<uint8_t*>(p);
+  return one_launch(*desc, packed, X, batch, Y, o, reinterpret_cast<uint32_t*>(ws),
+                    reinterpret_cast<float*>(ws + kNoallocCounterBytes), st);
 }
 
 int qtea_grouped_status(const void* workspace, uint32_t* flags, void* stream) {
