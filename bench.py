@@ -167,9 +167,8 @@ def traffic_per_launch(kernel, algorithmic_bytes, workload="llama3_8b_stack batc
     (sha256 recorded in the summary)."""
     import hashlib
 
-    name = "grouped_gemv" if kernel.startswith("grouped") else "fk_gemv"
-    path = os.path.join(ROOT, "profiles", f"traffic_{name}_b1_llama3_8b_stack.txt")
-    srcs = ["grouped.hip" if kernel.startswith("grouped") else "qtea.hip", "qtea_internal.h"]
+    path = os.path.join(ROOT, "profiles", "traffic_grouped_gemv_b1_llama3_8b_stack.txt")
+    srcs = ["grouped.hip", "grouped_plan.h", "qtea_internal.h"]
     if not os.path.exists(path):
         return None
     kv = {}
@@ -178,7 +177,7 @@ def traffic_per_launch(kernel, algorithmic_bytes, workload="llama3_8b_stack batc
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     h = hashlib.sha256()
-    for f in srcs:  # the kernel's source file, then the shared header
+    for f in srcs:  # the kernel's source file, then the shared headers
         h.update(open(os.path.join(ROOT, "paper_2609_00224_amd", "csrc", f), "rb").read())
     digest = h.hexdigest()
     if kv.get("kernel") != kernel or kv.get("source_sha256") != digest or kv.get("workload") != workload:
@@ -551,6 +550,10 @@ def main():
     ap.add_argument("--cold-copies", type=int, default=0,
                     help="time the workload warm (one copy replayed) and cold (rotating through this many "
                          "copies, each with its own weights, far beyond the 256 MB last-level cache)")
+    ap.add_argument("--chained-batches", type=lambda v: [int(b) for b in v.split(",") if b], default=[4, 16],
+                    help="further batch sizes timed through the chained per-GEMV launches (comma list)")
+    ap.add_argument("--residual-off", action="store_true",
+                    help="the ternary-only stack: same shapes and seeds, no salient columns (residual cost)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="after the bench, copy this many bytes device-to-device 3 times "
                          "(known-size reference for HBM counters)")
@@ -567,6 +570,9 @@ def main():
         cold_main(args)
         return
 
+    import dataclasses
+    from fractions import Fraction
+
     import torch
 
     import paper_2609_00224_amd as q
@@ -577,27 +583,32 @@ def main():
     assert torch.cuda.is_available(), "no GPU"
     dev = torch.device("cuda:0")
     wl = WORKLOADS[args.workload]
+    if args.residual_off:  # the ternary-only stack: same shapes and seeds, no salient columns
+        wl = dataclasses.replace(wl, name=wl.name + "_ternary_only", frac=Fraction(0))
     B = args.batch
     seed = synth.DEFAULT_SEED if args.seed is None else args.seed
-    mats = build_stack(wl, B, dev, seed, args.layers)
+    # chained timing at further batch sizes from the same stack (activation rows sliced)
+    extra_b = [b for b in args.chained_batches if b != B] if not (args.grouped_only or wl.groups) else []
+    Bmax = max([B] + extra_b)
+    mats = build_stack(wl, Bmax, dev, seed, args.layers)
+    full_x = [m["x"] for m in mats]
+    full_y = [m["y"] for m in mats]
+    for m in mats:
+        m["x"], m["y"] = m["x"][:B], m["y"][:B]
     n_layers = len({m["layer"] for m in mats})
-    ws_bytes = 4 if wl.groups else max(q.qtea_workspace_bytes(m["pm"].desc, B) for m in mats)
+    ws_bytes = max(q.qtea_workspace_bytes(m["pm"].desc, b) for m in mats for b in [B] + extra_b)
     ws = torch.zeros(max(ws_bytes, 4), dtype=torch.uint8, device=dev)
     stream = torch.cuda.Stream(device=dev)
-
     token_bytes = sum(m["bytes"] for m in mats)
-    ms_chain = float("nan")
-    if wl.groups and not args.grouped_only:
-        log("the grouped format runs through the grouped entry points only: timing the grouped execution")
-        args.grouped_only = True
-    if not args.grouped_only:
-        g = capture(mats, B, ws, stream)
-        ms_chain = time_graph(g, stream, args.steps, args.warmup)
-        del g
-    gbs_chain = token_bytes / (ms_chain * 1e-3) / 1e9
-    log(f"{wl.name} B={B} chained: {ms_chain * 1e3:.1f} us/token, {gbs_chain:.1f} GB/s "
-        f"({gbs_chain / HBM_PEAK_GBS:.1%} of peak)")
 
+    # 1. The measured streaming-read ceiling, the reference the path's rate is
+    # compared with (a plain read of 2 GiB, held under load).
+    clock_before = gpu_clock()
+    ceiling, ceiling_mean = read_ceiling(dev, stream)
+    log(f"streaming-read ceiling {ceiling:.1f} GB/s (mean of passes {ceiling_mean:.1f}), shader clock {clock_before}")
+
+    # 2. Grouped: every GEMV of the token in one launch (`value`: a throughput
+    # bound for independent GEMVs, whose activations are all ready at launch).
     grouped = not args.chained_only
     if grouped:
         gp = q.plan_grouped([m["pm"] for m in mats], [m["x"] for m in mats], [m["y"] for m in mats], batch=B)
@@ -607,24 +618,67 @@ def main():
         log(f"{wl.name} B={B} grouped: {ms * 1e3:.1f} us/token ({gp.info.n_units} units, "
             f"{gp.info.rows_per_panel}-row panels, {gp.info.grid} workgroups); single replays "
             f"median {spread['median']} p10 {spread['p10']} p90 {spread['p90']} us")
-    else:
+        if q.qtea_grouped_status(gp.workspace, stream=stream):
+            raise RuntimeError("grouped GEMV reported a queue error")
+
+    # 3. Chained: one qtea_gemm_lowbatch launch per GEMV in decode order (each
+    # launch starts after the previous one ends, as when each product feeds
+    # the next): the per-token latency of the named per-product call.
+    ms_chain = float("nan")
+    if wl.groups and not args.grouped_only and B > 1:
+        log("the grouped format runs at batch 1 only: timing the grouped execution")
+        args.grouped_only = True
+    chained_more = {}
+    if not args.grouped_only:
+        g = capture(mats, B, ws, stream)
+        ms_chain = time_graph(g, stream, args.steps, args.warmup)
+        del g
+        for b in extra_b:
+            sub = [dict(m, x=fx[:b], y=fy[:b]) for m, fx, fy in zip(mats, full_x, full_y)]
+            gb_ = capture(sub, b, ws, stream)
+            ms_b = time_graph(gb_, stream, max(10, args.steps // 2), max(3, args.warmup // 2))
+            del gb_
+            chained_more[str(b)] = {"us_per_token": round(ms_b * 1e3, 2),
+                                    "gbs": round(token_bytes / (ms_b * 1e-3) / 1e9, 1),
+                                    "kernel": kernel_name(b, e4m3=wl.resid == "e4m3")}
+            log(f"{wl.name} B={b} chained: {ms_b * 1e3:.1f} us/token, {chained_more[str(b)]['gbs']} GB/s")
+    gbs_chain = token_bytes / (ms_chain * 1e-3) / 1e9
+    log(f"{wl.name} B={B} chained: {ms_chain * 1e3:.1f} us/token, {gbs_chain:.1f} GB/s "
+        f"({gbs_chain / HBM_PEAK_GBS:.1%} of peak)")
+    if not grouped:
         ms = ms_chain
         spread = None
     gbs = token_bytes / (ms * 1e-3) / 1e9
     log(f"{wl.name} B={B}: {ms * 1e3:.1f} us/token, {gbs:.1f} GB/s ({gbs / HBM_PEAK_GBS:.1%} of peak)")
 
-    # Per-role timing: a graph of one role's launches over all layers.
+    # Per role: the role's launches over all layers in one graph, per launch,
+    # through qtea_gemm_lowbatch, and the same matrices each through a
+    # one-problem grouped plan (the grouped kernel on that matrix alone).
     roles = {}
     if not args.no_kernel_timing and not args.grouped_only:
         for mat, (role, N, K) in enumerate(wl.shapes):
             sub = [m for m in mats if m["mat"] == mat]
             gr = capture(sub, B, ws, stream)
             ms_r = time_graph(gr, stream, max(10, args.steps // 4), 5)
+            del gr
             per = ms_r / len(sub)
             roles[role] = {"N": N, "K": K, "us_per_launch": round(per * 1e3, 3),
                            "gbs": round(sub[0]["bytes"] / (per * 1e-3) / 1e9, 1)}
-            log(f"  {role:8s} {N}x{K}: {per * 1e3:.2f} us/launch, {roles[role]['gbs']} GB/s")
-            del gr
+            plans = [q.plan_grouped([m["pm"]], [m["x"]], [m["y"]], batch=B) for m in sub[:8]]
+            g1 = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(stream):
+                for p_ in plans:
+                    p_.run(stream=stream)
+                stream.synchronize()
+                with torch.cuda.graph(g1, stream=stream):
+                    for p_ in plans:
+                        p_.run(stream=stream)
+            stream.synchronize()
+            ms_g1 = time_graph(g1, stream, max(10, args.steps // 4), 5) / len(plans)
+            del g1, plans
+            roles[role]["grouped_one_us"] = round(ms_g1 * 1e3, 3)
+            log(f"  {role:8s} {N}x{K}: {per * 1e3:.2f} us/launch, {roles[role]['gbs']} GB/s "
+                f"(grouped kernel on the same matrix alone: {ms_g1 * 1e3:.2f} us)")
     # Roofline of the dominant kernel.  Grouped: one launch per step moves
     # the token's bytes.  Chained: every GEMV is a launch of the same kernel,
     # so the average launch moves token_bytes / launches.  Durations come
@@ -641,17 +695,17 @@ def main():
             "kernel": kname, "launches_per_step": n_launch,
             "algorithmic_bytes_per_launch": int(per_launch_bytes), "us_per_launch": round(us_launch, 3)}
     chained = {"us_per_token": round(ms_chain * 1e3, 2), "value": round(gbs_chain, 2), "unit": "GB/s",
-               "frac_hbm_peak": round(gbs_chain / HBM_PEAK_GBS, 4), "kernel": kernel_name(B),
+               "frac_hbm_peak": round(gbs_chain / HBM_PEAK_GBS, 4), "kernel": kernel_name(B, e4m3=wl.resid == "e4m3",
+                                                                                        g128=bool(wl.groups)),
                "launches_per_step": len(mats), "us_per_launch": round(ms_chain * 1e3 / len(mats), 3),
-               "per_role": roles} if not args.grouped_only else None
+               "per_role": roles, "other_batches": chained_more} if not args.grouped_only else None
 
     clock_after = gpu_clock()
-    ceiling, ceiling_mean = read_ceiling(dev, stream)
     trit_bytes = sum(m["N"] * m["pm"].desc.n_packs for m in mats)
     device_bytes = sum(int(m["pm"].desc.bytes_total) for m in mats)
     device_gbs = device_bytes / (ms * 1e-3) / 1e9
-    log(f"streaming-read ceiling {ceiling:.1f} GB/s (mean of passes {ceiling_mean:.1f}); this path "
-        f"{gbs / ceiling:.1%} of it in algorithmic bytes, {device_gbs / ceiling:.1%} in device bytes")
+    log(f"this path: {gbs / ceiling:.1%} of the streaming-read ceiling in algorithmic bytes, "
+        f"{device_gbs / ceiling:.1%} in device bytes")
     if grouped:  # leave the grouped outputs in y for the oracle comparison
         with torch.cuda.stream(stream):
             gg.replay()
@@ -676,18 +730,23 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": n_layers, "matrices_per_token": len(mats),
-                   "batch": B, "weight_bytes_per_token": token_bytes, "seed": seed},
+                   "batch": B, "weight_bytes_per_token": token_bytes, "seed": seed,
+                   "residual": "off" if args.residual_off else "on"},
         "us_per_token": round(ms * 1e3, 2),
         "us_per_token_single_replays": spread,
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "read_ceiling": {"gbs": round(ceiling, 1), "mean_gbs": round(ceiling_mean, 1),
                          "frac": round(gbs / ceiling, 4), "device_frac": round(device_gbs / ceiling, 4),
                          "kernel": "read_ceiling_kernel", "bytes": 2 << 30,
-                         "passes": "best of 5 x 20 launches after 200 launches of load"},
+                         "passes": "best of 5 x 20 launches after 200 launches of load, measured first"},
         "trit_bytes_per_token": trit_bytes, "trit_gbs": round(trit_bytes / (ms * 1e-3) / 1e9, 2),
         "device_bytes_per_token": device_bytes, "device_gbs": round(device_gbs, 2),
+        "shader_clock_before_timing": clock_before,
         "shader_clock_after_timing": clock_after,
         "execution": "grouped" if grouped else "chained",
+        "execution_note": ("grouped: every GEMV of the token in one launch, a throughput bound for independent "
+                           "GEMVs; chained: one qtea_gemm_lowbatch launch per GEMV in decode order, the "
+                           "per-token latency when each product feeds the next"),
         "chained": chained,
         "roofline": roof,
         "cpu_baseline": cpu,
