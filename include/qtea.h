@@ -346,7 +346,10 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
  *                     not zero-filled, or one left by a call that did not
  *                     complete); that take yields no chunk, so some outputs
  *                     of the call were not written
- *   QTEA_QUEUE_COUNT  the launch's takes did not add up to the plan's count
+ *   QTEA_QUEUE_COUNT  the chunks the launch ran (a hashed tag per chunk,
+ *                     summed at each workgroup's exit) or its takes did not
+ *                     add up to the plan's: queue words left over from an
+ *                     earlier call made it skip or repeat chunks
  * Either flag means the outputs of the flagged call are not to be used.
  * The last workgroup of every launch leaves the counters at zero, so the
  * next call starts clean; the flags stay set until the workspace is

@@ -88,18 +88,22 @@ static_assert(kWgPerCu * GLds<8>::BYTES <= 160 * 1024, "two workgroups per CU");
 // The chunk queue's words in the first bytes of the workspace: word 0 the
 // take counter, word 1 error flags (sticky until the workspace is
 // zero-filled again), words 2-3 a 64-bit exit word: the count of finished
-// workgroups (high half) and of the chunks they ran (low half).  The
-// workgroup whose exit completes a multiple of the grid checks that the
-// launch ran every chunk once and took exactly the plan's count, and leaves
-// the take counter and the exit word at zero for the next launch.  A take
-// past the plan's count yields no chunk, so every index stays in range,
-// and sets kQueueStale.  A launch that finds the words in a state a
-// completed launch does not leave reports it, one way or the other.
+// workgroups (top 16 bits) and the sum of the tags (chunk_tag) of the
+// chunks they ran (low 48 bits).  The workgroup whose exit completes a
+// multiple of the grid checks that the launch ran every chunk once (the
+// plan's exit_sum) and took exactly the plan's count, and leaves the take
+// counter and the exit word at zero for the next launch.  A take past the
+// plan's count yields no chunk, so every index stays in range, and sets
+// kQueueStale.  A launch that starts from words a completed launch does not
+// leave runs every chunk once or raises a flag, unless the left-over words
+// cancel the tags of the chunks it skipped: the tags are hashed, so that
+// takes some 2^-32 luck rather than a small left-over count.
 constexpr uint32_t kQueueStale = 1u;  // a take found the counter past the plan's count
 constexpr uint32_t kQueueCount = 2u;  // the launch's chunks or takes did not add up to the plan's
+constexpr uint64_t kExitSumMask = (uint64_t(1) << 48) - 1;
 
-__device__ __forceinline__ void queue_exit(uint32_t* counters, uint32_t n_grabs, uint32_t n_chunks,
-                                           uint32_t my_chunks) {
+__device__ __forceinline__ void queue_exit(uint32_t* counters, uint32_t n_grabs, uint64_t exit_sum,
+                                           uint64_t my_sum) {
   if (threadIdx.x != 0) return;
   // Relaxed: every queue word is read and written only by device-scope
   // atomics, which the device performs at one coherence point, and each
@@ -108,12 +112,12 @@ __device__ __forceinline__ void queue_exit(uint32_t* counters, uint32_t n_grabs,
   // acquire-release here would write back and invalidate the L2 of the
   // workgroup's XCD at every exit, under the other workgroups' loads.)
   uint64_t* ew = reinterpret_cast<uint64_t*>(counters + 2);
-  const uint64_t old = __hip_atomic_fetch_add(ew, (uint64_t(1) << 32) | my_chunks, __ATOMIC_RELAXED,
+  const uint64_t old = __hip_atomic_fetch_add(ew, (uint64_t(1) << 48) + my_sum, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT);
-  if ((uint32_t(old >> 32) + 1u) % gridDim.x != 0u) return;
-  const uint32_t ran = uint32_t(old) + my_chunks;
+  if ((uint32_t(old >> 48) + 1u) % gridDim.x != 0u) return;
+  const uint64_t ran = (old + my_sum) & kExitSumMask;
   const uint32_t taken = __hip_atomic_load(counters, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (ran != n_chunks || taken != n_grabs)
+  if (ran != exit_sum || taken != n_grabs)
     __hip_atomic_fetch_or(counters + 1, kQueueCount, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(counters, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(ew, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -177,12 +181,13 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   // table build's barrier, so a chunk switch does not wait for it.  (ONE:
   // one run per workgroup, nothing taken.)
   const uint32_t n_grabs = ONE ? 0u : uint32_t(H->n_grabs);
+  const uint64_t exit_sum = ONE ? 0u : H->exit_sum;
   if (!ONE && g >= NC) {
-    queue_exit(counters, n_grabs, uint32_t(NC), 0u);
+    queue_exit(counters, n_grabs, exit_sum, 0u);
     return;
   }
   int c = g, cn = ONE ? NC : g + G;
-  uint32_t my_chunks = 1;  // chunks this workgroup has started
+  uint64_t my_sum = chunk_tag(uint32_t(g));  // tags of the chunks this workgroup has started
   int* cnext_lds = flag + 1;  // chunk taken from the queue, published at the unit's last barrier
 
   const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, l16 = lane & 15;
@@ -699,7 +704,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     if (take) ctaken = __builtin_amdgcn_readfirstlane(*cnext_lds);  // written before the last barrier
     chunk_first = chunk_last;
     if (chunk_last) {
-      ++my_chunks;
+      my_sum += chunk_tag(uint32_t(cn));
       c = cn;
       u = rec_cn.ub;
       ue = rec_cn.ue;
@@ -714,7 +719,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     if (!G128) load_alpha(nxt, al);  // and of its row scales
     cur = nxt;
   }
-  if constexpr (!ONE) queue_exit(counters, n_grabs, uint32_t(NC), my_chunks);
+  if constexpr (!ONE) queue_exit(counters, n_grabs, exit_sum, my_sum);
 }
 
 // Sums the parts of every split panel in chunk order (deterministic) and
@@ -758,19 +763,6 @@ __global__ __launch_bounds__(RP / 4) void grouped_reduce_kernel(const uint8_t* _
 // ---------------------------------------------------------------------------
 // Host planning.
 // ---------------------------------------------------------------------------
-constexpr int kMaxRB = 8;
-// Chunks: the unit list is cut into chunks whose sizes shrink from about
-// 1/(kGuide G) of the remaining work to a single unit (guided self-
-// scheduling), at most kMaxChunksPerWg per workgroup on average.
-constexpr int kGuide = 3;
-constexpr int kMaxChunksPerWg = 16;
-
-int units_for(const qtea_desc& d, int RP, int* n_slices, int* n_panels) {
-  *n_slices = int(cdiv(d.n_groups, kSliceGroups));
-  *n_panels = int(cdiv(d.n_pad, RP));
-  return *n_slices * *n_panels;
-}
-
 template <int RB, bool F8, bool G128 = false, bool ONE = false>
 hipError_t set_lds_attr() {
   static bool done = false;
@@ -818,63 +810,15 @@ hipError_t launch_grouped(const uint8_t* plan, int grid, int n_splits, float* pa
   return hipGetLastError();
 }
 
-// The problem record of one packed matrix with its activations and outputs.
-void fill_problem(const qtea_desc& d, const void* packed, const uint16_t* x, float* y, int RP, GProblem& pr) {
-  const uint8_t* pk = static_cast<const uint8_t*>(packed);
-  pr = GProblem{};
-  pr.trits = pk + d.off_trits;
-  pr.alpha = reinterpret_cast<const uint16_t*>(pk + d.off_alpha);
-  pr.v = reinterpret_cast<const uint16_t*>(pk + d.off_v);
-  pr.S = reinterpret_cast<const int32_t*>(pk + d.off_salient);
-  pr.spos = reinterpret_cast<const int32_t*>(pk + d.off_spos);
-  pr.rval = reinterpret_cast<const uint16_t*>(pk + d.off_rval);
-  pr.ridx = reinterpret_cast<const uint32_t*>(pk + d.off_ridx);
-  Layout lm;  // regions the descriptor does not list
-  make_layout(d.N, d.K, d.n_salient, &lm, int(d.layout));  // succeeds: desc_ok checked it
-  pr.vs = reinterpret_cast<const uint32_t*>(pk + lm.off_vs);
-  pr.x = x;
-  pr.y = y;
-  pr.N = d.N;
-  pr.K = d.K;
-  pr.n_pad = d.n_pad;
-  pr.n_groups = int32_t(d.n_groups);
-  pr.nS = int32_t(d.n_salient);
-  int ns, np;
-  units_for(d, RP, &ns, &np);
-  pr.n_slices = ns;
-  pr.n_panels = np;
-  pr.unit_base = 0;
-}
-
-// The kernels address the packed bytes and the residual with 32-bit offsets.
-bool offsets_fit(const qtea_desc& d) {
-  const int64_t trit_bytes = d.n_pad * d.n_groups * kGroupPacks;
-  const int64_t resid_bytes = (d.n_pad / 4) * d.n_salient * (d.layout == kLayout ? 2 : 1);
-  return trit_bytes < (int64_t(1) << 31) && resid_bytes < (int64_t(1) << 31);
-}
-
-// Launch shape of one matrix on its own (qtea_gemv, qtea_gemm_lowbatch):
-// batch 1 runs the table kernel on 512-row panels, two workgroups per CU at
-// most; batch 2..16 the matrix-core kernel on its 1024-row panels, one per
-// CU.  Every workgroup takes the same number of units (the least that fits
-// the grid), so no workgroup carries more than the others.  The workspace
-// holds one arrival counter per panel, then two partial-row slots per
-// workgroup.
+// Launch shape of one matrix on its own: batch 1 runs the table kernel on
+// 512-row panels, two workgroups per CU at most; batch 2..16 the matrix-core
+// kernel on its 1024-row panels, one per CU.
 constexpr int kOneRB = 4;
-struct OneShape {
-  int rp, n_panels, n_slices, grid;
-  int64_t n_units, off_part, ws_bytes;
-};
+static_assert(GLds<kOneRB>::RP == kRowsPerRB * kOneRB && GLds<kMaxRB>::RP == kRowsPerRB * kMaxRB,
+              "panel heights of the planner");
 bool one_shape(const qtea_desc& d, int batch, OneShape* o) {
-  const int max_wg = batch == 1 ? grid_size() : cu_count();
-  if (max_wg < 1) return false;
-  o->rp = batch == 1 ? GLds<kOneRB>::RP : grouped_mma_rows_per_panel();
-  o->n_units = units_for(d, o->rp, &o->n_slices, &o->n_panels);
-  const int64_t per = cdiv(o->n_units, max_wg);
-  o->grid = int(cdiv(o->n_units, per));
-  o->off_part = align_up(4 * int64_t(o->n_panels), kAlign);
-  o->ws_bytes = o->off_part + 2 * int64_t(o->grid) * o->rp * batch * 4;
-  return true;
+  return one_shape_for(d, batch, batch == 1 ? grid_size() : cu_count(),
+                       batch == 1 ? GLds<kOneRB>::RP : grouped_mma_rows_per_panel(), o);
 }
 
 template <bool F8, bool G128>
@@ -946,9 +890,7 @@ int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes) {
   if (!out_bytes || n_problems < 1) return QTEA_ERR_INVALID_ARG;
   const int G = grid_size();
   if (G < 1) return QTEA_ERR_HIP;
-  const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
-  *out_bytes = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign) +
-               align_up(int64_t(sizeof(GChunk)) * max_chunks, kAlign) + int64_t(sizeof(GSplit)) * max_chunks;
+  *out_bytes = plan_bytes_for(n_problems, G);
   return QTEA_OK;
 }
 
@@ -958,193 +900,30 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   if (!descs || !packed || !x || !y || !plan || !info || n_problems < 1) return QTEA_ERR_INVALID_ARG;
   info->magic = 0;
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
-  int64_t need = 0;
-  const int st_plan = qtea_grouped_plan_bytes(n_problems, &need);
+  int64_t cap = 0;
+  const int st_plan = qtea_grouped_plan_bytes(n_problems, &cap);
   if (st_plan != QTEA_OK) return st_plan;
-  if (plan_bytes < need) return QTEA_ERR_WORKSPACE;
+  if (plan_bytes < cap) return QTEA_ERR_WORKSPACE;
   // batch 1: the table kernel, two workgroups per CU and the chunk queue;
   // batch 2..16: the matrix-core kernel, one workgroup per CU and one
   // static run of units each
-  const bool mma = batch > 1;
-  const int G = mma ? cu_count() : grid_size();
+  const int G = batch > 1 ? cu_count() : grid_size();
   if (G < 1) return QTEA_ERR_HIP;
-  const uint32_t layout = descs[0].layout;
-  if (layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;  // the grouped format runs at batch 1
-  for (int m = 0; m < n_problems; ++m) {
-    if (!desc_ok(&descs[m]) || !packed[m] || !x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
-    if (descs[m].layout != layout) return QTEA_ERR_INVALID_ARG;  // one residual format per plan
-    if (!offsets_fit(descs[m])) return QTEA_ERR_INVALID_ARG;
-  }
-
-  // rows per panel: the largest that still gives every workgroup several units
-  int RB = kMaxRB;
-  for (; !mma && RB > 4; RB /= 2) {
-    int64_t units = 0;
-    for (int m = 0; m < n_problems; ++m) {
-      int ns, np;
-      units += units_for(descs[m], GLds<kMaxRB>::RP / kMaxRB * RB, &ns, &np);
-    }
-    if (units >= 4 * int64_t(G)) break;
-  }
-  const int RP = mma ? grouped_mma_rows_per_panel() : GLds<kMaxRB>::RP / kMaxRB * RB;
-
-  const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
-  const int64_t off_chunks = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
-  const int64_t off_splits = off_chunks + align_up(int64_t(sizeof(GChunk)) * max_chunks, kAlign);
-  uint8_t* hbuf = static_cast<uint8_t*>(calloc(1, size_t(need)));
+  const int64_t need = plan_bytes_for(n_problems, G);
+  uint8_t* hbuf = static_cast<uint8_t*>(malloc(size_t(need)));
   if (!hbuf) return QTEA_ERR_INVALID_ARG;
-  GPlanHeader* H = reinterpret_cast<GPlanHeader*>(hbuf);
-  GProblem* P = reinterpret_cast<GProblem*>(hbuf + kPlanProblemsOff);
-  GChunk* chunks = reinterpret_cast<GChunk*>(hbuf + off_chunks);
-  std::vector<int64_t> ranges(size_t(max_chunks) + 1, 0);  // chunk k holds units [ranges[k], ranges[k + 1])
-  GSplit* splits = reinterpret_cast<GSplit*>(hbuf + off_splits);
-
-  // unit costs: packed bytes of the unit plus a fixed table-build share;
-  // prefix sums of the costs, and the end (exclusive) of each unit's panel
-  std::vector<int64_t> prefix(1, 0), panel_end;
-  std::vector<GChunk> ucur;
-  int64_t total_units = 0;
-  // Problems are laid out with the most K slices per panel first (stable),
-  // so that the small chunks at the end of the unit list split panels of
-  // few slices.  The kernel only needs each problem's units to be
-  // contiguous; outputs are addressed through each problem's own record.
-  std::vector<int> order(static_cast<size_t>(n_problems));
-  for (int m = 0; m < n_problems; ++m) order[size_t(m)] = m;
-  std::stable_sort(order.begin(), order.end(),
-                   [&](int a, int b) { return descs[a].n_groups > descs[b].n_groups; });
-  for (int m = 0; m < n_problems; ++m) {
-    const int src = order[size_t(m)];
-    const qtea_desc& d = descs[src];
-    int ns, np;
-    units_for(d, RP, &ns, &np);
-    GProblem& pr = P[m];
-    fill_problem(d, packed[src], x[src], y[src], RP, pr);
-    pr.unit_base = total_units;
-    for (int p = 0; p < np; ++p) {
-      const int64_t rows = std::min<int64_t>(RP, d.n_pad - int64_t(p) * RP);
-      const int64_t pe = total_units + int64_t(p + 1) * ns;
-      for (int s = 0; s < ns; ++s) {
-        const int64_t groups = std::min<int64_t>(kSliceGroups, d.n_groups - int64_t(s) * kSliceGroups);
-        prefix.push_back(prefix.back() + rows * groups * kGroupPacks + 8192);
-        panel_end.push_back(pe);
-        ucur.push_back(GChunk{0, 0, m, p, s, {0, 0, 0}});
-      }
-    }
-    total_units += int64_t(ns) * np;
-  }
-  if (total_units >= (int64_t(1) << 31)) {  // unit indices are 32-bit on the device
+  const int rc = plan_write(descs, packed, x, y, n_problems, batch, G, grouped_mma_rows_per_panel(), hbuf, need,
+                            info);
+  if (rc != QTEA_OK) {
     free(hbuf);
-    return QTEA_ERR_INVALID_ARG;
+    return rc;
   }
-  // chunks: guided sizes, a chunk that reaches the end of its panel (or
-  // several panels) within half a target taking them whole, so that most
-  // small panels are not split
-  int64_t n_chunks = 0;
-  if (mma) {
-    // one contiguous run of balanced cost per workgroup
-    const int64_t total_cost = prefix.back();
-    int64_t u = 0;
-    ranges[0] = 0;
-    for (int k = 1; k <= G && u < total_units; ++k) {
-      int64_t e = k == G ? total_units
-                         : int64_t(std::lower_bound(prefix.begin(), prefix.end(), (total_cost * k) / G) - prefix.begin());
-      e = std::min(total_units, std::max(e, u + 1));
-      chunks[n_chunks] = ucur[size_t(u)];
-      chunks[n_chunks].ub = int32_t(u);
-      chunks[n_chunks].ue = int32_t(e);
-      ranges[size_t(++n_chunks)] = e;
-      u = e;
-    }
-  } else {
-    const int64_t total_cost = prefix.back();
-    const int64_t unit_min = prefix[1] - prefix[0];
-    int64_t u = 0;
-    ranges[0] = 0;
-    while (u < total_units) {
-      const int64_t rem = total_cost - prefix[size_t(u)];
-      // every chunk but the last covers at least half its target, so a
-      // target of twice the remaining cost per remaining chunk of the budget
-      // finishes within the budget with chunks of equal cost, instead of
-      // leaving the whole rest to one workgroup
-      const int64_t left = max_chunks - n_chunks;
-      const int64_t target = std::max({unit_min, rem / (int64_t(kGuide) * G), 2 * rem / left});
-      int64_t e = u;
-      if (n_chunks + 1 == max_chunks) {
-        e = total_units;  // chunk budget spent: the rest is one chunk
-      } else {
-        while (e < total_units) {
-          const int64_t pe = panel_end[size_t(e)];
-          const int64_t have = prefix[size_t(e)] - prefix[size_t(u)];
-          if (have + prefix[size_t(pe)] - prefix[size_t(e)] <= target + target / 2) {
-            e = pe;  // the rest of this panel fits
-            if (prefix[size_t(e)] - prefix[size_t(u)] >= target) break;
-            continue;
-          }
-          if (e > u && have >= target / 2) break;  // cut at the panel boundary
-          while (e < pe && prefix[size_t(e)] - prefix[size_t(u)] < target) ++e;
-          break;
-        }
-      }
-      chunks[n_chunks] = ucur[size_t(u)];
-      chunks[n_chunks].ub = int32_t(u);
-      chunks[n_chunks].ue = int32_t(e);
-      ranges[size_t(++n_chunks)] = e;
-      u = e;
-    }
-  }
-  // split panels (a chunk is the first chunk of at most one of them, so
-  // there are at most n_chunks), and the largest number of parts of one
-  int max_parts = 1;
-  int64_t n_splits = 0;
-  for (int m = 0; m < n_problems; ++m) {
-    for (int p = 0; p < P[m].n_panels; ++p) {
-      const int64_t p0 = P[m].unit_base + int64_t(p) * P[m].n_slices, p1 = p0 + P[m].n_slices;
-      const auto rb = ranges.begin(), re = ranges.begin() + n_chunks + 1;
-      const int ga = int(std::upper_bound(rb, re, p0) - rb) - 1;
-      const int gb = int(std::lower_bound(rb, re, p1) - rb) - 1;
-      if (gb > ga) splits[n_splits++] = GSplit{m, p, ga, gb, p0 > ranges[size_t(ga)] ? 1 : 0, {0, 0, 0}};
-      max_parts = std::max(max_parts, gb - ga + 1);
-    }
-  }
-  // queue takes of one launch: every chunk past the first 2G, plus one
-  // final take by each workgroup that has a second chunk
-  const int64_t n_grabs = mma ? 0
-                              : std::max<int64_t>(0, n_chunks - 2 * int64_t(G)) +
-                                    std::min<int64_t>(G, std::max<int64_t>(0, n_chunks - G));
-  H->magic = kGPlanMagic;
-  H->version = 2;
-  H->n_problems = n_problems;
-  H->n_wg = G;
-  H->rows_per_panel = RP;
-  H->max_parts = max_parts;
-  H->batch = batch;
-  H->n_chunks = int32_t(n_chunks);
-  H->n_units = total_units;
-  H->off_chunks = off_chunks;
-  H->n_grabs = n_grabs;
-  H->off_splits = off_splits;
-  H->n_splits = n_splits;
-  H->f8 = layout != kLayout;
-
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(plan, hbuf, size_t(need), hipMemcpyHostToDevice, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   free(hbuf);
   if (e != hipSuccess) return QTEA_ERR_HIP;
-
   info->magic = kGPlanMagic;
-  info->n_problems = n_problems;
-  info->batch = batch;
-  info->grid = G;
-  info->rows_per_panel = RP;
-  info->max_parts = max_parts;
-  info->n_chunks = int32_t(n_chunks);
-  info->n_split_panels = int32_t(n_splits);
-  info->layout = int32_t(layout);
-  info->reserved = 0;
-  info->n_units = total_units;
-  info->plan_bytes = need;
-  info->workspace_bytes = kAlign + 2 * n_chunks * RP * int64_t(batch) * 4;
   return QTEA_OK;
 }
 

@@ -5,54 +5,12 @@
 #ifndef QTEA_GROUPED_PLAN_H_
 #define QTEA_GROUPED_PLAN_H_
 
+#include "plan_host.h"
 #include "qtea_internal.h"
 
 namespace qtea_grouped {
 
 using namespace qtea_detail;
-
-constexpr int kSliceGroups = 4;                           // groups per K slice (one per quarter-wave)
-constexpr int kSlicePacks = kSliceGroups * kGroupPacks;   // 64
-constexpr int kSliceCols = kSliceGroups * kGroupCols;     // 320
-constexpr uint32_t kGPlanMagic = 0x51475250u;            // "QGRP"
-constexpr int64_t kPlanProblemsOff = 256;
-
-struct GProblem {
-  const uint8_t* trits;
-  const uint16_t* alpha;
-  const uint16_t* v;
-  const int32_t* S;
-  const int32_t* spos;
-  const uint16_t* rval;  // fp16, or E4M3 bytes when the plan's f8 is set
-  const uint32_t* ridx;
-  const uint16_t* x;
-  float* y;
-  int64_t N, K, n_pad;
-  int32_t n_groups, nS, n_slices, n_panels;
-  int64_t unit_base;
-  const uint32_t* vs;  // v | (1 + rank in the slice's salient run) << 16, per device column
-};
-static_assert(sizeof(GProblem) == 128, "plan record size");
-
-// One problem run on its own (qtea_gemv, qtea_gemm_lowbatch): its record
-// is a kernel argument, and workgroup g of G takes the contiguous run of
-// units [g U / G, (g + 1) U / G) of the U = n_panels * n_slices units.  A
-// panel whose units fall in more than one run is finished by the last of
-// its workgroups to arrive (a counter per panel in the workspace), which
-// sums the parts in run order.
-struct GOne {
-  GProblem pr;
-  int32_t n_units;
-  int32_t batch;
-  int32_t reserved[2];
-};
-
-// Workgroup whose run holds unit x, for U units over G runs: the largest g
-// with floor(g U / G) <= x.
-__host__ __device__ __forceinline__ int one_owner(int64_t x, int64_t U, int64_t G) {
-  return int(((x + 1) * G - 1) / U);
-}
-__host__ __device__ __forceinline__ int64_t one_first(int64_t g, int64_t U, int64_t G) { return (g * U) / G; }
 
 // Coherent 16-byte load from the workspace (device scope: sc1), for parts
 // written by other workgroups with device-scope stores.
@@ -121,26 +79,6 @@ __device__ __forceinline__ void sum_parts(const float* part, int64_t S, int ga, 
     }
   }
 }
-
-struct GPlanHeader {
-  uint32_t magic, version;
-  int32_t n_problems, n_wg, rows_per_panel, max_parts, batch, n_chunks;
-  int64_t n_units, off_chunks, n_grabs, off_splits, n_splits;
-  int32_t f8, reserved;  // residual values are E4M3 bytes (layout 3) in every problem
-};
-
-// A chunk: units [ub, ue), the first of them at (problem m, panel, slice).
-struct GChunk {
-  int32_t ub, ue, m, panel, slice, reserved[3];
-};
-static_assert(sizeof(GChunk) == 32, "one scalar load per chunk record");
-
-// A panel whose slices fall in more than one chunk: its parts are in the
-// partial slots of chunks ga..gb (slot 2k, except 2ga + 1 when the part in
-// chunk ga starts after that chunk's first unit).
-struct GSplit {
-  int32_t m, panel, ga, gb, ga_odd, reserved[3];
-};
 
 typedef __attribute__((address_space(1))) const uint8_t gu8;
 typedef __attribute__((address_space(1))) const uint16_t gu16;

@@ -509,23 +509,7 @@ int pack_any(int layout, const int8_t* trits, int64_t N, int64_t K, const uint16
   if (hflags & kFlagBadTrit) return QTEA_ERR_BAD_TRIT;
   if (hflags & kFlagBadResid) return QTEA_ERR_BAD_RESIDUAL;
 
-  qtea_desc d;
-  d.magic = QTEA_DESC_MAGIC;
-  d.layout = uint32_t(layout);
-  d.N = N;
-  d.K = K;
-  d.n_salient = n_salient;
-  d.n_packs = L.n_packs;
-  d.n_groups = L.n_groups;
-  d.n_pad = L.n_pad;
-  d.bytes_total = L.total;
-  d.off_trits = L.off_trits;
-  d.off_alpha = L.off_alpha;
-  d.off_v = L.off_v;
-  d.off_salient = L.off_salient;
-  d.off_spos = L.off_spos;
-  d.off_rval = L.off_rval;
-  d.off_ridx = L.off_ridx;
+  const qtea_desc d = desc_from_layout(L, N, K, n_salient, layout);
   *out_desc = d;
   return QTEA_OK;
 }

@@ -63,15 +63,32 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
+
+def build_sanitized(out_dir: str) -> str:
+    """Compile the same source with the host address and undefined-behaviour
+    sanitizers into out_dir (load it through $QTEA_SYNTH_LIB, with the sanitizer
+    runtime preloaded); returns the library path."""
+    out = os.path.join(out_dir, "libsynth.so")
+    subprocess.check_call(
+        ["gcc", "-O1", "-g", "-fPIC", "-shared", "-fopenmp", "-std=c11",
+         "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer",
+         "-o", out, _SRC, "-lm"]
+    )
+    return out
+
+
 _lib = None
 
 
 def _L():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
-            build()
-        lib = ctypes.CDLL(_LIB)
+        path = os.environ.get("QTEA_SYNTH_LIB")  # another build of the same source (the sanitized one)
+        if not path:
+            if not os.path.exists(_LIB):
+                build()
+            path = _LIB
+        lib = ctypes.CDLL(path)
         u64, i64, i32, dbl, vp = (ctypes.c_uint64, ctypes.c_int64, ctypes.c_int,
                                   ctypes.c_double, ctypes.c_void_p)
         lib.synth_sm64_at.restype = u64

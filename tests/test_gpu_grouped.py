@@ -235,12 +235,14 @@ def test_grouped_queue_left_over_counter_is_flagged():
     for c, y in zip(cases, first):
         ref, wmax = oracle_rows(c)
         assert_close(y, ref, c["x"], wmax, f"grouped {c['N']}x{c['K']}")
-    # workspace words: [0] take counter, [1] flags, [2] chunks run, [3] workgroups finished
+    # workspace words: [0] take counter, [1] flags, [2:4] the exit word (finished
+    # workgroups in its top 16 bits, the tags of the chunks they ran below)
     words = ws[:16].view(torch.int32)
-    for start_take, start_exit in ((5, 0), (-(2 ** 31), 0), (0, 3)):
-        _report(f"grouped queue: take counter {start_take & 0xffffffff}, exit count {start_exit}")
+    exitw = ws[8:16].view(torch.int64)
+    for start_take, start_exit in ((5, 0), (-(2 ** 31), 0), (0, 3 << 48), (0, 7)):
+        _report(f"grouped queue: take counter {start_take & 0xffffffff}, exit word {start_exit:#x}")
         words[0] = start_take
-        words[3] = start_exit
+        exitw[0] = start_exit
         torch.cuda.synchronize()
         gp.run()
         flags = q.qtea_grouped_status(ws)
@@ -248,7 +250,7 @@ def test_grouped_queue_left_over_counter_is_flagged():
         if start_take < 0:
             assert flags & q.QTEA_QUEUE_STALE
         if start_exit == 0:
-            assert words[0].item() == 0 and words[2].item() == 0 and words[3].item() == 0, "counters not reset"
+            assert words[0].item() == 0 and exitw[0].item() == 0, "counters not reset"
         ws.zero_()
         again = run_clean()
         for a, b in zip(first, again):
