@@ -176,9 +176,10 @@ int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* gr
  * this matrix at this batch size on the current device.  A call splits the
  * matrix's output panels (512 rows at batch 1, 1024 above) and its K range
  * into work units over one launch; a panel whose units fall to more than
- * one workgroup is summed by the last of them to arrive.  The workspace
- * holds one arrival counter per panel and two slots of partial rows per
- * workgroup.  It must be zero-filled before its first use
+ * one workgroup is summed from their partial rows in a fixed order, at
+ * batch 1 by the last of them to arrive, at batch 2..16 by a second small
+ * kernel on the same stream.  The workspace holds one arrival counter per
+ * panel and two slots of partial rows per workgroup.  It must be zero-filled before its first use
  * (qtea_workspace_init or any zero fill); every call that runs to
  * completion leaves the counters at zero again, so one workspace serves any
  * sequence of stream-ordered calls.  Calls that may overlap in time must

@@ -150,8 +150,11 @@ __device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
 
 // F8: residual values are E4M3 bytes (layout 3), else fp16 (layout 2).
 // ONE: a single problem launched on its own (GOne, no plan): workgroup g
-// takes the units [g U / G, (g + 1) U / G), and a panel split between runs
-// is summed by the last of its workgroups to arrive (counters[panel]).
+// takes the units [g U / G, (g + 1) U / G); a panel split between runs has
+// its parts stored and summed after the launch by one_reduce_kernel (a
+// last-arriver sum inside this kernel cost more: the stores' completion,
+// the arrival's round trip and one workgroup summing up to 45 parts alone
+// stood between every split panel and its output).
 template <int NB, bool F8, bool ONE = false>
 __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
                                                           float* __restrict__ part,
@@ -189,36 +192,6 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int jr = lane & 15, kb = lane >> 4;  // MFMA A row / B column, and k-block
   const int rs = jr & 3;                     // byte rotation left after the tile's 4q
-
-  // decode tables, copy = the lane's index in its half-wave: digits 0-3 of
-  // code c as fp16 at c * 256 + 8 copy, digit 4 in the T4 table.  One copy
-  // of each code is computed (in the first image buffer, free until the
-  // first images are built), then every copy is written from it.
-  {
-    uint32_t* one_copy = reinterpret_cast<uint32_t*>(lds + L::IMG);  // [243][3] words
-    if (tid < kCodes) {
-      const int c = tid;
-      const int d0 = c % 3, r1 = c / 3, d1 = r1 % 3, r2 = r1 / 3, d2 = r2 % 3, r3 = r2 / 3, d3 = r3 % 3, d4 = r3 / 3;
-      _Float16 t[4] = {(_Float16)(d0 - 1), (_Float16)(d1 - 1), (_Float16)(d2 - 1), (_Float16)(d3 - 1)};
-      u32x2 m;
-      __builtin_memcpy(&m, t, 8);
-      const _Float16 t4[2] = {(_Float16)(d4 - 1), (_Float16)0};
-      uint32_t m4;
-      __builtin_memcpy(&m4, t4, 4);
-      one_copy[3 * c] = m.x;
-      one_copy[3 * c + 1] = m.y;
-      one_copy[3 * c + 2] = m4;
-    }
-    __syncthreads();
-    for (int e = tid; e < kCodes * 32; e += kMT) {
-      const int c = e >> 5, cp = e & 31;
-      *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = u32x2{one_copy[3 * c], one_copy[3 * c + 1]};
-      *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = one_copy[3 * c + 2];
-    }
-    __syncthreads();  // the first images overwrite the computed copy
-  }
-  if (tid < 3) bigf[tid] = 0;
-  __syncthreads();  // flags cleared before the first images can set one
 
   // per-lane constants: table copy offset (byte 0 of lane_base), unrotation selector
   const uint32_t lane_base = uint32_t(8 * (lane & 31));
@@ -306,6 +279,36 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   for (int q = 0; q < 4; ++q)
     W[q] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(PR(cur.m).trits) + w_off(cur, q)));
   load_xv(cur);
+  // decode tables, copy = the lane's index in its half-wave: digits 0-3 of
+  // code c as fp16 at c * 256 + 8 copy, digit 4 in the T4 table.  One copy
+  // of each code is computed (in the first image buffer, free until the
+  // first images are built), then every copy is written from it.
+  {
+    uint32_t* one_copy = reinterpret_cast<uint32_t*>(lds + L::IMG);  // [243][3] words
+    if (tid < kCodes) {
+      const int c = tid;
+      const int d0 = c % 3, r1 = c / 3, d1 = r1 % 3, r2 = r1 / 3, d2 = r2 % 3, r3 = r2 / 3, d3 = r3 % 3, d4 = r3 / 3;
+      _Float16 t[4] = {(_Float16)(d0 - 1), (_Float16)(d1 - 1), (_Float16)(d2 - 1), (_Float16)(d3 - 1)};
+      u32x2 m;
+      __builtin_memcpy(&m, t, 8);
+      const _Float16 t4[2] = {(_Float16)(d4 - 1), (_Float16)0};
+      uint32_t m4;
+      __builtin_memcpy(&m4, t4, 4);
+      one_copy[3 * c] = m.x;
+      one_copy[3 * c + 1] = m.y;
+      one_copy[3 * c + 2] = m4;
+    }
+    __syncthreads();
+    for (int e = tid; e < kCodes * 32; e += kMT) {
+      const int c = e >> 5, cp = e & 31;
+      *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = u32x2{one_copy[3 * c], one_copy[3 * c + 1]};
+      *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = one_copy[3 * c + 2];
+    }
+    __syncthreads();  // the first images overwrite the computed copy
+  }
+  if (tid < 3) bigf[tid] = 0;
+  __syncthreads();  // flags cleared before the first images can set one
+
   const bool big0 = build(0, 1.0f, 0);  // the run's first unit starts a part
   if (big0) bigf[0] = 1;
   __syncthreads();
@@ -547,43 +550,6 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) C[q][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       }
-      if constexpr (ONE) {
-        if (!owned) {
-          // the last of the panel's workgroups to arrive sums its parts in
-          // run order (slot 2k for a part at its run's first unit, 2k + 1
-          // for one starting later: only the first run's part can)
-          const int64_t ns = pr.n_slices, p0 = int64_t(cur.panel) * ns;
-          const int ga = one_owner(p0, one.n_units, G), gb = one_owner(p0 + ns - 1, one.n_units, G);
-          // every wave's stores have reached the cache before the arrival;
-          // the arrival's release then writes them back for the other XCDs
-          // (measured faster here than device-scope stores, which write
-          // through one partly filled line at a time)
-          __builtin_amdgcn_s_waitcnt(0);
-          __syncthreads();
-          if (tid == 0) {
-            const uint32_t before = __hip_atomic_fetch_add(counters + cur.panel, 1u, __ATOMIC_RELEASE,
-                                                           __HIP_MEMORY_SCOPE_AGENT);
-            const bool last = before == uint32_t(gb - ga);
-            if (last) __hip_atomic_store(counters + cur.panel, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            bigf[3] = last;
-            if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other parts, visible to this XCD
-          }
-          __syncthreads();
-          if (bigf[3]) {
-            const int odd0 = one_first(ga, one.n_units, G) < p0 ? 1 : 0;
-            const int64_t prow0 = int64_t(cur.panel) * kMRP;
-            // LDS scratch: the B-operand images, free until the next unit's build
-            sum_parts<kMT>(part, int64_t(kMRP) * B, ga, gb, odd0, reinterpret_cast<float4*>(lds + L::IMG),
-                           [&](int e, float4 v) {
-                             const int b = e / kMRP, r = e - b * kMRP;
-                             if (prow0 + r < pr.N) {  // N % 4 == 0
-#pragma unroll
-                               for (int i = 0; i < 4; ++i) pr.y[int64_t(b) * pr.N + prow0 + r + i] = v[i];
-                             }
-                           });
-          }
-        }
-      }
     }
     // the next unit's images into the other buffer, after the part end's
     // reads of the gather array (a next unit after a part end starts a new
@@ -597,6 +563,40 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     }
     __syncthreads();  // the next unit's images are complete; this unit's are free
     cur = nxt;
+  }
+}
+
+// Sums the parts of the split panels of a one-problem launch in run order
+// (deterministic): one workgroup per (panel, batch row), four consecutive
+// rows per thread, eight parts' loads in flight.  Part slot k holds [batch
+// row][kMRP] floats: slot 2k the part of run k that starts at the run's
+// first unit, 2k + 1 a part starting later in the run (only the first run
+// of a panel can).
+__global__ __launch_bounds__(kMRP / 4) void one_reduce_kernel(const GOne one, const float* __restrict__ part, int grid) {
+  const int panel = blockIdx.x, b = blockIdx.y, B = one.batch;
+  const int64_t U = one.n_units, G = grid, ns = one.pr.n_slices, p0 = int64_t(panel) * ns;
+  const int ga = one_owner(p0, U, G), gb = one_owner(p0 + ns - 1, U, G);
+  if (ga == gb) return;  // one run holds the panel: its rows of y were written by that run
+  const int odd0 = one_first(ga, U, G) < p0 ? 1 : 0;
+  const int row = 4 * threadIdx.x;
+  f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int k0 = ga; k0 <= gb; k0 += 8) {
+    f32x4 t[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = min(k0 + j, gb);
+      const int64_t slot = 2 * int64_t(k) + (k == ga ? odd0 : 0);
+      t[j] = *reinterpret_cast<const f32x4*>(part + (slot * B + b) * kMRP + row);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (k0 + j <= gb) sum += t[j];
+  }
+  const int64_t r = int64_t(panel) * kMRP + row;
+  if (r < one.pr.N) {  // N % 4 == 0: the four rows are all in or all out
+    float* y = one.pr.y + int64_t(b) * one.pr.N + r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y[i] = sum[i];
   }
 }
 
@@ -627,10 +627,19 @@ hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8,
 }
 
 hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint32_t* counters, hipStream_t st) {
-  if (f8) return one.batch <= 8 ? launch<1, true, true>(nullptr, grid, part, counters, one, st)
-                                : launch<2, true, true>(nullptr, grid, part, counters, one, st);
-  return one.batch <= 8 ? launch<1, false, true>(nullptr, grid, part, counters, one, st)
-                        : launch<2, false, true>(nullptr, grid, part, counters, one, st);
+  hipError_t e;
+  if (f8) e = one.batch <= 8 ? launch<1, true, true>(nullptr, grid, part, counters, one, st)
+                             : launch<2, true, true>(nullptr, grid, part, counters, one, st);
+  else e = one.batch <= 8 ? launch<1, false, true>(nullptr, grid, part, counters, one, st)
+                          : launch<2, false, true>(nullptr, grid, part, counters, one, st);
+  if (e != hipSuccess) return e;
+  bool split = false;
+  const int64_t ns = one.pr.n_slices;
+  for (int p = 0; p < one.pr.n_panels && !split; ++p)
+    split = one_owner(p * ns, one.n_units, grid) != one_owner(p * ns + ns - 1, one.n_units, grid);
+  if (!split) return hipSuccess;
+  hipLaunchKernelGGL(one_reduce_kernel, dim3(one.pr.n_panels, one.batch), dim3(kMRP / 4), 0, st, one, part, grid);
+  return hipGetLastError();
 }
 
 }  // namespace qtea_grouped

@@ -59,9 +59,9 @@ static_assert(sizeof(GProblem) == 128, "plan record size");
 // One problem run on its own (qtea_gemv, qtea_gemm_lowbatch): its record
 // is a kernel argument, and workgroup g of G takes the contiguous run of
 // units [g U / G, (g + 1) U / G) of the U = n_panels * n_slices units.  A
-// panel whose units fall in more than one run is finished by the last of
-// its workgroups to arrive (a counter per panel in the workspace), which
-// sums the parts in run order.
+// panel whose units fall in more than one run is summed in run order: at
+// batch 1 by the last of its workgroups to arrive (a counter per panel in
+// the workspace), at batch 2..16 by a small reduce kernel after the launch.
 struct GOne {
   GProblem pr;
   int32_t n_units;
@@ -167,7 +167,7 @@ inline bool offsets_fit(const qtea_desc& d) {
 // at most max_wg workgroups of rp-row panels.  Every workgroup takes the
 // same number of units (the least that fits the grid), so no workgroup
 // carries more than the others.  The workspace holds one arrival counter
-// per panel, then two partial-row slots per workgroup.
+// per panel (used at batch 1), then two partial-row slots per workgroup.
 struct OneShape {
   int rp, n_panels, n_slices, grid;
   int64_t n_units, off_part, ws_bytes;
