@@ -148,8 +148,11 @@ def replay_spread(g, stream, reps):
 
 def kernel_name(B, grouped=False, rows_per_panel=1024, e4m3=False, g128=False):
     f8 = "true" if e4m3 else "false"
+    # the grouped format runs every batch row through the batch-1 table kernel
     if grouped and g128:
         return f"grouped_gemv_kernel<{rows_per_panel // 128}, true, true>"
+    if g128:
+        return "grouped_gemv_kernel<4, true, true, true>"
     if grouped and B > 1:
         # hi/lo activation halves in one or two MFMAs
         return f"grouped_mma_kernel<{1 if B <= 8 else 2}, {f8}>"
@@ -588,7 +591,7 @@ def main():
     B = args.batch
     seed = synth.DEFAULT_SEED if args.seed is None else args.seed
     # chained timing at further batch sizes from the same stack (activation rows sliced)
-    extra_b = [b for b in args.chained_batches if b != B] if not (args.grouped_only or wl.groups) else []
+    extra_b = [b for b in args.chained_batches if b != B] if not args.grouped_only else []
     Bmax = max([B] + extra_b)
     mats = build_stack(wl, Bmax, dev, seed, args.layers)
     full_x = [m["x"] for m in mats]
@@ -633,9 +636,6 @@ def main():
     # launch starts after the previous one ends, as when each product feeds
     # the next): the per-token latency of the named per-product call.
     ms_chain = float("nan")
-    if wl.groups and not args.grouped_only and B > 1:
-        log("the grouped format runs at batch 1 only: timing the grouped execution")
-        args.grouped_only = True
     chained_more = {}
     if not args.grouped_only:
         g = capture(mats, B, ws, stream)
@@ -648,7 +648,7 @@ def main():
             del gb_
             chained_more[str(b)] = {"us_per_token": round(ms_b * 1e3, 2),
                                     "gbs": round(token_bytes / (ms_b * 1e-3) / 1e9, 1),
-                                    "kernel": kernel_name(b, e4m3=wl.resid == "e4m3")}
+                                    "kernel": kernel_name(b, e4m3=wl.resid == "e4m3", g128=bool(wl.groups))}
             log(f"{wl.name} B={b} chained: {ms_b * 1e3:.1f} us/token, {chained_more[str(b)]['gbs']} GB/s")
     gbs_chain = token_bytes / (ms_chain * 1e-3) / 1e9
     log(f"{wl.name} B={B} chained: {ms_chain * 1e3:.1f} us/token, {gbs_chain:.1f} GB/s "

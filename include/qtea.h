@@ -160,10 +160,13 @@ int qtea_pack_e4m3(const int8_t* trits, int64_t N, int64_t K, const uint16_t* ro
  *   other arguments          as qtea_pack_e4m3
  *   packed                   >= qtea_packed_bytes_g128(...)
  *
- * A matrix in this layout runs at batch 1: through qtea_gemv (or
- * qtea_gemm_lowbatch with batch 1) and the grouped entry points; a larger
- * batch answers QTEA_ERR_BATCH.  qtea_debug_unpack returns its codes as
- * [N][26 ceil(K/128)], group after group.
+ * A matrix in this layout runs through the batch-1 table kernel (the per-
+ * group scale and bias are applied as each group's table sums are added):
+ * at batch B, qtea_gemm_lowbatch and the grouped entry points run the B
+ * activation rows one after another (B batch-1 launches, or B batch-1
+ * problems in one grouped launch), so its weights are streamed once per
+ * row.  qtea_debug_unpack returns its codes as [N][26 ceil(K/128)], group
+ * after group.
  */
 int qtea_packed_bytes_g128(int64_t N, int64_t K, int64_t n_salient, int64_t* out_bytes);
 int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* group_scale,
@@ -184,7 +187,7 @@ int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* gr
  * completion leaves the counters at zero again, so one workspace serves any
  * sequence of stream-ordered calls.  Calls that may overlap in time must
  * not share a workspace.  Errors: QTEA_ERR_INVALID_ARG, QTEA_ERR_BATCH
- * (batch outside 1..16, or above 1 for the grouped format), QTEA_ERR_HIP.
+ * (batch outside 1..16), QTEA_ERR_HIP.
  */
 int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes);
 
@@ -273,7 +276,8 @@ int qtea_debug_unpack(const qtea_desc* desc, const void* packed, uint8_t* canon_
  * at one batch size (each W_m packed by qtea_pack or, all of them,
  * qtea_pack_e4m3; the same operation as qtea_gemm_lowbatch applied to every
  * problem) in one persistent launch.  Matrices packed by qtea_pack_g128 run
- * here at batch 1 (QTEA_ERR_BATCH for a larger batch).  The problems' packed bytes are
+ * here as one batch-1 problem per activation row (the plan and its info
+ * count those problems, at batch 1).  The problems' packed bytes are
  * streamed back to back: a workgroup already loads the next problem's
  * weights while it finishes the current one.  No problem may read another
  * problem's output (all activations must be ready when the launch starts);
@@ -302,7 +306,9 @@ typedef struct qtea_grouped_info {
   int64_t workspace_bytes; /* workspace needed by qtea_grouped_gemv      */
 } qtea_grouped_info;
 
-/* Size of the device plan buffer for n_problems problems on the current device. */
+/* Size of the device plan buffer for n_problems problems at any batch size
+ * on the current device (room for QTEA_MAX_BATCH rows per problem of the
+ * grouped format).  QTEA_ERR_INVALID_ARG for n_problems outside 1..2^24. */
 int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes);
 
 /*

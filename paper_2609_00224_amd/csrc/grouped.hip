@@ -887,10 +887,11 @@ int scratch_on_current_device(void** out, hipStream_t st) {
 extern "C" {
 
 int qtea_grouped_plan_bytes(int n_problems, int64_t* out_bytes) {
-  if (!out_bytes || n_problems < 1) return QTEA_ERR_INVALID_ARG;
+  if (!out_bytes || n_problems < 1 || n_problems > (1 << 24)) return QTEA_ERR_INVALID_ARG;
   const int G = grid_size();
   if (G < 1) return QTEA_ERR_HIP;
-  *out_bytes = plan_bytes_for(n_problems, G);
+  // room for the grouped format at any batch: one batch-1 problem per row
+  *out_bytes = plan_bytes_for(n_problems * QTEA_MAX_BATCH, G);
   return QTEA_OK;
 }
 
@@ -904,12 +905,37 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   const int st_plan = qtea_grouped_plan_bytes(n_problems, &cap);
   if (st_plan != QTEA_OK) return st_plan;
   if (plan_bytes < cap) return QTEA_ERR_WORKSPACE;
+  // The grouped format at batch B: one batch-1 problem per activation row
+  // (row b of problem m reads x_m + b K_m and writes y_m + b N_m), so that
+  // its per-group scales and biases stay in the table kernel.
+  std::vector<qtea_desc> d_rows;
+  std::vector<const void*> p_rows;
+  std::vector<const uint16_t*> x_rows;
+  std::vector<float*> y_rows;
+  if (descs[0].layout == kLayoutG128 && batch > 1) {
+    for (int m = 0; m < n_problems; ++m) {
+      if (!x[m] || !y[m]) return QTEA_ERR_INVALID_ARG;
+      for (int b = 0; b < batch; ++b) {
+        d_rows.push_back(descs[m]);
+        p_rows.push_back(packed[m]);
+        x_rows.push_back(x[m] + int64_t(b) * descs[m].K);
+        y_rows.push_back(y[m] + int64_t(b) * descs[m].N);
+      }
+    }
+    descs = d_rows.data();
+    packed = p_rows.data();
+    x = x_rows.data();
+    y = y_rows.data();
+    n_problems *= batch;
+    batch = 1;
+  }
   // batch 1: the table kernel, two workgroups per CU and the chunk queue;
   // batch 2..16: the matrix-core kernel, one workgroup per CU and one
   // static run of units each
   const int G = batch > 1 ? cu_count() : grid_size();
   if (G < 1) return QTEA_ERR_HIP;
   const int64_t need = plan_bytes_for(n_problems, G);
+  if (need > cap) return QTEA_ERR_WORKSPACE;
   uint8_t* hbuf = static_cast<uint8_t*>(malloc(size_t(need)));
   if (!hbuf) return QTEA_ERR_INVALID_ARG;
   const int rc = plan_write(descs, packed, x, y, n_problems, batch, G, grouped_mma_rows_per_panel(), hbuf, need,
@@ -930,9 +956,10 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
 int qtea_workspace_bytes(const qtea_desc* desc, int batch, int64_t* out_bytes) {
   if (!out_bytes || !desc_ok(desc)) return QTEA_ERR_INVALID_ARG;
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
-  if (desc->layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;  // the grouped format runs at batch 1
+  // the grouped format runs its batch rows one after another through the
+  // batch-1 kernel: the batch-1 workspace serves every batch
   OneShape o;
-  if (!one_shape(*desc, batch, &o)) return QTEA_ERR_HIP;
+  if (!one_shape(*desc, desc->layout == kLayoutG128 ? 1 : batch, &o)) return QTEA_ERR_HIP;
   *out_bytes = o.ws_bytes;
   return QTEA_OK;
 }
@@ -941,13 +968,18 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
                        float* Y, void* workspace, int64_t workspace_bytes, void* stream) {
   if (!desc_ok(desc) || !packed || !X || !Y || !offsets_fit(*desc)) return QTEA_ERR_INVALID_ARG;
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
-  if (desc->layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;
+  const bool rows = desc->layout == kLayoutG128;  // grouped format: one batch-1 launch per row
   OneShape o;
-  if (!one_shape(*desc, batch, &o)) return QTEA_ERR_HIP;
+  if (!one_shape(*desc, rows ? 1 : batch, &o)) return QTEA_ERR_HIP;
   if (!workspace || workspace_bytes < o.ws_bytes) return QTEA_ERR_WORKSPACE;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  return one_launch(*desc, packed, X, batch, Y, o, reinterpret_cast<uint32_t*>(ws),
-                    reinterpret_cast<float*>(ws + o.off_part), static_cast<hipStream_t>(stream));
+  for (int b = 0; b < (rows ? batch : 1); ++b) {
+    const int rc = one_launch(*desc, packed, X + b * desc->K, rows ? 1 : batch, Y + b * desc->N, o,
+                              reinterpret_cast<uint32_t*>(ws), reinterpret_cast<float*>(ws + o.off_part),
+                              static_cast<hipStream_t>(stream));
+    if (rc != QTEA_OK) return rc;
+  }
+  return QTEA_OK;
 }
 
 int qtea_gemv(const qtea_desc* desc, const void* packed, const uint16_t* x, float* y, void* workspace,
@@ -959,9 +991,9 @@ int qtea_gemm_lowbatch_noalloc(const qtea_desc* desc, const void* packed, const 
                                void* stream) {
   if (!desc_ok(desc) || !packed || !X || !Y || !offsets_fit(*desc)) return QTEA_ERR_INVALID_ARG;
   if (batch < 1 || batch > QTEA_MAX_BATCH) return QTEA_ERR_BATCH;
-  if (desc->layout == kLayoutG128 && batch != 1) return QTEA_ERR_BATCH;
+  const bool rows = desc->layout == kLayoutG128;  // grouped format: one batch-1 launch per row
   OneShape o;
-  if (!one_shape(*desc, batch, &o)) return QTEA_ERR_HIP;
+  if (!one_shape(*desc, rows ? 1 : batch, &o)) return QTEA_ERR_HIP;
   const int64_t part_bytes = o.ws_bytes - o.off_part;
   if (4 * int64_t(o.n_panels) > kNoallocCounterBytes || part_bytes > QTEA_NOALLOC_SCRATCH_BYTES - kNoallocCounterBytes)
     return QTEA_ERR_WORKSPACE;
@@ -970,8 +1002,12 @@ int qtea_gemm_lowbatch_noalloc(const qtea_desc* desc, const void* packed, const 
   const int rc = scratch_on_current_device(&p, st);
   if (rc != QTEA_OK) return rc;
   uint8_t* ws = static_cast<uint8_t*>(p);
-  return one_launch(*desc, packed, X, batch, Y, o, reinterpret_cast<uint32_t*>(ws),
-                    reinterpret_cast<float*>(ws + kNoallocCounterBytes), st);
+  for (int b = 0; b < (rows ? batch : 1); ++b) {
+    const int rc2 = one_launch(*desc, packed, X + b * desc->K, rows ? 1 : batch, Y + b * desc->N, o,
+                               reinterpret_cast<uint32_t*>(ws), reinterpret_cast<float*>(ws + kNoallocCounterBytes), st);
+    if (rc2 != QTEA_OK) return rc2;
+  }
+  return QTEA_OK;
 }
 
 int qtea_grouped_status(const void* workspace, uint32_t* flags, void* stream) {

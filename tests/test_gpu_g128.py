@@ -2,8 +2,9 @@
 with a scale and a bias per row and group, 26-byte packs, E4M3 residual
 values and a salient bitmap): packing read back bit for bit, the grouped
 batch-1 GEMV against the fp64 oracle (bit for bit on dyadic inputs, within
-the tolerance of gpu_cases on synthetic ones at the 8B shapes), and the
-entry points that do not take this layout."""
+the tolerance of gpu_cases on synthetic ones at the 8B shapes), the
+per-matrix call, and batches above one (the rows one after another
+through the batch-1 kernel)."""
 from __future__ import annotations
 
 import numpy as np
@@ -126,23 +127,63 @@ def test_g128_per_matrix_gemv_dyadic_exact():
             assert np.array_equal(y.cpu().numpy().astype(np.float64), ref), (N, K)
 
 
-def test_g128_batch_above_one_refused():
+@pytest.mark.parametrize("B", [2, 4, 16])
+def test_g128_batch_above_one_dyadic_exact(B):
+    """At batch B the grouped format runs its rows through the batch-1 table
+    kernel: per-matrix (qtea_gemm_lowbatch, B launches) and grouped (B batch-1
+    problems per matrix), bit for bit against the fp64 oracle on dyadic
+    inputs, every batch row."""
     import torch
 
     import paper_2609_00224_amd as q
 
-    c = g128_dyadic_case(1, 256, 500, 1, 10)
-    pm = gpu_pack_g128(c)
-    _report("refusals: batch 2 in the grouped format")
-    with pytest.raises(q.QteaError) as e:
-        q.qtea_workspace_bytes(pm.desc, 2)
-    assert e.value.status == q.QTEA_ERR_BATCH
-    ws = torch.zeros(1 << 22, dtype=torch.uint8, device="cuda")
-    x2 = to_dev(np.concatenate([c["x"], c["x"]]))
-    y2 = torch.empty((2, 256), dtype=torch.float32, device="cuda")
-    with pytest.raises(q.QteaError) as e:
-        q.qtea_gemm_lowbatch(pm.desc, pm.packed, x2, 2, y2, ws)
-    assert e.value.status == q.QTEA_ERR_BATCH
-    with pytest.raises(q.QteaError) as e:
-        q.plan_grouped([pm], [x2], [y2], batch=2)
-    assert e.value.status == q.QTEA_ERR_BATCH
+    cases = [g128_dyadic_case(80 + i + B, N, K, B, nS) for i, (N, K, nS) in enumerate(SHAPES[:4])]
+    mats = [gpu_pack_g128(c) for c in cases]
+    refs = [oracle_rows_g128(c, need_wmax=False)[0] for c in cases]
+    for c, pm, ref in zip(cases, mats, refs):
+        N, K = c["N"], c["K"]
+        _report(f"per-matrix lowbatch, grouped format, dyadic {N}x{K} B={B}")
+        assert ref.shape == (B, N)
+        ws = q.new_workspace(pm.desc, B)
+        assert q.qtea_workspace_bytes(pm.desc, B) == q.qtea_workspace_bytes(pm.desc, 1)
+        for _ in range(2):
+            y = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+            q.qtea_gemm_lowbatch(pm.desc, pm.packed, to_dev(c["x"]), B, y, ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(y.cpu().numpy().astype(np.float64), ref), (N, K, B)
+    _report(f"grouped, grouped format, dyadic, B={B}")
+    xs = [to_dev(c["x"]) for c in cases]
+    ys = [torch.full((B, c["N"]), float("nan"), dtype=torch.float32, device="cuda") for c in cases]
+    gp = q.plan_grouped(mats, xs, ys, batch=B)
+    assert gp.info.batch == 1 and gp.info.n_problems == B * len(cases)
+    for _ in range(2):
+        for y in ys:
+            y.fill_(float("nan"))
+        gp.run()
+        torch.cuda.synchronize()
+        for c, y, ref in zip(cases, ys, refs):
+            assert np.array_equal(y.cpu().numpy().astype(np.float64), ref), (c["N"], c["K"], B)
+    assert q.qtea_grouped_status(gp.workspace) == 0
+
+
+def test_g128_batch_4_synth_8b_shapes():
+    """The 8B layer's four shapes in the grouped format at batch 4 through
+    qtea_gemm_lowbatch, sampled rows of every batch row within tolerance."""
+    import torch
+
+    import paper_2609_00224_amd as q
+
+    shapes = [(6144, 4096), (4096, 4096), (28672, 4096), (4096, 14336)]
+    rng = np.random.default_rng(1)
+    for i, (N, K) in enumerate(shapes):
+        c = g128_synth_case(6, N, K, 4, mat=i)
+        _report(f"per-matrix lowbatch, grouped format, synth {N}x{K} B=4")
+        pm = gpu_pack_g128(c)
+        y = torch.full((4, N), float("nan"), dtype=torch.float32, device="cuda")
+        q.qtea_gemm_lowbatch(pm.desc, pm.packed, to_dev(c["x"]), 4, y, q.new_workspace(pm.desc, 4))
+        torch.cuda.synchronize()
+        rows = np.unique(np.concatenate([np.arange(64), np.arange(N - 64, N), rng.choice(N, 256, replace=False)]))
+        ref, wmax = oracle_rows_g128(c, rows=rows)
+        got = y.cpu().numpy()[:, rows]
+        assert_close(got, ref, c["x"], wmax, f"g128 B=4 {N}x{K}")
+        assert_precise(got, ref, f"g128 B=4 {N}x{K}")
