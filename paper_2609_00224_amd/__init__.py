@@ -22,6 +22,11 @@ from dataclasses import dataclass
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqtea.so")
+# The debug build (QTEA_DEBUG=1 in the environment when the library is
+# loaded): every decode table's rows for the byte values 243..255, which no
+# base-3 code takes, read NaN, so a corrupted packed byte shows as NaN in
+# its output row.  Same ABI.
+DEBUG_LIB_PATH = os.path.join(HERE, "libqtea_debug.so")
 
 QTEA_OK = 0
 QTEA_ERR_INVALID_ARG = -1
@@ -92,11 +97,21 @@ class QteaError(RuntimeError):
 _lib = None
 
 
-def load(path: str = LIB_PATH):
-    """Load the HIP library; raises if it has not been built."""
+def load(path: str = None):
+    """Load the HIP library (the debug build when QTEA_DEBUG=1); raises if it
+    has not been built."""
     global _lib
     if _lib is not None:
         return _lib
+    if path is None:
+        path = DEBUG_LIB_PATH if os.environ.get("QTEA_DEBUG") == "1" else LIB_PATH
+    _lib = open_library(path)
+    return _lib
+
+
+def open_library(path: str):
+    """Open one build of the library with the argument types of every entry
+    point (load() keeps one as the binding's library)."""
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built (run __graft_entry__.build()); "
                           "there is no fallback path")
@@ -150,7 +165,6 @@ def load(path: str = LIB_PATH):
     lib.qtea_quantize.restype = i32
     lib.qtea_quantize.argtypes = [vp, vp, i64, i64, ctypes.POINTER(QteaQuantParams),
                                   vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, vp]
-    _lib = lib
     return lib
 
 

@@ -10,6 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRCS = [os.path.join(HERE, "csrc", f) for f in ("qtea.hip", "grouped.hip", "grouped_mma.hip", "quant.hip")]
 LIB = os.path.join(HERE, "libqtea.so")
+# the debug build: unused byte values 243..255 of every decode table read NaN
+LIB_DEBUG = os.path.join(HERE, "libqtea_debug.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -24,16 +26,18 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, debug: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *SRCS]
+    out = LIB_DEBUG if debug else LIB
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [hipcc, *HIPCC_FLAGS, *(["-DQTEA_DEBUG=1"] if debug else []), "-I", os.path.join(ROOT, "include"),
+           "-o", tmp, *SRCS]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, debug="--debug" in sys.argv))

@@ -50,7 +50,16 @@ using namespace qtea_grouped;
 constexpr int kGT = 512;                                  // threads per workgroup
 constexpr int kGW = kGT / 64;                             // waves per workgroup
 constexpr int kWgPerCu = 2;                               // workgroups sharing a CU
-constexpr int kTabBytes = kCodes * 256;                   // 62,208: code row = 64 packs x 4 bytes
+// Table rows: one per code (code row = 64 packs x 4 bytes, 62,208 bytes).
+// The debug build (QTEA_DEBUG) also gives the unused byte values 243..255
+// rows, filled with NaN: a packed byte that is no base-3 code then turns
+// its output row into NaN instead of reading other LDS data.
+#ifdef QTEA_DEBUG
+constexpr int kTabRows = 256;
+#else
+constexpr int kTabRows = kCodes;
+#endif
+constexpr int kTabBytes = kTabRows * 256;
 // salient columns of a slice staged per wave (more: direct loads): fp16
 // values fill the wave's 1 KiB value area at 16 columns, E4M3 values at 32
 constexpr int kResCols = 16;
@@ -81,7 +90,9 @@ struct GLds {
 static_assert(GLds<4>::TPW == 1 && GLds<8>::TPW == 2, "one or two tiles per wave");
 static_assert(2 * kResCols * 32 == 1024 && 2 * kResCols8 * 16 == 1024,
               "one 16-byte load per lane stages two tiles' values");
+#ifndef QTEA_DEBUG
 static_assert(kWgPerCu * GLds<8>::BYTES <= 160 * 1024, "two workgroups per CU");
+#endif
 
 
 
@@ -151,6 +162,12 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   extern __shared__ float smem[];
   char* lds = reinterpret_cast<char*>(smem);
   float* rres = reinterpret_cast<float*>(lds + L::RR);
+#ifdef QTEA_DEBUG
+  // rows of the byte values 243..255: NaN, never overwritten (ordered before
+  // the first lookups by the first table build's barrier)
+  for (int i = threadIdx.x; i < (256 - kCodes) * 64; i += kGT)
+    reinterpret_cast<uint32_t*>(lds + kCodes * 256)[i] = 0x7fc00000u;
+#endif
   int* flag = reinterpret_cast<int*>(lds + L::FLAG);
 
   const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);

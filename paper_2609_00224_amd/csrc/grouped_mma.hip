@@ -55,12 +55,20 @@ constexpr int kMW = kMT / 64;             // waves: one 64-row tile each
 constexpr int kMRP = kMW * 64;            // rows per panel
 constexpr int kMu = 10;                   // MFMAs per group unit and column block
 constexpr int kRowStride = 256;           // bytes per code in the digit 0-3 table (32 copies x 8)
-constexpr int kTab = kCodes * kRowStride; // 62,208 bytes
+// Rows of both decode tables: one per code; the debug build (QTEA_DEBUG)
+// adds rows for the unused byte values 243..255 filled with fp16 NaN, so a
+// packed byte that is no base-3 code makes its output rows NaN.
+#ifdef QTEA_DEBUG
+constexpr int kTabRows = 256;
+#else
+constexpr int kTabRows = kCodes;
+#endif
+constexpr int kTab = kTabRows * kRowStride; // 62,208 bytes (65,536 in the debug build)
 // Digit-4 table: code c, copy k at kTab + c * 128 + 4 k, half the digit 0-3
 // entry's address plus a constant (one shift per byte).  Its reads have a
 // 4-byte stride across a half-wave; a table at the digit 0-3 entry's own
 // address (8-byte stride) takes twice as long per 2-byte read.
-constexpr int kT4Bytes = kCodes * 128;
+constexpr int kT4Bytes = kTabRows * 128;
 constexpr int kImg = kMu * 64 * 16;       // one B-operand image (10 MFMAs x 64 lanes x 16 bytes)
 constexpr float kBigScale = 1.0f / 65536.0f;
 
@@ -306,6 +314,12 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     }
     __syncthreads();  // the first images overwrite the computed copy
   }
+#ifdef QTEA_DEBUG
+  for (int i = tid; i < (256 - kCodes) * 64; i += kMT)  // the rows of byte values 243..255 of both tables
+    reinterpret_cast<uint32_t*>(lds + kCodes * kRowStride)[i] = 0x7e007e00u;
+  for (int i = tid; i < (256 - kCodes) * 32; i += kMT)
+    reinterpret_cast<uint32_t*>(lds + L::T4OFF + kCodes * 128)[i] = 0x7e007e00u;
+#endif
   if (tid < 3) bigf[tid] = 0;
   __syncthreads();  // flags cleared before the first images can set one
 

@@ -39,6 +39,16 @@ def test_every_declared_symbol_is_exported(lib):
         ctypes.cast(getattr(lib, name), ctypes.c_void_p)
 
 
+def test_debug_build_exports_the_same_symbols():
+    """libqtea_debug.so (QTEA_DEBUG) has the same ABI as the library."""
+    if not os.path.exists(q.DEBUG_LIB_PATH):
+        pytest.fail("libqtea_debug.so is not built: run __graft_entry__.build()")
+    dbg = q.open_library(q.DEBUG_LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(dbg, name), name
+    assert dbg.qtea_abi_version() == q.QTEA_ABI_VERSION
+
+
 def test_abi_version_and_status_strings(lib):
     hdr = open(os.path.join(ROOT, "include", "qtea.h")).read()
     assert int(re.search(r"#define QTEA_ABI_VERSION (\d+)", hdr).group(1)) == q.QTEA_ABI_VERSION
