@@ -581,31 +581,43 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 }
 
 // Sums the parts of the split panels of a one-problem launch in run order
-// (deterministic): one workgroup per (panel, batch row), four consecutive
-// rows per thread, eight parts' loads in flight.  Part slot k holds [batch
-// row][kMRP] floats: slot 2k the part of run k that starts at the run's
-// first unit, 2k + 1 a part starting later in the run (only the first run
-// of a panel can).
-__global__ __launch_bounds__(kMRP / 4) void one_reduce_kernel(const GOne one, const float* __restrict__ part, int grid) {
+// (deterministic): one workgroup per (panel, batch row), kRedGroups groups of
+// 256 threads; group h sums parts ga + h, ga + h + kRedGroups, ... (four
+// consecutive rows per thread, eight parts' loads in flight), and the groups'
+// sums are added in group order.  Part slot k holds [batch row][kMRP]
+// floats: slot 2k the part of run k that starts at the run's first unit,
+// 2k + 1 a part starting later in the run (only the first run of a panel
+// can).
+constexpr int kRedGroups = 4;
+__global__ __launch_bounds__(kMRP / 4 * kRedGroups) void one_reduce_kernel(const GOne one,
+                                                                          const float* __restrict__ part,
+                                                                          int grid) {
+  __shared__ f32x4 gsum[kRedGroups - 1][kMRP / 4];
   const int panel = blockIdx.x, b = blockIdx.y, B = one.batch;
   const int64_t U = one.n_units, G = grid, ns = one.pr.n_slices, p0 = int64_t(panel) * ns;
   const int ga = one_owner(p0, U, G), gb = one_owner(p0 + ns - 1, U, G);
   if (ga == gb) return;  // one run holds the panel: its rows of y were written by that run
   const int odd0 = one_first(ga, U, G) < p0 ? 1 : 0;
-  const int row = 4 * threadIdx.x;
+  const int v = threadIdx.x % (kMRP / 4), h = threadIdx.x / (kMRP / 4);
+  const int row = 4 * v;
   f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int k0 = ga; k0 <= gb; k0 += 8) {
+  for (int k0 = ga + h; k0 <= gb; k0 += 8 * kRedGroups) {
     f32x4 t[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int k = min(k0 + j, gb);
+      const int k = min(k0 + j * kRedGroups, gb);
       const int64_t slot = 2 * int64_t(k) + (k == ga ? odd0 : 0);
       t[j] = *reinterpret_cast<const f32x4*>(part + (slot * B + b) * kMRP + row);
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j)
-      if (k0 + j <= gb) sum += t[j];
+      if (k0 + j * kRedGroups <= gb) sum += t[j];
   }
+  if (h > 0) gsum[h - 1][v] = sum;
+  __syncthreads();
+  if (h > 0) return;
+#pragma unroll
+  for (int i = 0; i < kRedGroups - 1; ++i) sum += gsum[i][v];
   const int64_t r = int64_t(panel) * kMRP + row;
   if (r < one.pr.N) {  // N % 4 == 0: the four rows are all in or all out
     float* y = one.pr.y + int64_t(b) * one.pr.N + r;
@@ -652,7 +664,8 @@ hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint3
   for (int p = 0; p < one.pr.n_panels && !split; ++p)
     split = one_owner(p * ns, one.n_units, grid) != one_owner(p * ns + ns - 1, one.n_units, grid);
   if (!split) return hipSuccess;
-  hipLaunchKernelGGL(one_reduce_kernel, dim3(one.pr.n_panels, one.batch), dim3(kMRP / 4), 0, st, one, part, grid);
+  hipLaunchKernelGGL(one_reduce_kernel, dim3(one.pr.n_panels, one.batch), dim3(kMRP / 4 * kRedGroups), 0, st, one,
+                     part, grid);
   return hipGetLastError();
 }
 
