@@ -171,7 +171,7 @@ def traffic_per_launch(kernel, algorithmic_bytes, workload="llama3_8b_stack batc
     import hashlib
 
     path = os.path.join(ROOT, "profiles", "traffic_grouped_gemv_b1_llama3_8b_stack.txt")
-    srcs = ["grouped.hip", "grouped_plan.h", "qtea_internal.h"]
+    srcs = ["grouped.hip", "grouped_plan.h", "plan_host.h", "qtea_internal.h"]
     if not os.path.exists(path):
         return None
     kv = {}

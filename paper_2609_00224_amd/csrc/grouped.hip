@@ -193,10 +193,16 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   const int G = ONE ? int(gridDim.x) : H->n_wg, NC = ONE ? int(gridDim.x) : H->n_chunks;
   // Chunks g and g + G are this workgroup's first two; every later chunk is
   // taken from the queue counters[0] (2G + the count before the increment)
-  // at the first unit of a chunk, one chunk ahead of need.  The next chunk's
-  // record is loaded at the top of every unit and first used after the
-  // table build's barrier, so a chunk switch does not wait for it.  (ONE:
-  // one run per workgroup, nothing taken.)
+  // while the current chunk runs, for the chunk after the next one, as late
+  // as the prefetch allows: each unit loads the next unit's operands, so the
+  // chunk after chunk c must be known at the top of c's last unit, and a take
+  // is issued at the top of a unit and published at its last barrier.  The
+  // take is made at the current chunk's second-to-last unit (at its only unit
+  // for a one-unit chunk): taking at a chunk's first unit instead fixes the
+  // large early chunks to workgroups at the start, and the launch ends less
+  // evenly.  The next chunk's record is loaded at the top of every unit and
+  // first used after the table build's barrier, so a chunk switch does not
+  // wait for it.  (ONE: one run per workgroup, nothing taken.)
   const uint32_t n_grabs = ONE ? 0u : uint32_t(H->n_grabs);
   const uint64_t exit_sum = ONE ? 0u : H->exit_sum;
   if (!ONE && g >= NC) {
@@ -399,7 +405,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   int pstart_slice = cur.slice;     // first slice of the open panel part
   bool part_at_chunk_start = true;  // the open panel part began at its chunk's first unit
   bool chunk_first = true;
-  int ctaken = NC;  // chunk taken at the current chunk's first unit (NC: none)
+  int ctaken = NC;  // chunk after the next one, taken while the current chunk runs (NC: none)
 
   for (int it = 0;; ++it) {
     const GProblem& pr = PR(cur.m);
@@ -414,8 +420,9 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       pstart_slice = cur.slice;
       part_at_chunk_start = chunk_first;
     }
-    // at a chunk's first unit, take the chunk after the next one from the queue
-    const bool take = !ONE && chunk_first && cn < NC;
+    // at the chunk's second-to-last unit (its only unit for a one-unit
+    // chunk), take the chunk after the next one from the queue
+    const bool take = !ONE && cn < NC && (ue - u == 2 || (chunk_first && ue - u == 1));
     uint32_t taken = 0;
     if (take && tid == 0) taken = __hip_atomic_fetch_add(counters, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int col0 = cur.slice * kSliceCols;

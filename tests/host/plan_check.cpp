@@ -302,8 +302,9 @@ void check_plan(const std::vector<Mat>& mats, int batch, int G, const char* what
 
 // ---------------------------------------------------------------------------
 // The chunk queue of the batch-1 kernel, step by step.  Workgroup g starts
-// chunk g and has chunk g + G next; at the first unit of every chunk that
-// has a next one it takes a ticket t from word 0 (chunk 2G + t if t is below
+// chunk g and has chunk g + G next; once during every chunk that has a next
+// one (in the kernel: at its second-to-last unit) it takes a ticket t
+// from word 0 (chunk 2G + t if t is below
 // the plan's count, else none, and a stale flag); when it has no next chunk
 // it adds (1 << 48) + (the tags of the chunks it ran) to the exit word, and
 // the exit that makes the count (top 16 bits) a multiple of G checks the
