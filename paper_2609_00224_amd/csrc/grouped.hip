@@ -753,16 +753,13 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 constexpr int kRedBatch = 8;
 
 template <int RP>
-__global__ __launch_bounds__(RP / 4) void grouped_reduce_kernel(const uint8_t* __restrict__ plan,
+__global__ __launch_bounds__(RP / 4) void grouped_reduce_kernel(const GSplit* __restrict__ splits, const int B,
                                                                 const float* __restrict__ part) {
   typedef float f32x4 __attribute__((ext_vector_type(4)));
-  const GPlanHeader* H = reinterpret_cast<const GPlanHeader*>(plan);
-  const GProblem* P = reinterpret_cast<const GProblem*>(plan + kPlanProblemsOff);
-  const GSplit sd = reinterpret_cast<const GSplit*>(plan + H->off_splits)[blockIdx.x];
-  const int B = H->batch;
+  // the split record is the only load before the parts' (it names y)
+  const GSplit sd = splits[blockIdx.x];
+  if (sd.y == nullptr) return;  // no record (a launch wider than the plan's split count)
   const int row = 4 * threadIdx.x;
-  const GProblem& pr = P[sd.m];
-  const int64_t r = int64_t(sd.panel) * RP + row;
   for (int b = 0; b < B; ++b) {  // a part's partial rows: [batch row][RP]
     f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
     for (int k0 = sd.ga; k0 <= sd.gb; k0 += kRedBatch) {
@@ -777,10 +774,10 @@ __global__ __launch_bounds__(RP / 4) void grouped_reduce_kernel(const uint8_t* _
       for (int j = 0; j < kRedBatch; ++j)
         if (k0 + j <= sd.gb) sum += t[j];
     }
-    float* y = pr.y + int64_t(b) * pr.N;
+    float* y = sd.y + int64_t(b) * sd.ystride;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      if (r + i < pr.N) y[r + i] = sum[i];
+      if (row + i < sd.rows) y[row + i] = sum[i];
   }
 }
 
@@ -821,15 +818,15 @@ int grid_size() {
 }
 
 template <int RB, bool F8, bool G128 = false>
-hipError_t launch_grouped(const uint8_t* plan, int grid, int n_splits, float* part, uint32_t* counters,
-                          hipStream_t st) {
+hipError_t launch_grouped(const uint8_t* plan, int grid, const GSplit* splits, int n_splits, float* part,
+                          uint32_t* counters, hipStream_t st) {
   const hipError_t e = set_lds_attr<RB, F8, G128>();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((grouped_gemv_kernel<RB, F8, G128>), dim3(grid), dim3(kGT), GLds<RB>::BYTES, st, plan,
                      part, counters, GOne{});
   if (n_splits > 0) {
     constexpr int RP = GLds<RB>::RP;
-    hipLaunchKernelGGL(grouped_reduce_kernel<RP>, dim3(n_splits), dim3(RP / 4), 0, st, plan, part);
+    hipLaunchKernelGGL(grouped_reduce_kernel<RP>, dim3(n_splits), dim3(RP / 4), 0, st, splits, 1, part);
   }
   return hipGetLastError();
 }
@@ -1053,6 +1050,11 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws);
   float* part = reinterpret_cast<float*>(ws + kAlign);
   const uint8_t* pl = static_cast<const uint8_t*>(plan);
+  if (info->n_problems < 1 || info->grid < 1 || info->grid > kMaxPlanGrid || info->n_split_panels < 0 ||
+      info->n_split_panels > kMaxChunksPerWg * info->grid)
+    return QTEA_ERR_INVALID_ARG;
+  // the split records, where the planner put them for this plan's shape
+  const GSplit* splits = reinterpret_cast<const GSplit*>(pl + plan_off_splits(info->n_problems, info->grid));
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (info->layout != kLayout && info->layout != kLayoutE4M3 && info->layout != kLayoutG128)
     return QTEA_ERR_INVALID_ARG;
@@ -1063,24 +1065,25 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
     if (info->rows_per_panel != grouped_mma_rows_per_panel()) return QTEA_ERR_INVALID_ARG;
     e = launch_grouped_mma(pl, info->grid, info->batch, f8, part, st);
     if (e == hipSuccess && info->n_split_panels > 0) {
-      hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, pl, part);
+      hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, splits,
+                         info->batch, part);
       e = hipGetLastError();
     }
     return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
   }
   if (g128) {
     switch (info->rows_per_panel) {
-      case GLds<4>::RP: e = launch_grouped<4, true, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
-      case GLds<8>::RP: e = launch_grouped<8, true, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+      case GLds<4>::RP: e = launch_grouped<4, true, true>(pl, info->grid, splits, info->n_split_panels, part, counters, st); break;
+      case GLds<8>::RP: e = launch_grouped<8, true, true>(pl, info->grid, splits, info->n_split_panels, part, counters, st); break;
       default: return QTEA_ERR_INVALID_ARG;
     }
     return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;
   }
   switch (info->rows_per_panel * (f8 ? -1 : 1)) {
-    case GLds<4>::RP: e = launch_grouped<4, false>(pl, info->grid, info->n_split_panels, part, counters, st); break;
-    case GLds<8>::RP: e = launch_grouped<8, false>(pl, info->grid, info->n_split_panels, part, counters, st); break;
-    case -GLds<4>::RP: e = launch_grouped<4, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
-    case -GLds<8>::RP: e = launch_grouped<8, true>(pl, info->grid, info->n_split_panels, part, counters, st); break;
+    case GLds<4>::RP: e = launch_grouped<4, false>(pl, info->grid, splits, info->n_split_panels, part, counters, st); break;
+    case GLds<8>::RP: e = launch_grouped<8, false>(pl, info->grid, splits, info->n_split_panels, part, counters, st); break;
+    case -GLds<4>::RP: e = launch_grouped<4, true>(pl, info->grid, splits, info->n_split_panels, part, counters, st); break;
+    case -GLds<8>::RP: e = launch_grouped<8, true>(pl, info->grid, splits, info->n_split_panels, part, counters, st); break;
     default: return QTEA_ERR_INVALID_ARG;
   }
   return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;

@@ -104,10 +104,15 @@ static_assert(sizeof(GChunk) == 32, "one scalar load per chunk record");
 
 // A panel whose slices fall in more than one chunk: its parts are in the
 // partial slots of chunks ga..gb (slot 2k, except 2ga + 1 when the part in
-// chunk ga starts after that chunk's first unit).
+// chunk ga starts after that chunk's first unit).  y is the panel's first
+// output row of batch row 0, rows the panel's rows that are rows of y, and
+// ystride the batch-row stride of y (N): the reduce kernel needs no other
+// record.  m is the problem's index in the plan.
 struct GSplit {
-  int32_t m, panel, ga, gb, ga_odd, reserved[3];
+  float* y;
+  int32_t rows, ystride, ga, gb, ga_odd, m;
 };
+static_assert(sizeof(GSplit) == 32, "one scalar load per split record");
 
 // Rows per panel of the batch-1 kernel are kRowsPerRB times its row blocks
 // per wave (4 or 8); the matrix-core kernel's panel height is its own.
@@ -187,11 +192,17 @@ inline bool one_shape_for(const qtea_desc& d, int batch, int max_wg, int rp, One
   return true;
 }
 
-// Bytes of the plan of n_problems problems for a launch of G workgroups.
+// Layout of the plan of n_problems problems for a launch of G workgroups:
+// header, problem records, chunk records from plan_off_chunks, split
+// records from plan_off_splits, plan_bytes_for bytes in all.
+inline int64_t plan_off_chunks(int n_problems) {
+  return align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
+}
+inline int64_t plan_off_splits(int n_problems, int G) {
+  return plan_off_chunks(n_problems) + align_up(int64_t(sizeof(GChunk)) * kMaxChunksPerWg * G, kAlign);
+}
 inline int64_t plan_bytes_for(int n_problems, int G) {
-  const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
-  return align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign) +
-         align_up(int64_t(sizeof(GChunk)) * max_chunks, kAlign) + int64_t(sizeof(GSplit)) * max_chunks;
+  return plan_off_splits(n_problems, G) + int64_t(sizeof(GSplit)) * kMaxChunksPerWg * G;
 }
 
 // The plan of a grouped launch, written into hbuf (hbytes bytes, at least
@@ -233,8 +244,7 @@ inline int plan_write(const qtea_desc* descs, const void* const* packed, const u
   const int RP = mma ? mma_rows : kRowsPerRB * RB;
 
   const int64_t max_chunks = int64_t(kMaxChunksPerWg) * G;
-  const int64_t off_chunks = align_up(kPlanProblemsOff + int64_t(sizeof(GProblem)) * n_problems, kAlign);
-  const int64_t off_splits = off_chunks + align_up(int64_t(sizeof(GChunk)) * max_chunks, kAlign);
+  const int64_t off_chunks = plan_off_chunks(n_problems), off_splits = plan_off_splits(n_problems, G);
   GPlanHeader* H = reinterpret_cast<GPlanHeader*>(hbuf);
   GProblem* P = reinterpret_cast<GProblem*>(hbuf + kPlanProblemsOff);
   GChunk* chunks = reinterpret_cast<GChunk*>(hbuf + off_chunks);
@@ -341,7 +351,11 @@ inline int plan_write(const qtea_desc* descs, const void* const* packed, const u
       const auto rb = ranges.begin(), re = ranges.begin() + n_chunks + 1;
       const int ga = int(std::upper_bound(rb, re, p0) - rb) - 1;
       const int gb = int(std::lower_bound(rb, re, p1) - rb) - 1;
-      if (gb > ga) splits[n_splits++] = GSplit{m, p, ga, gb, p0 > ranges[size_t(ga)] ? 1 : 0, {0, 0, 0}};
+      if (gb > ga) {
+        const int64_t row0 = int64_t(p) * RP;
+        splits[n_splits++] = GSplit{P[m].y + row0, int32_t(std::min<int64_t>(RP, P[m].N - row0)), int32_t(P[m].N),
+                                    ga, gb, p0 > ranges[size_t(ga)] ? 1 : 0, m};
+      }
       max_parts = std::max(max_parts, gb - ga + 1);
     }
   }

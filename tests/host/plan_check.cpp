@@ -190,6 +190,7 @@ void check_plan(const std::vector<Mat>& mats, int batch, int G, const char* what
   CHECK(H.n_chunks >= 1 && H.n_chunks <= int64_t(kMaxChunksPerWg) * G, "%s: n_chunks %d", what, H.n_chunks);
   CHECK(H.off_chunks >= kPlanProblemsOff + int64_t(sizeof(GProblem)) * n && H.off_chunks % kAlign == 0, "off_chunks");
   CHECK(H.off_splits >= H.off_chunks + int64_t(sizeof(GChunk)) * H.n_chunks, "off_splits");
+  CHECK(H.off_splits == plan_off_splits(n, G) && H.off_chunks == plan_off_chunks(n), "%s: record offsets", what);
   CHECK(H.off_splits + int64_t(sizeof(GSplit)) * H.n_splits <= int64_t(po.buf.size()), "%s: splits past the plan",
         what);
   CHECK(H.f8 == (mats[0].layout != kLayout ? 1 : 0), "f8");
@@ -283,8 +284,10 @@ void check_plan(const std::vector<Mat>& mats, int batch, int G, const char* what
       CHECK(si < H.n_splits, "%s: a split panel has no record", what);
       const GSplit& s = S[size_t(si++)];
       const int odd = p0 > C[size_t(ga)].ub ? 1 : 0;
-      CHECK(s.m == m && s.panel == p && s.ga == ga && s.gb == gb && s.ga_odd == odd, "%s: split record of (%d, %d)",
-            what, m, p);
+      const int64_t row0 = int64_t(p) * RP;
+      CHECK(s.m == m && s.y == pr.y + row0 && s.rows == std::min<int64_t>(RP, pr.N - row0) && s.rows > 0 &&
+                s.ystride == pr.N && s.ga == ga && s.gb == gb && s.ga_odd == odd,
+            "%s: split record of (%d, %d)", what, m, p);
       // partial slots of the parts: 2k, or 2k + 1 for a part that starts
       // after its chunk's first unit; each slot holds one part
       for (int k = ga; k <= gb; ++k) {
