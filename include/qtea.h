@@ -73,7 +73,8 @@ typedef struct qtea_desc {
   int64_t n_salient;    /* |S|                                               */
   int64_t n_packs;      /* one-byte packs per row: ceil(K / 5), or 26 per
                            128-column group in layout 4                      */
-  int64_t n_groups;     /* ceil(n_packs / 16) sixteen-pack groups            */
+  int64_t n_groups;     /* ceil(n_packs / 16) sixteen-pack groups; layout 4:
+                           two per 128-column group, 13 packs each          */
   int64_t n_pad;        /* N rounded up to a multiple of 64                  */
   int64_t bytes_total;  /* size of the packed buffer in bytes                */
   int64_t off_trits, off_alpha, off_v, off_salient, off_spos, off_rval, off_ridx;

@@ -142,11 +142,14 @@ __device__ __forceinline__ constexpr uint32_t perm_sel(int k) {
 }
 
 // F8: residual values are E4M3 bytes (layouts 3, 4), else fp16 (layout 2).
-// G128: the paper's 128-column groups (layout 4): a slice is two groups, its
-// device columns 160 g + c (c < 128) the group's columns; each 16-byte unit's
-// sum is scaled by its row's alpha[r][g] as it is added, and the quarter
-// holding the first half of a group adds beta[r][g] times the group's sum
-// of x.
+// G128: the paper's 128-column groups (layout 4): a slice is two groups, a
+// group two 16-pack slots of 13 packs (65 columns each, device columns
+// 160 g + 80 h + c, c < 65); a lane's 13 bytes of a slot row are 13 bytes
+// apart from the next row's, loaded as the 16 bytes from the dword below
+// them and shifted into place (one v_alignbyte per dword), and looked up 13
+// at a time; each slot row's sum is scaled by its row's alpha[r][g] as it is
+// added, and the quarter holding the group's first slot adds beta[r][g]
+// times the group's sum of x.
 //
 // ONE: a single problem launched on its own (GOne): no plan and no queue;
 // workgroup g takes the contiguous run of units [g U / G, (g + 1) U / G), and
@@ -223,15 +226,20 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   const int gi = w * GPW + gw;  // group in the panel
   const int rtile = gw >> 4, g16 = gw & 15;
 
-  // table slot bytes of this lane: byte k of slotreg[d] = 4 * (16 q + ((4 d + k + l16) mod 16))
+  // table slot bytes of this lane: byte k of slotreg[d] = 4 * (16 q + ((4 d +
+  // k + l16) mod 16)), layout 4: mod 13 (the packs of a slot row are stored
+  // rotated by the row the same way)
+  constexpr int NLK = G128 ? kG128SlotPacks : kGroupPacks;  // lookups per 16-byte load
   uint32_t slotreg[4];
 #pragma unroll
   for (int d = 0; d < 4; ++d) {
     uint32_t r = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) r |= uint32_t(4 * (16 * q + ((4 * d + k + l16) & 15))) << (8 * k);
+    for (int k = 0; k < 4; ++k) r |= uint32_t(4 * (16 * q + (4 * d + k + l16) % NLK)) << (8 * k);
     slotreg[d] = r;
   }
+  // layout 4: this lane's slot rows start (row mod 4) bytes into their 16-byte loads
+  const uint32_t g128_sh = uint32_t((wr * 16 + l16) & 3);
 
   int u, ue;
   Cursor cur;
@@ -256,9 +264,11 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
 
   // activations: this thread stages slice column tid (kept as loaded, checked when staged)
   // real column of device column tid of slice s (layout 4: 160 device
-  // columns per 128-column group, the last 32 padding)
+  // columns per 128-column group, 80 per slot, the last 15 of a slot unused)
+  const int g128_h = (tid % 160) / kGroupCols, g128_c = (tid % 160) % kGroupCols;
+  const bool g128_in = g128_c < kG128SlotCols && kG128SlotCols * g128_h + g128_c < kScaleCols;
   auto real_col = [&](int s) -> uint32_t {
-    return G128 ? uint32_t(s * 2 * kScaleCols + kScaleCols * (tid / 160) + tid % 160)
+    return G128 ? uint32_t(s * 2 * kScaleCols + kScaleCols * (tid / 160) + kG128SlotCols * g128_h + g128_c)
                 : uint32_t(s * kSliceCols + tid);
   };
   auto load_xv = [&](const Cursor c, uint16_t& xr, uint16_t& vr) {
@@ -327,7 +337,9 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const int ng = pr.n_groups, n_tiles = int(pr.n_pad >> 6);
     const int grp = min(c.slice * kSliceGroups + q, ng - 1);
     const int tl = min(c.panel * TPP + wt + (kGW / 4) * t, n_tiles - 1);
-    return (uint32_t(tl * ng + grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks;
+    const uint32_t row = uint32_t(wr * 16 + l16);
+    return G128 ? (uint32_t(tl * ng + grp) * kTileRows + row) * kG128SlotPacks - g128_sh
+                : (uint32_t(tl * ng + grp) * kTileRows + row) * kGroupPacks;
   };
   // Table entry at LDS byte address `a`.  The kernel has no static LDS, so
   // the dynamic allocation (the tables first) starts at address 0.
@@ -336,10 +348,18 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   u32x4 W[RB];
   uint16_t xr, vr;
   load_xv(cur, xr, vr);
+  {
+    // (a buffer load: a layout-4 slot row's load is dword- but not 16-byte-aligned)
+    const GProblem& pc = PR(cur.m);
+    const __amdgpu_buffer_rsrc_t wres0 = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint8_t*>(pc.trits), 0,
+        int(uint32_t(pc.n_pad >> 6) * uint32_t(pc.n_groups) * (kTileRows * (G128 ? kG128SlotPacks : kGroupPacks))),
+        kBufferWord3);
 #pragma unroll
-  for (int t = 0; t < RB; ++t) {
-    W[t] = __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(gptr(PR(cur.m).trits) + w_off(cur, t)));
-    __builtin_amdgcn_sched_barrier(0);  // the loop's order of the weight loads
+    for (int t = 0; t < RB; ++t) {
+      W[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres0, int(w_off(cur, t)), 0, kAuxNT));
+      __builtin_amdgcn_sched_barrier(0);  // the loop's order of the weight loads
+    }
   }
   int s_lo_c, s_hi_c;  // salient range of the current unit
   {
@@ -371,7 +391,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     if (w * 64 < kSliceCols) {  // whole waves (kSliceCols is a multiple of 64)
       const GProblem& pr = PR(c.m);
       const int gcol = int(real_col(c.slice)), dcol = c.slice * kSliceCols + tid;
-      const bool xin = gcol < pr.K && (!G128 || tid % 160 < kScaleCols);
+      const bool xin = gcol < pr.K && (!G128 || g128_in);
       const float xf = xin ? h2f(xr) : 0.0f;
       const float vf = dcol < pr.n_groups * kGroupCols ? h2f(vr) : 0.0f;
       float* st = reinterpret_cast<float*>(lds + L::ST + b * L::STB);
@@ -430,7 +450,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const int rcol0 = G128 ? cur.slice * 2 * kScaleCols : col0;
     auto xcol = [&](int j) -> int {
       const int jl = j - rcol0;
-      return G128 ? (jl >= 0 && jl < 2 * kScaleCols ? 160 * (jl >> 7) + (jl & (kScaleCols - 1)) : -1) : jl;
+      return G128 ? (jl >= 0 && jl < 2 * kScaleCols ? int(g128_dcol(jl)) : -1) : jl;
     };
     const int sb = it & 1;  // staging buffer of this unit
     const float* a_lds = reinterpret_cast<const float*>(lds + L::ST + sb * L::STB);
@@ -501,10 +521,10 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     const GProblem& pn = PR(nxt.m);
     const int n_ng = pn.n_groups, n_nt = int(pn.n_pad >> 6);
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint8_t*>(pn.trits), 0, int(uint32_t(n_nt) * uint32_t(n_ng) * (kTileRows * kGroupPacks)), kBufferWord3);
+        const_cast<uint8_t*>(pn.trits), 0, int(uint32_t(n_nt) * uint32_t(n_ng) * (kTileRows * NLK)), kBufferWord3);
     const int n_grp = min(nxt.slice * kSliceGroups + q, n_ng - 1), n_t0 = nxt.panel * TPP + wt;
     const uint32_t smask = has_next ? 0xffffffffu : 0u;
-    const uint32_t lane_off = ((uint32_t(n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * kGroupPacks) & smask;
+    const uint32_t lane_off = ((uint32_t(n_grp) * kTileRows + uint32_t(wr * 16 + l16)) * NLK - (G128 ? g128_sh : 0u)) & smask;
     // (the sums restart after every panel end: a part starts right after one)
     // layout 4: the sum of x over this quarter's group, for the first
     // quarter of each group (the other adds no bias)
@@ -516,21 +536,27 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
     }
 #pragma unroll
     for (int t = 0; t < RB; ++t) {
-      const u32x4 wv = W[t];
+      u32x4 wv = W[t];
+      if constexpr (G128) {  // the slot row's 13 bytes to bytes 0..12
+        const u32x4 w0 = W[t];
+        wv = u32x4{__builtin_amdgcn_alignbyte(w0[1], w0[0], g128_sh), __builtin_amdgcn_alignbyte(w0[2], w0[1], g128_sh),
+                   __builtin_amdgcn_alignbyte(w0[3], w0[2], g128_sh), __builtin_amdgcn_alignbyte(w0[3], w0[3], g128_sh)};
+      }
       float e[16];
 #pragma unroll
       for (int d = 0; d < 4; ++d) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) e[4 * d + k] = tab_at(__builtin_amdgcn_perm(slotreg[d], wv[d], perm_sel(k)));
+        for (int k = 0; k < 4; ++k)
+          e[4 * d + k] = 4 * d + k < NLK ? tab_at(__builtin_amdgcn_perm(slotreg[d], wv[d], perm_sel(k))) : 0.0f;
       }
-      // all sixteen table reads in flight before the first add
-      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: addresses
-      __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // DS reads
-      __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);  // VALU: sums
+      // all the table reads in flight before the first add
+      __builtin_amdgcn_sched_group_barrier(0x002, NLK, 0);  // VALU: addresses
+      __builtin_amdgcn_sched_group_barrier(0x100, NLK, 0);  // DS reads
+      __builtin_amdgcn_sched_group_barrier(0x002, NLK, 0);  // VALU: sums
       if constexpr (G128) {
         float su = e[0];
 #pragma unroll
-        for (int i = 1; i < 16; ++i) su += e[i];
+        for (int i = 1; i < NLK; ++i) su += e[i];
         const float al4 = h2f(uint16_t(AB[t] & 0xffffu)), be4 = h2f(uint16_t(AB[t] >> 16));
         acc[t] = __builtin_fmaf(be4, xq, __builtin_fmaf(al4, su, acc[t]));
         AB[t] = ab_at(nxt, t);  // the next unit's, after the last use
@@ -545,7 +571,7 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
       // refill after the last read of the old bytes, into the same registers
       // (a load issued earlier would need other registers and a copy at the
       // loop edge, and the copy would wait for the load)
-      const uint32_t tile_off = (uint32_t(min(n_t0 + (kGW / 4) * t, n_nt - 1)) * uint32_t(n_ng) * (kTileRows * kGroupPacks)) & smask;
+      const uint32_t tile_off = (uint32_t(min(n_t0 + (kGW / 4) * t, n_nt - 1)) * uint32_t(n_ng) * (kTileRows * NLK)) & smask;
       if (!ONE || has_next)
         W[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, int(lane_off), int(tile_off), kAuxNT));
       __builtin_amdgcn_sched_barrier(0);

@@ -22,11 +22,23 @@ constexpr int kLayout = 2;      // residual values fp16
 constexpr int kLayoutE4M3 = 3;  // residual values FP8 E4M3 (one byte each)
 // The paper's format: per row and 128-column group a scale alpha and a bias
 // beta, the group's 128 trits in 26 one-byte packs, E4M3 residual values.
-// On the device a group takes 32 pack slots (two 16-pack groups), slots
-// 26..31 holding the all-zero code.
+// On the device a group takes two 16-pack groups ("slots"), each holding 13
+// of its packs (65 of its columns: packs 0..12, then 13..25) densely: a
+// slot's rows are 13 bytes apart, so a row and group take the paper's 26
+// bytes.  A slot still spans 80 device columns (16 x 5), the last 15 zero.
 constexpr int kLayoutG128 = 4;
 constexpr int kScaleCols = 128;  // columns per quantization group
 constexpr int kScalePacks = 26;  // packs per quantization group (25 of five columns, one of three)
+constexpr int kG128SlotPacks = 13;  // packs per 16-pack slot in layout 4
+constexpr int kG128SlotCols = 65;   // their columns
+// Layout 4: the device column of real column j (group j / 128, slot of its
+// column c = j mod 128: c / 65, column within the slot c mod 65).
+constexpr int64_t g128_dcol(int64_t j) {
+  return 2 * kGroupCols * (j / kScaleCols) + kGroupCols * ((j % kScaleCols) / kG128SlotCols) +
+         (j % kScaleCols) % kG128SlotCols;
+}
+// Layout 4: the first real column of 16-pack slot dg.
+constexpr int64_t g128_slot_col0(int64_t dg) { return kScaleCols * (dg >> 1) + kG128SlotCols * (dg & 1); }
 constexpr int64_t kAlign = 256;
 constexpr int64_t kHeaderBytes = 256;
 constexpr int kFlagOffset = 128;
@@ -45,11 +57,12 @@ struct Layout {
   int64_t total;
 };
 
-// Layout 4 differs in three regions: trits hold two 16-pack groups per
-// 128-column group; "alpha" holds u32 (alpha | beta << 16) per row and group
-// as [n_pad/64][n_groups/2][64]; v is in device column order (80 per
-// 16-pack group, zero in the padding slots).  n_packs is the paper's count
-// (26 per group).
+// Layout 4 differs in three regions: trits hold two 16-pack slots of 13
+// bytes per row and 128-column group ([n_pad/64][n_groups][64][13]);
+// "alpha" holds u32 (alpha | beta << 16) per row and group as
+// [n_pad/64][n_groups/2][64]; v is in device column order (80 per 16-pack
+// slot, zero in the unused columns).  n_packs is the paper's count (26 per
+// group).
 inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L, int layout = kLayout) {
   if (N < 4 || N % 4 != 0 || K < 1 || nS < 0 || nS > K) return false;
   if (layout != kLayout && layout != kLayoutE4M3 && layout != kLayoutG128) return false;
@@ -62,7 +75,7 @@ inline bool make_layout(int64_t N, int64_t K, int64_t nS, Layout* L, int layout 
   L->n_tiles = L->n_pad / kTileRows;
   int64_t o = kHeaderBytes;
   L->off_trits = o;
-  o = align_up(o + L->n_pad * L->n_groups * kGroupPacks, kAlign);
+  o = align_up(o + L->n_pad * L->n_groups * (g128 ? kG128SlotPacks : kGroupPacks), kAlign);
   L->off_alpha = o;
   o = align_up(o + (g128 ? 2 * L->n_pad * L->n_groups : 2 * L->n_pad), kAlign);
   L->off_v = o;

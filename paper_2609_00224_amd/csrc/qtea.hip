@@ -104,9 +104,9 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
     for (int64_t i = t0; i < nS; i += stride) o_S[i] = S[i];
   for (int64_t g = t0; g <= n_groups; g += stride) {
     // lower bound of the first column of 16-pack group g in the sorted
-    // salient list (layout 4: group g holds columns from 128 (g / 2) + 80 (g % 2))
+    // salient list (layout 4: slot g holds columns from 128 (g / 2) + 65 (g % 2))
     int64_t lo = 0, hi = nS;
-    const int64_t key = g128 ? kScaleCols * (g >> 1) + kGroupCols * (g & 1) : g * kGroupCols;
+    const int64_t key = g128 ? g128_slot_col0(g) : g * kGroupCols;
     while (lo < hi) {
       const int64_t mid = (lo + hi) / 2;
       if (S[mid] < key)
@@ -197,11 +197,12 @@ __global__ void write_header_kernel(uint8_t* packed, int64_t N, int64_t K, int64
   }
 }
 
-// Layout 4 trits: one thread per 16-byte unit (tile, 16-pack group dg, row).
-// Byte i of row l's unit holds pack slot 16 (dg % 2) + ((i + l) mod 16) of
-// quantization group dg / 2: slot p < 26 codes the group's columns
-// 5p..5p+4 (zero trits past its column 127 and past K), slots 26..31 the
-// all-zero code.
+// Layout 4 trits: one thread per 13-byte row of a slot (tile, 16-pack slot
+// dg, row l), at byte 13 ((tile n_groups + dg) 64 + l).  Byte i holds pack
+// (i + (l mod 16)) mod 13 of the slot, i.e. pack 13 (dg % 2) + that of
+// quantization group dg / 2, which codes the group's columns 5p..5p+4 (zero
+// trits past its column 127 and past K).  The rotation by the row spreads
+// the rows of a wave's lookups over the table's columns.
 __global__ void pack_trits128_kernel(const int8_t* __restrict__ trits, int64_t N, int64_t K,
                                      int64_t n_groups, int64_t n_units, uint8_t* __restrict__ out) {
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
@@ -210,33 +211,26 @@ __global__ void pack_trits128_kernel(const int8_t* __restrict__ trits, int64_t N
     const int64_t dg = (u / kTileRows) % n_groups;
     const int64_t tile = u / (kTileRows * n_groups);
     const int64_t r = tile * kTileRows + l, g = dg >> 1;
-    uint32_t w[4] = {kZeroCode4, kZeroCode4, kZeroCode4, kZeroCode4};
-    if (r < N) {
-      const int8_t* row = trits + r * K;
-      for (int i = 0; i < kGroupPacks; ++i) {
-        const int64_t p = kGroupPacks * (dg & 1) + ((i + l) & (kGroupPacks - 1));
-        if (p >= kScalePacks) continue;  // the all-zero code stays
-        uint32_t code = 0, pw = 1;
-        for (int e = 0; e < 5; ++e) {
-          const int64_t c = 5 * p + e, j = kScaleCols * g + c;
-          int t = (c < kScaleCols && j < K) ? row[j] : 0;
-          t = t < -1 ? -1 : (t > 1 ? 1 : t);  // invalid input is reported by validate_kernel
-          code += uint32_t(t + 1) * pw;
-          pw *= 3;
-        }
-        const int sh = 8 * (i & 3);
-        w[i >> 2] = (w[i >> 2] & ~(0xffu << sh)) | (code << sh);
+    uint8_t* dst = out + u * kG128SlotPacks;
+    for (int i = 0; i < kG128SlotPacks; ++i) {
+      const int64_t p = kG128SlotPacks * (dg & 1) + (i + (l & 15)) % kG128SlotPacks;
+      uint32_t code = 0, pw = 1;
+      for (int e = 0; e < 5; ++e) {
+        const int64_t c = 5 * p + e, j = kScaleCols * g + c;
+        int t = (r < N && c < kScaleCols && j < K) ? trits[r * K + j] : 0;
+        t = t < -1 ? -1 : (t > 1 ? 1 : t);  // invalid input is reported by validate_kernel
+        code += uint32_t(t + 1) * pw;
+        pw *= 3;
       }
+      dst[i] = uint8_t(code);
     }
-    const u32x4 v = {w[0], w[1], w[2], w[3]};
-    *reinterpret_cast<u32x4*>(out + u * 16) = v;
   }
 }
 
 // Layout 4 scales and rescales: (alpha | beta << 16) per row and group as
 // [n_pad/64][n_sg][64] (zero in padded rows), v in device column order
-// (column c of 16-pack group dg is slot 16 (dg % 2) + c / 5, column c % 5 of
-// that slot; zero in the padding).
+// (device column c < 65 of slot dg is the group's column 65 (dg % 2) + c;
+// zero past it).
 __global__ void pack_scales128_kernel(const uint16_t* __restrict__ alpha, const uint16_t* __restrict__ beta,
                                       const uint16_t* __restrict__ v, int64_t N, int64_t K, int64_t n_pad,
                                       int64_t n_sg, uint32_t* __restrict__ o_ab, uint16_t* __restrict__ o_v) {
@@ -249,16 +243,15 @@ __global__ void pack_scales128_kernel(const uint16_t* __restrict__ alpha, const 
   }
   for (int64_t i = t0; i < 2 * n_sg * kGroupCols; i += stride) {
     const int64_t dg = i / kGroupCols, col = i % kGroupCols;
-    const int64_t p = kGroupPacks * (dg & 1) + col / 5, c = 5 * p + col % 5;
-    const int64_t j = kScaleCols * (dg >> 1) + c;
-    o_v[i] = (p < kScalePacks && c < kScaleCols && j < K) ? v[j] : uint16_t(0);
+    const int64_t c = kG128SlotCols * (dg & 1) + col, j = kScaleCols * (dg >> 1) + c;
+    o_v[i] = (col < kG128SlotCols && c < kScaleCols && j < K) ? v[j] : uint16_t(0);
   }
 }
 
 // The vs region (u32 per device column): pass 1 copies the v bits, pass 2
 // marks every salient column with 1 + its rank among the salient columns of
 // its 320-column slice (device columns; layout 4 maps column j to device
-// column 160 (j / 128) + j % 128).
+// column g128_dcol(j)).
 __global__ void pack_vs_kernel(const uint16_t* __restrict__ o_v, int64_t n_cols, uint32_t* __restrict__ o_vs) {
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
   for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n_cols; i += stride) o_vs[i] = o_v[i];
@@ -271,7 +264,7 @@ __global__ void mark_salient_kernel(const int32_t* __restrict__ S, const int32_t
   for (int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; s < nS; s += stride) {
     const int64_t j = S[s];
     if (j < 0 || j >= K) continue;
-    const int64_t dc = g128 ? 160 * (j / kScaleCols) + j % kScaleCols : j;
+    const int64_t dc = g128 ? g128_dcol(j) : j;
     const int64_t g0 = 4 * (dc / (4 * kGroupCols));
     if (dc >= n_groups * kGroupCols || g0 > n_groups) continue;
     const int64_t rank = s - spos[g0];
@@ -351,9 +344,9 @@ __global__ void unpack_codes128_kernel(const uint8_t* __restrict__ tr, int64_t N
   for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < N * n_packs; e += stride) {
     const int64_t r = e / n_packs, pp = e % n_packs;
     const int64_t g = pp / kScalePacks, p = pp % kScalePacks;
-    const int64_t tile = r / kTileRows, l = r % kTileRows, dg = 2 * g + p / kGroupPacks;
-    const int64_t i = ((p % kGroupPacks) - l) & (kGroupPacks - 1);
-    const uint8_t c = tr[((tile * n_groups + dg) * kTileRows + l) * 16 + i];
+    const int64_t tile = r / kTileRows, l = r % kTileRows, dg = 2 * g + p / kG128SlotPacks;
+    const int64_t i = ((p % kG128SlotPacks) - (l & 15) + 2 * kG128SlotPacks) % kG128SlotPacks;
+    const uint8_t c = tr[((tile * n_groups + dg) * kTileRows + l) * kG128SlotPacks + i];
     if (canon) canon[e] = c;
     if (trits) {
       uint32_t rest = c;

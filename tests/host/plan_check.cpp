@@ -77,7 +77,7 @@ std::vector<Region> regions(const qtea_desc& d, const Layout& L) {
   const bool g128 = d.layout == uint32_t(kLayoutG128);
   const int64_t vb = d.layout == uint32_t(kLayout) ? 2 : 1;
   return {
-      {"trits", d.off_trits, d.n_pad * d.n_groups * 16},
+      {"trits", d.off_trits, d.n_pad * d.n_groups * (g128 ? kG128SlotPacks : 16)},
       {"alpha", d.off_alpha, g128 ? 4 * d.n_pad * (d.n_groups / 2) : 2 * d.n_pad},
       {"v", d.off_v, 2 * d.n_groups * 80},
       {"S", d.off_salient, 4 * d.n_salient},

@@ -115,9 +115,11 @@ def test_algorithmic_bytes_e4m3_matches_oracle():
 
 
 def test_g128_packed_bytes_and_host_checks(lib):
-    # 26 packs per 128 columns take 32 device slots; scales and biases 4 bytes per row and group
+    # 26 packs per 128 columns take 26 device bytes per row (two slots of 13);
+    # scales and biases 4 bytes per row and group
     n = q.qtea_packed_bytes_g128(4096, 4096, 205)
-    assert n % 256 == 0 and n >= 4096 * 32 * 32 + 4 * 4096 * 32
+    assert n % 256 == 0 and n >= 4096 * 32 * 26 + 4 * 4096 * 32
+    assert n < 4096 * 32 * 32 + 4 * 4096 * 32  # no padding slots
     with pytest.raises(q.QteaError) as e:
         q.qtea_packed_bytes_g128(6, 10, 0)
     assert e.value.status == q.QTEA_ERR_INVALID_ARG
