@@ -374,12 +374,19 @@ __global__ __launch_bounds__(kGT) void grouped_gemv_kernel(const uint8_t* __rest
   if (!G128) load_alpha(cur, al);
   // layout 4: (alpha | beta << 16) of row block t's row in the quarter's group, one unit ahead
   uint32_t AB[G128 ? RB : 1];
+  // through a buffer resource over the problem's scale words: the lane's
+  // part of the offset (group and row) in a register, the row block's tile
+  // (uniform) in the scalar offset, so a row block's load costs no address
+  // arithmetic per lane
   auto ab_at = [&](const Cursor c, int t) -> uint32_t {
     const GProblem& pr = PR(c.m);
     const int n_sg = pr.n_groups >> 1, n_tiles = int(pr.n_pad >> 6);
     const int sg = min(2 * c.slice + (q >> 1), n_sg - 1);
     const int tl = min(c.panel * TPP + wt + (kGW / 4) * t, n_tiles - 1);
-    return reinterpret_cast<gu32*>(gptr(pr.alpha))[(uint32_t(tl * n_sg + sg) << 6) + uint32_t(wr * 16 + l16)];
+    const __amdgpu_buffer_rsrc_t ares = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(pr.alpha), 0, int(uint32_t(n_tiles) * uint32_t(n_sg) * 256u), kBufferWord3);
+    return __builtin_amdgcn_raw_buffer_load_b32(ares, int((uint32_t(sg) * 64u + uint32_t(wr * 16 + l16)) * 4u),
+                                                int(uint32_t(tl) * uint32_t(n_sg) * 256u), 0);
   };
   if constexpr (G128) {
 #pragma unroll
