@@ -127,6 +127,26 @@ def time_graph(g, stream, reps, warmup):
     return e0.elapsed_time(e1) / reps  # ms per replay
 
 
+def time_calls(fn, stream, reps, warmup):
+    """ms per call of fn() (which enqueues one step on `stream`), called back
+    to back: `warmup` calls, a synchronize, then `reps` calls between two
+    events on the stream."""
+    import torch
+
+    with torch.cuda.stream(stream):
+        for _ in range(warmup):
+            fn()
+        stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
 def replay_spread(g, stream, reps):
     """Median, p10 and p90 of single replays, each between its own pair of
     events (a separate pass after the timed one)."""
@@ -621,14 +641,20 @@ def main():
 
     # 2. Grouped: every GEMV of the token in one launch (`value`: a throughput
     # bound for independent GEMVs, whose activations are all ready at launch).
+    # A step is one qtea_grouped_gemv call (its two kernels, no host work),
+    # called once per token as a caller would; the host stays far ahead of
+    # the device.  The same step replayed as a captured graph is reported
+    # beside it: each graph launch adds about 4 us between steps here.
     if grouped:
-        ms = time_graph(gg, stream, args.steps, args.warmup)
+        ms = time_calls(lambda: gp.run(stream=stream), stream, args.steps, args.warmup)
+        ms_graph = time_graph(gg, stream, args.steps, args.warmup)
         spread = replay_spread(gg, stream, min(args.steps, 200))
         log(f"streaming-read ceiling {ceiling:.1f} GB/s (mean of passes {ceiling_mean:.1f}), shader clock "
             f"{clock_before}")
         log(f"{wl.name} B={B} grouped: {ms * 1e3:.1f} us/token ({gp.info.n_units} units, "
-            f"{gp.info.rows_per_panel}-row panels, {gp.info.grid} workgroups); single replays "
-            f"median {spread['median']} p10 {spread['p10']} p90 {spread['p90']} us")
+            f"{gp.info.rows_per_panel}-row panels, {gp.info.grid} workgroups); as graph replays "
+            f"{ms_graph * 1e3:.1f} us; single replays median {spread['median']} p10 {spread['p10']} "
+            f"p90 {spread['p90']} us")
         if q.qtea_grouped_status(gp.workspace, stream=stream):
             raise RuntimeError("grouped GEMV reported a queue error")
 
@@ -743,6 +769,7 @@ def main():
                    "batch": B, "weight_bytes_per_token": token_bytes, "seed": seed,
                    "residual": "off" if args.residual_off else "on"},
         "us_per_token": round(ms * 1e3, 2),
+        "us_per_token_graph_replays": round(ms_graph * 1e3, 2) if grouped else None,
         "us_per_token_single_replays": spread,
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "read_ceiling": {"gbs": round(ceiling, 1), "mean_gbs": round(ceiling_mean, 1),
