@@ -44,7 +44,8 @@ def _grouped(mats, cases):
     return [y.cpu().numpy() for y in ys], gp
 
 
-SHAPES = [(256, 1000, 50), (4160, 640, 32), (64, 5, 1), (1024, 14336, 300), (192, 130, 0), (512, 4096, 205)]
+SHAPES = [(256, 1000, 50), (4160, 640, 32), (64, 5, 1), (1024, 14336, 300), (192, 130, 0), (512, 4096, 205),
+          (4, 1, 1), (12, 300, 15), (68, 129, 3)]
 
 
 def test_g128_layout_decode_bit_exact():
