@@ -339,7 +339,11 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
  * partial rows of split panels.  Zero-fill it once before the first call;
  * every call leaves the counters at zero (see qtea_grouped_status for the
  * error flags).  Calls that may overlap in time must not share a workspace.  fp32 accumulation, run-to-run
- * deterministic (parts are summed in a fixed order).
+ * deterministic (parts are summed in a fixed order).  `info` must be the
+ * record qtea_grouped_plan filled for this `plan` buffer: the launch shape
+ * and the position of the plan's split records are taken from it.  Errors:
+ * QTEA_ERR_INVALID_ARG (an info that no plan could have filled),
+ * QTEA_ERR_WORKSPACE (workspace smaller than info->workspace_bytes).
  */
 int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* workspace,
                       int64_t workspace_bytes, void* stream);
