@@ -35,7 +35,11 @@
 //     gives digits 0-3 as two fp16 pairs (the A operand pairs as they are),
 //     and a 2-byte read from a 32-copy digit-4 table at half that address
 //     gives digit 4 (one v_perm pairs two bytes' digit 4 into one operand
-//     register);
+//     register); with two column blocks (NB = 2, batch 9..16) one table of
+//     16-byte entries (digits 0-4 and a pad, 16 copies) gives all five
+//     digits in one 12-byte read per byte, and a v_perm pairs the digit-4
+//     halves (half the LDS reads; at NB = 1 this form measured slower: its
+//     entries' registers spill inside the loop);
 //   - ten MFMAs per row tile and column block: eight take digits 0-3 of two
 //     packs each, two take digit 4 of eight packs each; the B operands are
 //     per slice images in LDS, one 16-byte slot per MFMA lane (slots swizzled
@@ -74,7 +78,11 @@ constexpr float kBigScale = 1.0f / 65536.0f;
 
 template <int NB>
 struct MLds {
+  static constexpr bool E12 = NB == 2;  // one 16-byte entry per code and copy, no digit-4 table
   static constexpr int T4OFF = kTab;
+  // (E12 leaves the digit-4 region unused: with the images at the same
+  // offsets as at NB = 1 the kernel measured 5 % faster than with them moved
+  // down into it)
   static constexpr int IMG = kTab + kT4Bytes;  // [2 buffers][NB] images
   static constexpr int FLAG = IMG + 2 * NB * kImg;    // int [3]: slice needs scaling
   // the rest: the open panel part's activations at its salient columns,
@@ -90,6 +98,8 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
 typedef __attribute__((address_space(1))) const u32x2 gu32x2;
 typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+typedef unsigned int u32x3 __attribute__((ext_vector_type(3)));
+typedef __attribute__((address_space(3))) const u32x3 lds_u32x3;
 typedef __attribute__((address_space(3))) const _Float16 lds_h;
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
@@ -202,7 +212,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   const int rs = jr & 3;                     // byte rotation left after the tile's 4q
 
   // per-lane constants: table copy offset (byte 0 of lane_base), unrotation selector
-  const uint32_t lane_base = uint32_t(8 * (lane & 31));
+  const uint32_t lane_base = L::E12 ? uint32_t(16 * (lane & 15)) : uint32_t(8 * (lane & 31));
   const uint32_t sel_rot = 0x07060504u - 0x01010101u * uint32_t(rs);
 
 
@@ -307,18 +317,27 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       one_copy[3 * c + 2] = m4;
     }
     __syncthreads();
-    for (int e = tid; e < kCodes * 32; e += kMT) {
-      const int c = e >> 5, cp = e & 31;
-      *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = u32x2{one_copy[3 * c], one_copy[3 * c + 1]};
-      *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = one_copy[3 * c + 2];
+    if constexpr (L::E12) {
+      for (int e = tid; e < kCodes * 16; e += kMT) {
+        const int c = e >> 4, cp = e & 15;
+        *reinterpret_cast<u32x4*>(lds + c * kRowStride + 16 * cp) =
+            u32x4{one_copy[3 * c], one_copy[3 * c + 1], one_copy[3 * c + 2], 0u};
+      }
+    } else {
+      for (int e = tid; e < kCodes * 32; e += kMT) {
+        const int c = e >> 5, cp = e & 31;
+        *reinterpret_cast<u32x2*>(lds + c * kRowStride + 8 * cp) = u32x2{one_copy[3 * c], one_copy[3 * c + 1]};
+        *reinterpret_cast<uint32_t*>(lds + L::T4OFF + c * 128 + 4 * cp) = one_copy[3 * c + 2];
+      }
     }
     __syncthreads();  // the first images overwrite the computed copy
   }
 #ifdef QTEA_DEBUG
   for (int i = tid; i < (256 - kCodes) * 64; i += kMT)  // the rows of byte values 243..255 of both tables
     reinterpret_cast<uint32_t*>(lds + kCodes * kRowStride)[i] = 0x7e007e00u;
-  for (int i = tid; i < (256 - kCodes) * 32; i += kMT)
-    reinterpret_cast<uint32_t*>(lds + L::T4OFF + kCodes * 128)[i] = 0x7e007e00u;
+  if (!L::E12)
+    for (int i = tid; i < (256 - kCodes) * 32; i += kMT)
+      reinterpret_cast<uint32_t*>(lds + L::T4OFF + kCodes * 128)[i] = 0x7e007e00u;
 #endif
   if (tid < 3) bigf[tid] = 0;
   __syncthreads();  // flags cleared before the first images can set one
@@ -402,11 +421,21 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
         }
         u32x2 d03[8];
         uint32_t d4[4];
+        if constexpr (L::E12) {
+          u32x3 ent[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) d03[k] = *(lds_u32x2*)(size_t(ad[k]));
+          for (int k = 0; k < 8; ++k) ent[k] = *(lds_u32x3*)(size_t(ad[k]));
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          d4[k] = lds_pair((ad[2 * k] >> 1) + L::T4OFF, (ad[2 * k + 1] >> 1) + L::T4OFF);
+          for (int k = 0; k < 8; ++k) d03[k] = u32x2{ent[k].x, ent[k].y};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) d4[k] = __builtin_amdgcn_perm(ent[2 * k + 1].z, ent[2 * k].z, 0x05040100u);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) d03[k] = *(lds_u32x2*)(size_t(ad[k]));
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            d4[k] = lds_pair((ad[2 * k] >> 1) + L::T4OFF, (ad[2 * k + 1] >> 1) + L::T4OFF);
+          }
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
