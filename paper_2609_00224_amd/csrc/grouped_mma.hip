@@ -85,11 +85,14 @@ struct MLds {
   // down into it)
   static constexpr int IMG = kTab + kT4Bytes;  // [2 buffers][NB] images
   static constexpr int FLAG = IMG + 2 * NB * kImg;    // int [3]: slice needs scaling
+  // residual hit masks: u32x2 [position p][position byte t]
+  static constexpr int RMASK = FLAG + 16;
   // the rest: the open panel part's activations at its salient columns,
   // fp16 [part rank][8 NB batch rows], gathered as the slices are staged
-  static constexpr int XSAL = FLAG + 16;
-  static constexpr int XCAP = (160 * 1024 - XSAL) / (2 * 8 * NB);  // salient columns held
-  static constexpr int BYTES = XSAL + XCAP * 2 * 8 * NB;
+  static constexpr int XSAL = RMASK + 4 * 256 * 8;
+  static constexpr int XCAP = (160 * 1024 - XSAL - 256) / (2 * 8 * NB);  // salient columns held
+  static constexpr int XDUMMY = XSAL + XCAP * 2 * 8 * NB;  // a dword per lane: the stores of other columns
+  static constexpr int BYTES = XDUMMY + 256;
 };
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
@@ -269,8 +272,10 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       if (tid + kMT * i < kSliceCols * BP) {
         const float a = float(__builtin_bit_cast(_Float16, uint16_t(vr[i] & 0xffffu))) *
                         float(__builtin_bit_cast(_Float16, xr[i]));
+        // every lane stores (no branch): a column that is not gathered goes to the lane's own dummy slot
         const int rank = xbase + int(vr[i] >> 16) - 1;
-        if ((vr[i] >> 16) != 0u && rank < L::XCAP) xsal[rank * BP + pb[i]] = xr[i];
+        const bool keep = (vr[i] >> 16) != 0u && rank < L::XCAP;
+        *reinterpret_cast<uint16_t*>(lds + (keep ? L::XSAL + 2 * (rank * BP + pb[i]) : L::XDUMMY + 4 * lane)) = xr[i];
         big |= !(__builtin_fabsf(a) < 65504.0f);
         _Float16 hi, lo;
         split_hl(a * scale, hi, lo);
@@ -339,8 +344,20 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     for (int i = tid; i < (256 - kCodes) * 32; i += kMT)
       reinterpret_cast<uint32_t*>(lds + L::T4OFF + kCodes * 128)[i] = 0x7e007e00u;
 #endif
+  // Residual hit masks: entry p * 256 + t holds, for each of the four
+  // four-row groups q whose positions (2 bits each) make up the byte t,
+  // 0xffff in half q when that group's salient value sits in row p.
+  static_assert(kMT == 4 * 256, "one hit-mask entry per thread");
+  {
+    const uint32_t p = uint32_t(tid) >> 8, t = uint32_t(tid) & 255u;
+    uint32_t m[2] = {0u, 0u};
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (((t >> (2 * q)) & 3u) == p) m[q >> 1] |= 0xffffu << (16 * (q & 1));
+    *reinterpret_cast<u32x2*>(lds + L::RMASK + 8 * tid) = u32x2{m[0], m[1]};
+  }
   if (tid < 3) bigf[tid] = 0;
-  __syncthreads();  // flags cleared before the first images can set one
+  __syncthreads();  // flags cleared and masks written before the first images and residuals
 
   const bool big0 = build(0, 1.0f, 0);  // the run's first unit starts a part
   if (big0) bigf[0] = 1;
@@ -374,6 +391,11 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       pstart_slice = cur.slice;
       part_first = u == ub;
     }
+    // gather rank of the next unit's first salient column in its part (for
+    // the image build at the unit's end)
+    const int xb_n = (!has_next || nxt.slice == 0) ? 0
+                                                   : cptr(pr.spos)[nxt.slice * kSliceGroups] -
+                                                         cptr(pr.spos)[pstart_slice * kSliceGroups];
     const int sb = it & 1;
     const bool big = __builtin_amdgcn_readfirstlane(bigf[it % 3]) != 0;
     if (tid == 0) bigf[(it + 2) % 3] = 0;  // flag of the unit after next
@@ -503,6 +525,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
                  (uint32_t(tlc) * uint32_t(pr.nS) * 16u + 4u * uint32_t(jr >> 2)) * (F8 ? 1u : 2u);
       gu32* rip = gptr(pr.ridx) + uint32_t(tlc) * uint32_t(pr.nS);
       const uint32_t psh = 8u * uint32_t(jr >> 2);
+      const uint32_t rmask = uint32_t(L::RMASK) + 2048u * uint32_t(jr & 3);  // the lane's row's mask table
       const uint32_t bmask = (jr < B && jr < BP) ? 0xffffu : 0u;
       const bool gathered = s_hi - s_lo <= L::XCAP;  // uniform
       const uint16_t* xg = xsal + min(jr, BP - 1);
@@ -536,28 +559,30 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 #pragma unroll
           for (int h = 0; h < 8; ++h) xb[h] = xp[uint32_t(col[h])];
         }
-        // B: x[j][S_s] in the hi columns (j < min(B, BP)), zero elsewhere;
-        // A: the value of four-row group 4 (jr >> 2) + q in row jr & 3 only
-        _Float16 bx[8], ar[4][8];
+        // B: x[j][S_s] in the hi columns (j < min(B, BP)), zero elsewhere
+        // and past the part's last salient column (whose clamped duplicates
+        // then add nothing); A: the value of four-row group 4 (jr >> 2) + q
+        // in row jr & 3 only, masked by the hit-mask entry of the column's
+        // position byte, then paired by column
+        _Float16 bx[8];
+        u32x2 mv[8];
 #pragma unroll
         for (int h = 0; h < 8; ++h) {
           const uint32_t in = (s0 + 8 * kb + h < s_hi) ? 0xffffu : 0u;
           bx[h] = __builtin_bit_cast(_Float16, uint16_t(xb[h] & (in & bmask)));
-          const uint32_t pwh = pw[h] >> psh;
+          const u32x2 m = *(lds_u32x2*)(size_t(rmask + (__builtin_amdgcn_ubfe(pw[h], psh, 8) << 3)));
           const u32x2 hv = F8 ? e4m3x4_to_half(rv[h].x) : rv[h];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const uint32_t wd = q < 2 ? hv.x : hv.y;
-            const uint32_t val = (q & 1) ? wd >> 16 : wd & 0xffffu;
-            const uint32_t hit = (((pwh >> (2 * q)) & 3u) == uint32_t(jr & 3)) ? in : 0u;
-            ar[q][h] = __builtin_bit_cast(_Float16, uint16_t(val & hit));
-          }
+          mv[h] = u32x2{hv.x & m.x, hv.y & m.y};
         }
         const half8 Bx = {bx[0], bx[1], bx[2], bx[3], bx[4], bx[5], bx[6], bx[7]};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const half8 Ar = {ar[q][0], ar[q][1], ar[q][2], ar[q][3], ar[q][4], ar[q][5], ar[q][6], ar[q][7]};
-          C[q][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ar, Bx, C[q][0], 0, 0, 0);
+          const uint32_t sel = (q & 1) ? 0x07060302u : 0x05040100u;
+          uint32_t dw[4];
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+            dw[d] = __builtin_amdgcn_perm(q < 2 ? mv[2 * d + 1].x : mv[2 * d + 1].y, q < 2 ? mv[2 * d].x : mv[2 * d].y, sel);
+          C[q][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_half8(dw[0], dw[1], dw[2], dw[3]), Bx, C[q][0], 0, 0, 0);
         }
       }
       // 3. hi + lo, and the store: lane jr < B holds rows 16 kb + 4q + v of batch row jr
@@ -598,12 +623,7 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
     // reads of the gather array (a next unit after a part end starts a new
     // part and refills it from rank 0)
     if (pend && has_next) __syncthreads();
-    if (has_next) {
-      const int xb_n = nxt.slice == 0 ? 0
-                                      : cptr(pr.spos)[nxt.slice * kSliceGroups] -
-                                            cptr(pr.spos)[pstart_slice * kSliceGroups];
-      if (build(sb ^ 1, 1.0f, xb_n)) bigf[(it + 1) % 3] = 1;
-    }
+    if (has_next && build(sb ^ 1, 1.0f, xb_n)) bigf[(it + 1) % 3] = 1;
     __syncthreads();  // the next unit's images are complete; this unit's are free
     cur = nxt;
   }
