@@ -272,10 +272,16 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
       if (tid + kMT * i < kSliceCols * BP) {
         const float a = float(__builtin_bit_cast(_Float16, uint16_t(vr[i] & 0xffffu))) *
                         float(__builtin_bit_cast(_Float16, xr[i]));
-        // every lane stores (no branch): a column that is not gathered goes to the lane's own dummy slot
+        // every lane stores (no branch): a column that is not gathered goes
+        // to the lane's own dummy slot (fewer spills in the grouped kernel;
+        // the one-matrix kernel at NB = 2 measured faster with the branch)
         const int rank = xbase + int(vr[i] >> 16) - 1;
         const bool keep = (vr[i] >> 16) != 0u && rank < L::XCAP;
-        *reinterpret_cast<uint16_t*>(lds + (keep ? L::XSAL + 2 * (rank * BP + pb[i]) : L::XDUMMY + 4 * lane)) = xr[i];
+        if constexpr (ONE && NB == 2) {
+          if (keep) xsal[rank * BP + pb[i]] = xr[i];
+        } else {
+          *reinterpret_cast<uint16_t*>(lds + (keep ? L::XSAL + 2 * (rank * BP + pb[i]) : L::XDUMMY + 4 * lane)) = xr[i];
+        }
         big |= !(__builtin_fabsf(a) < 65504.0f);
         _Float16 hi, lo;
         split_hl(a * scale, hi, lo);
