@@ -644,11 +644,15 @@ def main():
     # A step is one qtea_grouped_gemv call (its two kernels, no host work),
     # called once per token as a caller would; the host stays far ahead of
     # the device.  The same step replayed as a captured graph is reported
-    # beside it: each graph launch adds about 4 us between steps here.
+    # beside it: each graph launch adds about 4 us between steps here.  The
+    # graph replays and their spread are measured first, so that the calls
+    # of `value` (its own warmup, then the timed steps) run a few dozen steps
+    # into the token's load: the shader clock dips when this load follows
+    # another one and recovers over about a hundred steps.
     if grouped:
-        ms = time_calls(lambda: gp.run(stream=stream), stream, args.steps, args.warmup)
         ms_graph = time_graph(gg, stream, args.steps, args.warmup)
         spread = replay_spread(gg, stream, min(args.steps, 200))
+        ms = time_calls(lambda: gp.run(stream=stream), stream, args.steps, args.warmup)
         log(f"streaming-read ceiling {ceiling:.1f} GB/s (mean of passes {ceiling_mean:.1f}), shader clock "
             f"{clock_before}")
         log(f"{wl.name} B={B} grouped: {ms * 1e3:.1f} us/token ({gp.info.n_units} units, "
@@ -718,7 +722,7 @@ def main():
     # Roofline of the dominant kernel.  Grouped: one launch per step moves
     # the token's bytes.  Chained: every GEMV is a launch of the same kernel,
     # so the average launch moves token_bytes / launches.  Durations come
-    # from HIP events around the graph replays above.
+    # from HIP events on the stream around the timed steps above.
     n_launch = 1 if grouped else len(mats)
     kname = kernel_name(B, grouped, gp.info.rows_per_panel if grouped else 1024, wl.resid == "e4m3",
                         bool(wl.groups))
