@@ -866,13 +866,13 @@ hipError_t launch_grouped(const uint8_t* plan, int grid, const GSplit* splits, i
 
 // Launch shape of one matrix on its own: batch 1 runs the table kernel on
 // 512-row panels, two workgroups per CU at most; batch 2..16 the matrix-core
-// kernel on its 1024-row panels, one per CU.
+// kernel on its panels (1024 rows at batch 2..8, 768 at 9..16), one per CU.
 constexpr int kOneRB = 4;
 static_assert(GLds<kOneRB>::RP == kRowsPerRB * kOneRB && GLds<kMaxRB>::RP == kRowsPerRB * kMaxRB,
               "panel heights of the planner");
 bool one_shape(const qtea_desc& d, int batch, OneShape* o) {
   return one_shape_for(d, batch, batch == 1 ? grid_size() : cu_count(),
-                       batch == 1 ? GLds<kOneRB>::RP : grouped_mma_rows_per_panel(), o);
+                       batch == 1 ? GLds<kOneRB>::RP : grouped_mma_rows_per_panel(batch), o);
 }
 
 template <bool F8, bool G128>
@@ -992,7 +992,7 @@ int qtea_grouped_plan(const qtea_desc* descs, const void* const* packed, const u
   if (need > cap) return QTEA_ERR_WORKSPACE;
   uint8_t* hbuf = static_cast<uint8_t*>(malloc(size_t(need)));
   if (!hbuf) return QTEA_ERR_INVALID_ARG;
-  const int rc = plan_write(descs, packed, x, y, n_problems, batch, G, grouped_mma_rows_per_panel(), hbuf, need,
+  const int rc = plan_write(descs, packed, x, y, n_problems, batch, G, grouped_mma_rows_per_panel(batch), hbuf, need,
                             info);
   if (rc != QTEA_OK) {
     free(hbuf);
@@ -1095,11 +1095,16 @@ int qtea_grouped_gemv(const qtea_grouped_info* info, const void* plan, void* wor
   if (g128 && info->batch != 1) return QTEA_ERR_INVALID_ARG;
   hipError_t e;
   if (info->batch > 1) {
-    if (info->rows_per_panel != grouped_mma_rows_per_panel()) return QTEA_ERR_INVALID_ARG;
+    const int rp = grouped_mma_rows_per_panel(info->batch);
+    if (info->rows_per_panel != rp || (rp != 1024 && rp != 768)) return QTEA_ERR_INVALID_ARG;
     e = launch_grouped_mma(pl, info->grid, info->batch, f8, part, st);
     if (e == hipSuccess && info->n_split_panels > 0) {
-      hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, splits,
-                         info->batch, part);
+      if (rp == 1024)
+        hipLaunchKernelGGL(grouped_reduce_kernel<1024>, dim3(info->n_split_panels), dim3(1024 / 4), 0, st, splits,
+                           info->batch, part);
+      else
+        hipLaunchKernelGGL(grouped_reduce_kernel<768>, dim3(info->n_split_panels), dim3(768 / 4), 0, st, splits,
+                           info->batch, part);
       e = hipGetLastError();
     }
     return e == hipSuccess ? QTEA_OK : QTEA_ERR_HIP;

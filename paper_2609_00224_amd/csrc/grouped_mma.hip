@@ -54,9 +54,16 @@
 namespace qtea_grouped {
 namespace {
 
-constexpr int kMT = 1024;                 // threads per workgroup (one per CU)
-constexpr int kMW = kMT / 64;             // waves: one 64-row tile each
-constexpr int kMRP = kMW * 64;            // rows per panel
+// Workgroup shape (one workgroup per CU): 1024 threads at NB = 1, 768 at
+// NB = 2, whose larger register budget (168 instead of 128 per lane) takes
+// its spills from about 40 registers to 5 (8B stack, batch 16: 827 -> 720
+// us per token; at NB = 1 the 768-thread shape, with no spills to remove,
+// lost 25 % to the fewer waves).  Each wave owns one 64-row tile.
+template <int NB>
+struct MShape {
+  static constexpr int MT = NB == 1 ? 1024 : 768;  // threads per workgroup
+  static constexpr int MRP = MT;                   // rows per panel (64 per wave)
+};
 constexpr int kMu = 10;                   // MFMAs per group unit and column block
 constexpr int kRowStride = 256;           // bytes per code in the digit 0-3 table (32 copies x 8)
 // Rows of both decode tables: one per code; the debug build (QTEA_DEBUG)
@@ -177,10 +184,11 @@ __device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
 // the arrival's round trip and one workgroup summing up to 45 parts alone
 // stood between every split panel and its output).
 template <int NB, bool F8, bool ONE = false>
-__global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
+__global__ __launch_bounds__(MShape<NB>::MT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
                                                           float* __restrict__ part,
                                                           uint32_t* __restrict__ counters, const GOne one) {
   using L = MLds<NB>;
+  constexpr int kMT = MShape<NB>::MT, kMRP = MShape<NB>::MRP;
   constexpr int BP = 8 * NB;  // batch rows per hi (or lo) column set
   extern __shared__ float smem[];
   char* lds = reinterpret_cast<char*>(smem);
@@ -353,14 +361,13 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
   // Residual hit masks: entry p * 256 + t holds, for each of the four
   // four-row groups q whose positions (2 bits each) make up the byte t,
   // 0xffff in half q when that group's salient value sits in row p.
-  static_assert(kMT == 4 * 256, "one hit-mask entry per thread");
-  {
-    const uint32_t p = uint32_t(tid) >> 8, t = uint32_t(tid) & 255u;
+  for (int e = tid; e < 4 * 256; e += kMT) {
+    const uint32_t p = uint32_t(e) >> 8, t = uint32_t(e) & 255u;
     uint32_t m[2] = {0u, 0u};
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (((t >> (2 * q)) & 3u) == p) m[q >> 1] |= 0xffffu << (16 * (q & 1));
-    *reinterpret_cast<u32x2*>(lds + L::RMASK + 8 * tid) = u32x2{m[0], m[1]};
+    *reinterpret_cast<u32x2*>(lds + L::RMASK + 8 * e) = u32x2{m[0], m[1]};
   }
   if (tid < 3) bigf[tid] = 0;
   __syncthreads();  // flags cleared and masks written before the first images and residuals
@@ -639,14 +646,15 @@ __global__ __launch_bounds__(kMT) void grouped_mma_kernel(const uint8_t* __restr
 // (deterministic): one workgroup per (panel, batch row), kRedGroups groups of
 // 256 threads; group h sums parts ga + h, ga + h + kRedGroups, ... (four
 // consecutive rows per thread, eight parts' loads in flight), and the groups'
-// sums are added in group order.  Part slot k holds [batch row][kMRP]
-// floats: slot 2k the part of run k that starts at the run's first unit,
-// 2k + 1 a part starting later in the run (only the first run of a panel
-// can).
+// sums are added in group order.  Part slot k holds [batch row][RP]
+// floats (RP rows per panel): slot 2k the part of run k that starts at the
+// run's first unit, 2k + 1 a part starting later in the run (only the first
+// run of a panel can).
 constexpr int kRedGroups = 4;
-__global__ __launch_bounds__(kMRP / 4 * kRedGroups) void one_reduce_kernel(const GOne one,
-                                                                          const float* __restrict__ part,
-                                                                          int grid) {
+template <int RP>
+__global__ __launch_bounds__(RP / 4 * kRedGroups) void one_reduce_kernel(const GOne one,
+                                                                        const float* __restrict__ part, int grid) {
+  constexpr int kMRP = RP;
   __shared__ f32x4 gsum[kRedGroups - 1][kMRP / 4];
   const int panel = blockIdx.x, b = blockIdx.y, B = one.batch;
   const int64_t U = one.n_units, G = grid, ns = one.pr.n_slices, p0 = int64_t(panel) * ns;
@@ -690,14 +698,14 @@ hipError_t launch(const uint8_t* plan, int grid, float* part, uint32_t* counters
     if (e != hipSuccess) return e;
     done = true;
   }
-  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8, ONE>), dim3(grid), dim3(kMT), MLds<NB>::BYTES, st, plan, part,
+  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8, ONE>), dim3(grid), dim3(MShape<NB>::MT), MLds<NB>::BYTES, st, plan, part,
                      counters, one);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int grouped_mma_rows_per_panel() { return kMRP; }
+int grouped_mma_rows_per_panel(int batch) { return batch <= 8 ? MShape<1>::MRP : MShape<2>::MRP; }
 
 hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8, float* part, hipStream_t st) {
   const GOne none{};
@@ -719,8 +727,12 @@ hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint3
   for (int p = 0; p < one.pr.n_panels && !split; ++p)
     split = one_owner(p * ns, one.n_units, grid) != one_owner(p * ns + ns - 1, one.n_units, grid);
   if (!split) return hipSuccess;
-  hipLaunchKernelGGL(one_reduce_kernel, dim3(one.pr.n_panels, one.batch), dim3(kMRP / 4 * kRedGroups), 0, st, one,
-                     part, grid);
+  if (one.batch <= 8)
+    hipLaunchKernelGGL(one_reduce_kernel<MShape<1>::MRP>, dim3(one.pr.n_panels, one.batch),
+                       dim3(MShape<1>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
+  else
+    hipLaunchKernelGGL(one_reduce_kernel<MShape<2>::MRP>, dim3(one.pr.n_panels, one.batch),
+                       dim3(MShape<2>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
   return hipGetLastError();
 }
 

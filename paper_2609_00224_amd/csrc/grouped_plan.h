@@ -126,7 +126,8 @@ hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8,
 // The same kernel on one problem (one.batch rows), `grid` workgroups, split
 // panels finished by their last workgroup (counters: one word per panel).
 hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint32_t* counters, hipStream_t st);
-int grouped_mma_rows_per_panel();
+// Rows per panel of the matrix-core kernel at `batch` (2..16).
+int grouped_mma_rows_per_panel(int batch);
 
 }  // namespace qtea_grouped
 
