@@ -238,8 +238,9 @@ int qtea_gemm_lowbatch(const qtea_desc* desc, const void* packed, const uint16_t
  * one GPU uses that GPU's array: calls that may overlap in time on one GPU
  * (other streams, other host threads) race and must not be made.
  * Errors as qtea_gemm_lowbatch, with QTEA_ERR_WORKSPACE for a call whose
- * workspace (qtea_workspace_bytes) would not fit the array: batch 1 always
- * fits a 256-CU device; larger batches fit when the matrix's panels do.
+ * workspace (qtea_workspace_bytes) would not fit the array: on a device of
+ * up to 256 CUs every batch fits a matrix of up to 16384 x 512 rows (one
+ * arrival counter per 512-row panel).
  */
 #define QTEA_NOALLOC_SCRATCH_BYTES (16 * 1048576 + 65536)
 int qtea_gemm_lowbatch_noalloc(const qtea_desc* desc, const void* packed, const uint16_t* X, int batch,

@@ -866,13 +866,13 @@ hipError_t launch_grouped(const uint8_t* plan, int grid, const GSplit* splits, i
 
 // Launch shape of one matrix on its own: batch 1 runs the table kernel on
 // 512-row panels, two workgroups per CU at most; batch 2..16 the matrix-core
-// kernel on its panels (1024 rows at batch 2..8, 768 at 9..16), one per CU.
+// kernel on 512-row panels, one workgroup per CU at most.
 constexpr int kOneRB = 4;
 static_assert(GLds<kOneRB>::RP == kRowsPerRB * kOneRB && GLds<kMaxRB>::RP == kRowsPerRB * kMaxRB,
               "panel heights of the planner");
 bool one_shape(const qtea_desc& d, int batch, OneShape* o) {
   return one_shape_for(d, batch, batch == 1 ? grid_size() : cu_count(),
-                       batch == 1 ? GLds<kOneRB>::RP : grouped_mma_rows_per_panel(batch), o);
+                       batch == 1 ? GLds<kOneRB>::RP : one_mma_rows_per_panel(batch), o);
 }
 
 template <bool F8, bool G128>

@@ -54,15 +54,20 @@
 namespace qtea_grouped {
 namespace {
 
-// Workgroup shape (one workgroup per CU): 1024 threads at NB = 1, 768 at
-// NB = 2, whose larger register budget (168 instead of 128 per lane) takes
-// its spills from about 40 registers to 5 (8B stack, batch 16: 827 -> 720
-// us per token; at NB = 1 the 768-thread shape, with no spills to remove,
-// lost 25 % to the fewer waves).  Each wave owns one 64-row tile.
-template <int NB>
+// Workgroup shape (one workgroup per CU; each wave owns one 64-row tile).
+// Grouped launches: 1024 threads at NB = 1, 768 at NB = 2, whose larger
+// register budget (168 instead of 128 per lane) takes its spills from about
+// 40 registers to 5 (8B stack, batch 16: 827 -> 720 us per token; at NB = 1
+// the 768-thread shape, with no spills to remove, lost 25 % to the fewer
+// waves).  One matrix on its own: 512 threads at both (256 registers, no
+// spills, and twice the panels of a short launch to spread over the CUs:
+// the 8B stack chained at batch 4 / 8 / 16 takes 2104 / 2178 / 2685 us
+// against 2406 / 2560 / 3314 with the grouped shapes; 256 threads were
+// slower again).
+template <int NB, bool ONE>
 struct MShape {
-  static constexpr int MT = NB == 1 ? 1024 : 768;  // threads per workgroup
-  static constexpr int MRP = MT;                   // rows per panel (64 per wave)
+  static constexpr int MT = ONE ? 512 : (NB == 1 ? 1024 : 768);  // threads per workgroup
+  static constexpr int MRP = MT;                                  // rows per panel (64 per wave)
 };
 constexpr int kMu = 10;                   // MFMAs per group unit and column block
 constexpr int kRowStride = 256;           // bytes per code in the digit 0-3 table (32 copies x 8)
@@ -184,11 +189,11 @@ __device__ __forceinline__ void split_hl(float a, _Float16& hi, _Float16& lo) {
 // the arrival's round trip and one workgroup summing up to 45 parts alone
 // stood between every split panel and its output).
 template <int NB, bool F8, bool ONE = false>
-__global__ __launch_bounds__(MShape<NB>::MT) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
+__global__ __launch_bounds__((MShape<NB, ONE>::MT)) void grouped_mma_kernel(const uint8_t* __restrict__ plan,
                                                           float* __restrict__ part,
                                                           uint32_t* __restrict__ counters, const GOne one) {
   using L = MLds<NB>;
-  constexpr int kMT = MShape<NB>::MT, kMRP = MShape<NB>::MRP;
+  constexpr int kMT = MShape<NB, ONE>::MT, kMRP = MShape<NB, ONE>::MRP;
   constexpr int BP = 8 * NB;  // batch rows per hi (or lo) column set
   extern __shared__ float smem[];
   char* lds = reinterpret_cast<char*>(smem);
@@ -698,14 +703,15 @@ hipError_t launch(const uint8_t* plan, int grid, float* part, uint32_t* counters
     if (e != hipSuccess) return e;
     done = true;
   }
-  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8, ONE>), dim3(grid), dim3(MShape<NB>::MT), MLds<NB>::BYTES, st, plan, part,
+  hipLaunchKernelGGL((grouped_mma_kernel<NB, F8, ONE>), dim3(grid), dim3(MShape<NB, ONE>::MT), MLds<NB>::BYTES, st, plan, part,
                      counters, one);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int grouped_mma_rows_per_panel(int batch) { return batch <= 8 ? MShape<1>::MRP : MShape<2>::MRP; }
+int grouped_mma_rows_per_panel(int batch) { return batch <= 8 ? MShape<1, false>::MRP : MShape<2, false>::MRP; }
+int one_mma_rows_per_panel(int batch) { return batch <= 8 ? MShape<1, true>::MRP : MShape<2, true>::MRP; }
 
 hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8, float* part, hipStream_t st) {
   const GOne none{};
@@ -728,11 +734,11 @@ hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint3
     split = one_owner(p * ns, one.n_units, grid) != one_owner(p * ns + ns - 1, one.n_units, grid);
   if (!split) return hipSuccess;
   if (one.batch <= 8)
-    hipLaunchKernelGGL(one_reduce_kernel<MShape<1>::MRP>, dim3(one.pr.n_panels, one.batch),
-                       dim3(MShape<1>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
+    hipLaunchKernelGGL((one_reduce_kernel<MShape<1, true>::MRP>), dim3(one.pr.n_panels, one.batch),
+                       dim3(MShape<1, true>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
   else
-    hipLaunchKernelGGL(one_reduce_kernel<MShape<2>::MRP>, dim3(one.pr.n_panels, one.batch),
-                       dim3(MShape<2>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
+    hipLaunchKernelGGL((one_reduce_kernel<MShape<2, true>::MRP>), dim3(one.pr.n_panels, one.batch),
+                       dim3(MShape<2, true>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
   return hipGetLastError();
 }
 

@@ -126,8 +126,10 @@ hipError_t launch_grouped_mma(const uint8_t* plan, int grid, int batch, bool f8,
 // The same kernel on one problem (one.batch rows), `grid` workgroups, split
 // panels finished by their last workgroup (counters: one word per panel).
 hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint32_t* counters, hipStream_t st);
-// Rows per panel of the matrix-core kernel at `batch` (2..16).
+// Rows per panel of the matrix-core kernel at `batch` (2..16): grouped
+// launches, and one matrix on its own.
 int grouped_mma_rows_per_panel(int batch);
+int one_mma_rows_per_panel(int batch);
 
 }  // namespace qtea_grouped
 

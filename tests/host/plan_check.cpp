@@ -175,9 +175,11 @@ struct Part {
   int64_t chunk, slot;
 };
 
-// rows per panel of the matrix-core kernel at batch 2..16 (its workgroup
-// shape: 1024 threads up to batch 8, 768 above)
+// rows per panel of the matrix-core kernel at batch 2..16 in a grouped
+// launch (its workgroup shape: 1024 threads up to batch 8, 768 above); one
+// matrix on its own runs 512-row panels
 int mma_rows_for(int batch) { return batch <= 8 ? 1024 : 768; }
+constexpr int kOneMmaRows = 512;
 
 void check_plan(const std::vector<Mat>& mats, int batch, int G, const char* what) {
   const int mma_rows = mma_rows_for(batch);
@@ -567,19 +569,18 @@ int main() {
   printf("ok chunk queue model (%d checks)\n", g_checks);
 
   // one matrix on its own at the library's shapes (512-row panels over up
-  // to 512 workgroups at batch 1; 1024- or 768-row panels over up to 256 at
-  // 2..16)
+  // to 512 workgroups at batch 1, over up to 256 at 2..16)
   for (const auto* sh : {s8b, s14b, s70b})
     for (int i = 0; i < 4; ++i)
       for (int layout : {kLayout, kLayoutE4M3, kLayoutG128}) {
         const Mat m{sh[i][0], sh[i][1], sh[i][1] / 20, layout};
         check_one(m, 1, 512, 512);
-        for (int b : {2, 4, 8, 9, 16}) check_one(m, b, 256, mma_rows_for(b));
+        for (int b : {2, 4, 8, 9, 16}) check_one(m, b, 256, kOneMmaRows);
         for (int wgs : {1, 3, 7, 100}) check_one(m, 1, wgs, 512);
       }
   for (const Mat& m : edge) {
     check_one(m, 1, 512, 512);
-    check_one(m, 16, 256, mma_rows_for(16));
+    check_one(m, 16, 256, kOneMmaRows);
   }
   printf("ok one-matrix runs (%d checks)\n", g_checks);
   return 0;

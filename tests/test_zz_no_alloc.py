@@ -3,8 +3,9 @@ workspace entry point it shares its kernels with (qtea_gemm_lowbatch),
 through the C ABI: the outputs are the same bit for bit (same kernels, same
 launch shape, same summation order), on two calls in a row of which the
 second has the smaller input, then the first again (the scratch's counters
-are left at zero by every completed call); a call whose workspace would not
-fit the fixed scratch is refused on the host."""
+are left at zero by every completed call); batch 16 on a large matrix fits
+the fixed scratch; a call whose workspace would not fit it is refused on the
+host."""
 from __future__ import annotations
 
 import numpy as np
@@ -57,22 +58,28 @@ def test_noalloc_matches_workspace_entry_point():
         assert np.array_equal(a, b), tag
 
 
-def test_noalloc_batch_one_large_matrix_and_refusal():
+def test_noalloc_large_matrix_batch_1_and_16_and_refusal():
     import torch
 
     import paper_2609_00224_amd as q
 
-    c = synth_case(33, 16384, 5120, 1)
+    c = synth_case(33, 16384, 5120, 16)
     pm = gpu_pack(c)
-    _report("noalloc 16384x5120 batch 1")
-    a, b = _both(pm, c["x"], 1)
-    assert np.array_equal(a, b)
-    # batch 16 over 256 units of 1024 rows needs 2 x 256 x 1024 x 16 x 4 bytes
-    # of partial rows, beyond the fixed scratch: refused before any launch
-    need = q.qtea_workspace_bytes(pm.desc, 16)
-    assert need > q.QTEA_NOALLOC_SCRATCH_BYTES
-    X = torch.zeros((16, 5120), dtype=torch.float16, device="cuda")
-    Y = torch.zeros((16, 16384), dtype=torch.float32, device="cuda")
+    for B in (1, 16):
+        _report(f"noalloc 16384x5120 batch {B}")
+        # batch 16: 2 x 256 workgroups x 512 rows x 16 x 4 bytes of partial
+        # rows, which the fixed scratch holds
+        assert q.qtea_workspace_bytes(pm.desc, B) <= q.QTEA_NOALLOC_SCRATCH_BYTES
+        a, b = _both(pm, c["x"][:B], B)
+        assert np.isfinite(a).all()
+        assert np.array_equal(a, b)
+    # 16385 panels of 512 rows need more arrival counters than the scratch
+    # keeps (4 bytes each, 65536 bytes): refused before any launch
+    tall = synth_case(34, 16385 * 512, 5, 1)
+    pt = gpu_pack(tall)
+    _report("noalloc refusal, 8389120x5 batch 1")
+    X = to_dev(tall["x"])
+    Y = torch.zeros((1, tall["trits"].shape[0]), dtype=torch.float32, device="cuda")
     with pytest.raises(q.QteaError) as e:
-        q.qtea_gemm_lowbatch_noalloc(pm.desc, pm.packed, X, 16, Y)
+        q.qtea_gemm_lowbatch_noalloc(pt.desc, pt.packed, X, 1, Y)
     assert e.value.status == q.QTEA_ERR_WORKSPACE
