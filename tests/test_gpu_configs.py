@@ -10,8 +10,9 @@ grouped call over the whole set of matrices):
 
 The 14B- and 70B-shaped stacks are taken two layers deep (every matrix shape
 of the layer at full size; the kernels see the same shapes as in the full
-stacks).  Outputs: every row of matrices up to 4096 x 14336 elements, else
-the first and last 64 rows and 1024 random rows, against the fp64 oracle
+stacks).  Outputs: every row of the single GEMV and of the single layer,
+and of the stacks' matrices up to 4096 x 14336 elements, else the first and
+last 64 rows and 1024 random rows, against the fp64 oracle
 within the tolerance of gpu_cases.  Decode: the first layer's packed codes
 and residual rows read back bit-exactly.
 """
@@ -77,8 +78,11 @@ def _stack(name, layers):
     return wl, mats
 
 
-def _sample_rows(N, K, rng):
-    if N * K <= 4096 * 14336:
+FULL_ROWS = ("gemv_4096x4096", "llama3_8b_layer")
+
+
+def _sample_rows(N, K, rng, full=False):
+    if full or N * K <= 4096 * 14336:
         return np.arange(N, dtype=np.int64)
     rnd = rng.choice(np.arange(64, N - 64), size=1024, replace=False)
     return np.unique(np.concatenate([np.arange(64), np.arange(N - 64, N), rnd])).astype(np.int64)
@@ -103,7 +107,7 @@ def test_config_grouped_parity(name, layers, B):
     worst = 0.0
     for m, x, y in zip(mats, xs, ys):
         N, K = m["N"], m["K"]
-        rows = _sample_rows(N, K, rng)
+        rows = _sample_rows(N, K, rng, full=name in FULL_ROWS)
         L = synth.layer_inputs(SEED, m["layer"], m["mat"], N, K, p0=wl.p0, frac=wl.frac, rows=rows)
         codes = oracle.pack(L["trits"])
         xh = x.cpu().numpy()
