@@ -178,7 +178,7 @@ int qtea_pack_g128(const int8_t* trits, int64_t N, int64_t K, const uint16_t* gr
 /*
  * Workspace bytes that qtea_gemv (batch = 1) / qtea_gemm_lowbatch need for
  * this matrix at this batch size on the current device.  A call splits the
- * matrix's output panels (512 rows at batch 1, 1024 above) and its K range
+ * matrix's output panels (512 rows) and its K range
  * into work units over one launch; a panel whose units fall to more than
  * one workgroup is summed from their partial rows in a fixed order, at
  * batch 1 by the last of them to arrive, at batch 2..16 by a second small
