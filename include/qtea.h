@@ -50,7 +50,8 @@ enum qtea_status {
   QTEA_ERR_BAD_TRIT = -2,    /* a trit outside {-1, 0, +1}                   */
   QTEA_ERR_BAD_RESIDUAL = -3,/* idx > 3, S not strictly increasing in [0,K),
                                 a salient bitmap that disagrees with n_salient
-                                or marks a column >= K, an E4M3 NaN value  */
+                                or marks a column >= K, an E4M3 NaN value,
+                                an fp16 residual value that is not finite */
   QTEA_ERR_BATCH = -4,       /* batch outside [1, QTEA_MAX_BATCH]            */
   QTEA_ERR_WORKSPACE = -5,   /* workspace or packed buffer too small         */
   QTEA_ERR_HIP = -6,         /* a HIP runtime call or kernel launch failed   */
@@ -104,7 +105,7 @@ int qtea_packed_bytes(int64_t N, int64_t K, int64_t n_salient, int64_t* out_byte
  *   row_scale   device fp16  [N]       alpha
  *   col_rescale device fp16  [K]       v
  *   salient     device int32 [n_salient], strictly increasing, in [0, K)
- *   resid_val   device fp16  [n_salient][N/4]   R[s][g]
+ *   resid_val   device fp16  [n_salient][N/4]   R[s][g], finite
  *   resid_idx   device uint8 [n_salient][N/4]   position of R[s][g] in rows 4g..4g+3
  *   packed      device buffer of packed_bytes >= qtea_packed_bytes(...)
  *   out_desc    host; filled on success

@@ -19,9 +19,10 @@
 // A slice whose |a| reaches the fp16 range is scaled by 2^-16 before the
 // split (and its products by 2^16 after): rare, handled on a slow path.
 //
-// Work unit = (problem, panel of 1024 rows, K slice of 4 sixteen-pack groups
+// Work unit = (problem, panel of MRP rows, K slice of 4 sixteen-pack groups
 // = 320 columns), the same units and plan as the batch-1 kernel; here one
-// 1024-thread workgroup per CU takes one contiguous run of units.  Per unit:
+// workgroup of MRP threads per CU (MShape below) takes one contiguous run of
+// units.  Per unit:
 //
 //   - each wave owns one 64-row tile of the panel: four MFMA row tiles, tile
 //     q holding rows 16m + 4q + s (m, s < 4), whose bytes are rotated by the
@@ -649,7 +650,7 @@ __global__ __launch_bounds__((MShape<NB, ONE>::MT)) void grouped_mma_kernel(cons
 
 // Sums the parts of the split panels of a one-problem launch in run order
 // (deterministic): one workgroup per (panel, batch row), kRedGroups groups of
-// 256 threads; group h sums parts ga + h, ga + h + kRedGroups, ... (four
+// RP / 4 threads; group h sums parts ga + h, ga + h + kRedGroups, ... (four
 // consecutive rows per thread, eight parts' loads in flight), and the groups'
 // sums are added in group order.  Part slot k holds [batch row][RP]
 // floats (RP rows per panel): slot 2k the part of run k that starts at the
@@ -733,12 +734,10 @@ hipError_t launch_one_mma(const GOne& one, int grid, bool f8, float* part, uint3
   for (int p = 0; p < one.pr.n_panels && !split; ++p)
     split = one_owner(p * ns, one.n_units, grid) != one_owner(p * ns + ns - 1, one.n_units, grid);
   if (!split) return hipSuccess;
-  if (one.batch <= 8)
-    hipLaunchKernelGGL((one_reduce_kernel<MShape<1, true>::MRP>), dim3(one.pr.n_panels, one.batch),
-                       dim3(MShape<1, true>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
-  else
-    hipLaunchKernelGGL((one_reduce_kernel<MShape<2, true>::MRP>), dim3(one.pr.n_panels, one.batch),
-                       dim3(MShape<2, true>::MRP / 4 * kRedGroups), 0, st, one, part, grid);
+  constexpr int RP = MShape<1, true>::MRP;
+  static_assert(MShape<2, true>::MRP == RP, "one panel height for one-matrix launches");
+  hipLaunchKernelGGL(one_reduce_kernel<RP>, dim3(one.pr.n_panels, one.batch), dim3(RP / 4 * kRedGroups), 0, st, one,
+                     part, grid);
   return hipGetLastError();
 }
 

@@ -83,8 +83,10 @@ __global__ void pack_trits_kernel(const int8_t* __restrict__ trits, int64_t N, i
 }
 
 // Scales, salient list and residual blocks.  VT is the residual value type:
-// uint16_t (fp16 bits, layout 2) or uint8_t (E4M3 bytes, layout 3; a NaN code
-// is flagged).  With S == o_S the salient list is already in place (derived
+// uint16_t (fp16 bits, layout 2; an infinity or NaN is flagged) or uint8_t
+// (E4M3 bytes, layout 3; a NaN code is flagged).  Finite values let the
+// kernels pad a part's salient columns with duplicates whose products with
+// a zero activation are exact zeros.  With S == o_S the salient list is already in place (derived
 // from a bitmap) and only read.
 template <typename VT>
 __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint16_t* __restrict__ v,
@@ -122,7 +124,7 @@ __global__ void pack_meta_kernel(const uint16_t* __restrict__ alpha, const uint1
     const int64_t tile = i / (16 * nS), rem = i - tile * 16 * nS;
     const int64_t s = rem >> 4, g = 16 * tile + (rem & 15);
     const VT val = g < G ? rval[s * G + g] : VT(0);
-    if (sizeof(VT) == 1 && e4m3_is_nan(val)) f |= kFlagBadResid;
+    if (sizeof(VT) == 1 ? e4m3_is_nan(uint8_t(val)) : (uint32_t(val) & 0x7c00u) == 0x7c00u) f |= kFlagBadResid;
     o_rval[i] = val;
   }
   if (f) atomicOr(flags, f);

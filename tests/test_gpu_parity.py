@@ -226,6 +226,13 @@ def test_error_statuses():
     with pytest.raises(q.QteaError) as e:
         gpu_pack(bad)
     assert e.value.status == q.QTEA_ERR_BAD_RESIDUAL
+    for v in (np.inf, -np.inf, np.nan):  # a residual value that is not finite
+        bad = dict(case)
+        bad["R"] = case["R"].copy()
+        bad["R"][-1, -1] = v
+        with pytest.raises(q.QteaError) as e:
+            gpu_pack(bad)
+        assert e.value.status == q.QTEA_ERR_BAD_RESIDUAL, v
     pm = gpu_pack(case)
     X = to_dev(np.zeros((17, 100), np.float16))
     Y = torch.empty((17, 64), dtype=torch.float32, device="cuda")
