@@ -64,6 +64,9 @@ def test_grouped_batch_dyadic_exact(B):
     _report(f"grouped batch {B} dyadic {DYADIC_GROUP}")
     (outs,), gp = _run_group(cases, B)
     assert gp.info.batch == B
+    # the matrix-core workgroup shape: 1024 threads (rows per panel) up to
+    # batch 8, 768 above
+    assert gp.info.rows_per_panel == (1024 if B <= 8 else 768)
     assert gp.info.n_split_panels > 0, "the group should split panels between workgroups"
     for c, y in zip(cases, outs):
         ref, _ = oracle_rows(c, need_wmax=False)
